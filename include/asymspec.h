@@ -1,0 +1,150 @@
+/*
+ * asymspec.h -- C ABI of the AsymSpec fused decision step for MI355X (gfx950).
+ *
+ * AsymSpec ("Context-Asymmetric Speculative Decoding for Agentic LLMs",
+ * arXiv 2608.26004) runs three forwards per speculative step: the drafter on
+ * the full context (logits a, drafts d_1..d_K), the same drafter on the
+ * compressed context (logits b) and the verifier on the compressed context
+ * (logits t), each at the K+1 speculated positions (Sec. 3.2; Alg. 1).  This
+ * library is the step that consumes those logits:
+ *
+ *   delta_i    = a_i - b_i                                  (Sec. 3.2, Eq. 1)
+ *   f_i        = t_i + beta * delta_i      fused logits     (Sec. 3.2, Eq. 2)
+ *   D_i        = JSD(softmax(a_i) || softmax(b_i))          (Sec. 3.3, Eq. 3)
+ *   gamma_eff  = gamma * exp(-D_i)          CDA gate        (Sec. 3.3, Eq. 3)
+ *   accept d_i iff softmax(t_i)[d_i] > gamma_eff * softmax(b_i)[d_i]  (Eq. 4)
+ *   first rejection at j: emit argmax f_j; all accepted: emit argmax t_K
+ *                                                           (Alg. 1)
+ *
+ * The paper defines the step for greedy decoding (temperature 0).  For a
+ * request with temperature tau > 0 the library uses the speculative-sampling
+ * form of the same gate: fused target p~ = softmax(f/tau), proposal
+ * q = softmax(a/tau); accept d_i iff u_i < min(1, p~(d_i) / (gamma_eff q(d_i)));
+ * at the first rejection the emitted token is an inverse-CDF draw from the
+ * residual max(0, p~ - q) with the caller uniform u_K; when all drafts pass it
+ * is an inverse-CDF draw from softmax(t_K/tau) with u_K.  With a == b and
+ * gamma = 1 this is exactly standard speculative sampling.
+ *
+ * Conventions
+ *   - Every pointer argument of asymspec_fuse_verify is a DEVICE pointer owned
+ *     by the caller.  The library allocates, frees and retains nothing on this
+ *     path; outputs are overwritten.
+ *   - Calls are asynchronous: work is enqueued on `stream` (a hipStream_t, or
+ *     NULL for the default stream) and the call returns; outputs are valid
+ *     once the stream has been synchronised.
+ *   - Errors are returned as negative status codes; argument checks happen on
+ *     the host before anything is enqueued.  No exception crosses the ABI.
+ *   - Layout: contiguous row-major; logits are [B][K+1][V] with row stride V;
+ *     any V >= 1.  Row K of a and b is never read (the bonus token of Alg. 1
+ *     uses the verifier alone).
+ *   - Masked tokens: -inf logits are allowed.  A token whose fused logit is
+ *     not a number (a = b = -inf) counts as masked.  NaN inputs otherwise give
+ *     unspecified outputs.  Every row that is read must hold a finite logit.
+ */
+#ifndef ASYMSPEC_H
+#define ASYMSPEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------- */
+#define ASYMSPEC_OK            0
+#define ASYMSPEC_E_ARG        -1  /* null pointer, size or parameter out of range */
+#define ASYMSPEC_E_ALIGN      -2  /* a pointer is not aligned as documented         */
+#define ASYMSPEC_E_WORKSPACE  -3  /* workspace smaller than asymspec_workspace_size */
+#define ASYMSPEC_E_DEVICE     -4  /* no gfx950 device current, or launch failure     */
+
+/* ---- logit storage types --------------------------------------------- */
+#define ASYMSPEC_BF16 0           /* bfloat16 bit patterns, 2 bytes per logit */
+#define ASYMSPEC_FP32 1           /* IEEE binary32, 4 bytes per logit         */
+
+/* ---- acceptance gates -------------------------------------------------- */
+#define ASYMSPEC_GATE_CDA   0     /* gamma_eff = gamma * exp(-JSD)   (Eq. 3)          */
+#define ASYMSPEC_GATE_FIXED 1     /* gamma_eff = gamma, the fixed-gamma gate the paper
+                                     compares against (App. B, "Models and
+                                     hyperparameters") */
+
+typedef struct asymspec_params {
+  float beta;        /* fusion weight of Eq. 2; finite, >= 0 (paper default 1.0) */
+  float gamma;       /* base threshold of Eq. 3-4; in (0, 1] (paper default 0.5)  */
+  int32_t gate_mode; /* ASYMSPEC_GATE_CDA or ASYMSPEC_GATE_FIXED                  */
+  uint32_t flags;    /* reserved, must be 0                                       */
+} asymspec_params;
+
+/* Bytes of device workspace asymspec_fuse_verify needs for this shape
+ * (0 for invalid arguments).  The workspace needs no initialisation and may be
+ * reused across calls of any shape: every record the kernel exchanges between
+ * workgroups is tagged with a per-call epoch.  Calls that may run at the same
+ * time need distinct workspaces. */
+size_t asymspec_workspace_size(int B, int K, int V, int dtype);
+
+/* Zero-fill a workspace on `stream` with a fill kernel (never required for
+ * correctness; useful to scrub a buffer).  Returns ASYMSPEC_OK, ASYMSPEC_E_ARG
+ * or ASYMSPEC_E_DEVICE. */
+int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * One decision step (Alg. 1, the body of the while loop after the three
+ * forwards) for B independent requests with K drafts each.
+ *
+ *   verifier_logits     t [B][K+1][V]  (dtype)          16-byte aligned
+ *   drafter_full_logits a [B][K+1][V]  (dtype)          16-byte aligned; rows 0..K-1 read
+ *   drafter_comp_logits b [B][K+1][V]  (dtype)          16-byte aligned; rows 0..K-1 read
+ *   draft_tokens        d [B][K] int32, each in [0, V)  (may be NULL when K = 0)
+ *   draft_probs         q(d) [B][K] float, or NULL: the proposal probability of
+ *                       each draft for sampling rows; NULL means softmax(a/tau)[d]
+ *                       computed here.  Unused on greedy rows.
+ *   uniforms            u [B][K+1] float in [0,1): u[b][i] (i < K) decides the
+ *                       acceptance of draft i on sampling rows, u[b][K] drives the
+ *                       emission draw.  Unused for greedy requests, but required.
+ *   temperature         tau [B] float; tau <= 0 selects greedy decoding for
+ *                       that request (the paper's setting), tau > 0 sampling.
+ *   B >= 1, K >= 0, V >= 1, B*(K+1)*V < 2^40
+ *   params              see asymspec_params (host pointer)
+ *   accept_len          [B] int32 out: number of accepted drafts, in [0, K]
+ *   next_token          [B] int32 out: the token emitted after them
+ *   fused_logprobs      [B][K+1] float out: [i] (i < K) = log p~_i(d_i), the
+ *                       fused log-probability of draft i (temperature 1 for
+ *                       greedy requests, tau for sampling ones); [K] = the
+ *                       log-probability of next_token under the distribution
+ *                       that emitted it (the fused row at the first rejection,
+ *                       or the verifier's bonus row)
+ *   gate_out            [B][K][2] float out (D_i, gamma_eff_i), or NULL
+ *   workspace           device scratch of >= asymspec_workspace_size bytes,
+ *                       256-byte aligned, contents opaque between calls
+ *   stream              hipStream_t or NULL
+ *
+ * Integer and float arrays must be 4-byte aligned.  Returns ASYMSPEC_OK or a
+ * negative status; on error nothing is enqueued.
+ */
+int asymspec_fuse_verify(const void* verifier_logits,
+                         const void* drafter_full_logits,
+                         const void* drafter_comp_logits,
+                         int dtype,
+                         const int32_t* draft_tokens,
+                         const float* draft_probs,
+                         const float* uniforms,
+                         const float* temperature,
+                         int B, int K, int V,
+                         const asymspec_params* params,
+                         int32_t* accept_len,
+                         int32_t* next_token,
+                         float* fused_logprobs,
+                         float* gate_out,
+                         void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/* Static text for a status code. */
+const char* asymspec_status_string(int status);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int asymspec_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ASYMSPEC_H */

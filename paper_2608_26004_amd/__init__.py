@@ -1,0 +1,166 @@
+"""MI355X (gfx950) implementation of the AsymSpec fused decision step.
+
+The compute lives in ``libasymspec.so`` (hand-written HIP for CDNA4); this
+module only marshals arguments: torch tensors in, device pointers and the
+current HIP stream out to the C ABI declared in ``include/asymspec.h``.
+There is no fallback: if the library is missing, every call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = ["fuse_verify", "workspace_size", "Workspace", "load_library", "status_string",
+           "BF16", "FP32", "GATE_CDA", "GATE_FIXED", "AsymSpecError"]
+
+BF16 = 0
+FP32 = 1
+GATE_CDA = 0
+GATE_FIXED = 1
+
+OK = 0
+E_ARG = -1
+E_ALIGN = -2
+E_WORKSPACE = -3
+E_DEVICE = -4
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libasymspec.so")
+_lib = None
+
+
+class AsymSpecError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"asymspec error {status}: {msg}")
+        self.status = status
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("beta", ctypes.c_float), ("gamma", ctypes.c_float),
+                ("gate_mode", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+
+def load_library(path: str | None = None):
+    """Load (once) and return the ctypes handle of libasymspec.so."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise ImportError(f"{p} is missing: build it with `python -m paper_2608_26004_amd.build` "
+                          "(hipcc --offload-arch=gfx950)")
+    lib = ctypes.CDLL(p)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    lib.asymspec_workspace_size.argtypes = [i32, i32, i32, i32]
+    lib.asymspec_workspace_size.restype = sz
+    lib.asymspec_workspace_clear.argtypes = [vp, sz, vp]
+    lib.asymspec_workspace_clear.restype = i32
+    lib.asymspec_fuse_verify.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, i32, i32, i32,
+                                         ctypes.POINTER(_Params), vp, vp, vp, vp, vp, sz, vp]
+    lib.asymspec_fuse_verify.restype = i32
+    lib.asymspec_status_string.argtypes = [i32]
+    lib.asymspec_status_string.restype = ctypes.c_char_p
+    lib.asymspec_version.argtypes = []
+    lib.asymspec_version.restype = i32
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().asymspec_status_string(status).decode()
+
+
+def workspace_size(B: int, K: int, V: int, dtype: int) -> int:
+    return int(load_library().asymspec_workspace_size(B, K, V, dtype))
+
+
+def _ptr(x):
+    return None if x is None else ctypes.c_void_p(x.data_ptr())
+
+
+def _stream_handle(device):
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+class Workspace:
+    """A zero-filled device workspace reused across calls of one shape class
+    (grows on demand).  Calls sharing one Workspace must not overlap."""
+
+    def __init__(self, device=None):
+        self.device = device
+        self.buf = None
+
+    def get(self, nbytes: int, device):
+        import torch
+        if self.buf is None or self.buf.numel() < nbytes or self.buf.device != device:
+            self.buf = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=device)
+        return self.buf
+
+
+_default_ws = {}
+
+
+def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
+                beta: float = 1.0, gamma: float = 0.5, gate_mode: int = GATE_CDA,
+                return_gate: bool = False, workspace: Workspace | None = None, out=None):
+    """One AsymSpec decision step on the current HIP stream.
+
+    t, a, b: [B, K+1, V] torch.bfloat16 or torch.float32 on the GPU
+    draft_tokens: [B, K] int32; draft_probs: [B, K] float32 or None;
+    uniforms: [B, K+1] float32; temperature: [B] float32 (<= 0: greedy).
+    Returns (accept_len [B] int32, next_token [B] int32,
+             fused_logprobs [B, K+1] float32[, gate [B, K, 2] float32])."""
+    import torch
+    lib = load_library()
+    if t.dtype == torch.bfloat16:
+        dt = BF16
+    elif t.dtype == torch.float32:
+        dt = FP32
+    else:
+        raise TypeError(f"logits must be bfloat16 or float32, got {t.dtype}")
+    if t.dim() != 3:
+        raise ValueError("logits must be [B, K+1, V]")
+    B, Kp1, V = t.shape
+    K = Kp1 - 1
+    dev = t.device
+    for name, x in (("a", a), ("b", b)):
+        if x.shape != t.shape or x.dtype != t.dtype or x.device != dev:
+            raise ValueError(f"{name} must match t in shape, dtype and device")
+    for x in (t, a, b, draft_tokens, uniforms, temperature) + ((draft_probs,) if draft_probs is not None else ()):
+        if not x.is_contiguous():
+            raise ValueError("all tensors must be contiguous")
+    if draft_tokens.dtype != torch.int32 or tuple(draft_tokens.shape) != (B, K):
+        raise ValueError("draft_tokens must be int32 [B, K]")
+    if uniforms.dtype != torch.float32 or tuple(uniforms.shape) != (B, K + 1):
+        raise ValueError("uniforms must be float32 [B, K+1]")
+    if temperature.dtype != torch.float32 or tuple(temperature.shape) != (B,):
+        raise ValueError("temperature must be float32 [B]")
+    if draft_probs is not None and (draft_probs.dtype != torch.float32 or tuple(draft_probs.shape) != (B, K)):
+        raise ValueError("draft_probs must be float32 [B, K] or None")
+    if out is None:
+        acc = torch.empty(B, dtype=torch.int32, device=dev)
+        nxt = torch.empty(B, dtype=torch.int32, device=dev)
+        flp = torch.empty(B, K + 1, dtype=torch.float32, device=dev)
+        gate = torch.empty(B, K, 2, dtype=torch.float32, device=dev) if return_gate else None
+    else:
+        acc, nxt, flp, gate = out
+    ws_bytes = workspace_size(B, K, V, dt)
+    if ws_bytes == 0:
+        raise AsymSpecError(E_ARG, "invalid shape")
+    if workspace is None:
+        workspace = _default_ws.setdefault(dev, Workspace(dev))
+    wsbuf = workspace.get(ws_bytes, dev)
+    params = _Params(float(beta), float(gamma), int(gate_mode), 0)
+    st = lib.asymspec_fuse_verify(_ptr(t), _ptr(a), _ptr(b), dt, _ptr(draft_tokens),
+                                  _ptr(draft_probs), _ptr(uniforms), _ptr(temperature),
+                                  B, K, V, ctypes.byref(params), _ptr(acc), _ptr(nxt),
+                                  _ptr(flp), _ptr(gate), _ptr(wsbuf), wsbuf.numel(),
+                                  _stream_handle(dev))
+    if st != OK:
+        raise AsymSpecError(st, status_string(st))
+    if return_gate:
+        return acc, nxt, flp, gate
+    return acc, nxt, flp

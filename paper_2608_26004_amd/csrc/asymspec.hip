@@ -1,0 +1,1219 @@
+// AsymSpec fused decision step for MI355X (gfx950, CDNA4, wave64).
+//
+// One persistent cooperative launch does the whole step of Alg. 1 for every
+// request: the vocabulary-wide statistics of the verifier logits t and the
+// drafter logits a (full view) and b (compressed view), the delta-fused logits
+// f = t + beta (a - b) (Sec. 3.2, Eq. 1-2), the Jensen-Shannon divergence D and
+// the CDA gate gamma * exp(-D) (Sec. 3.3, Eq. 3), the acceptance test (Eq. 4,
+// or its speculative-sampling form for temperature > 0), and the emission at
+// the first rejection or the bonus token.
+//
+// Work decomposition.  A logit row [V] is cut into S chunks of
+// kThreads * kNV 16-byte vectors.  A team of S workgroups owns a sequence of
+// rows; member m always takes chunk m.  Per row:
+//   pass 1   the chunk, loaded once into VGPRs, yields per-chunk max / sum-exp
+//            statistics, fused-logit argmax and an a-vs-b bitwise flag;
+//   barrier  members publish 128-byte records tagged with the launch epoch and
+//            wait for all S of the row (relaxed agent-scope loads, no cache
+//            flushes: every cross-workgroup word goes through sc1 accesses);
+//   decide   each member combines the S records and classifies the row as
+//            surely accepted / surely rejected / open, using D in [0, ln 2];
+//   pass 2   only where needed, on the still-resident chunk: the JSD term
+//            (open rows, or when the caller asks for D) and the per-wave sums
+//            of the residual max(0, p~ - q) (sampling rows that may reject) or
+//            of the bonus weights;
+//   finalize the last member to finish pass 2 (atomic counter) settles the
+//            row; the last row of a request to settle runs the request
+//            epilogue: accept_len, the inverse-CDF scan of one 2048-element
+//            segment for sampled emissions, and the outputs.
+// The next row's chunk is prefetched into a second register buffer before
+// pass 1 of the current one, so its HBM latency overlaps pass 1, the barrier
+// and pass 2.
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <chrono>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <unistd.h>
+
+#include "asymspec.h"
+
+#define DEV __device__ __forceinline__
+
+namespace asym {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kNV = 2;                         // 16-B vectors per thread per stream
+constexpr int kChunkVec = kThreads * kNV;      // vectors per chunk
+constexpr int kSegVec = 64 * kNV;              // vectors per wave segment
+constexpr float kL2E = 1.44269504088896340736f;
+constexpr double kLn2 = 0.693147180559945309417232121458;
+constexpr float kFloorM = -1.0e30f;            // start value of running maxima
+constexpr uint32_t kBf16NegInf = 0xFF80u;
+constexpr uint32_t kF32NegInf = 0xFF800000u;
+constexpr long kSpinLimit = 1L << 17;          // bounded barrier polls (~0.1 s)
+
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+enum Kind { kGreedyDraft = 0, kSampleDraft = 1, kGreedyBonus = 2, kSampleBonus = 3 };
+enum Slot { sT = 0, sA = 1, sB = 2, sF = 3, sAT = 4, kSlots = 5 };
+
+// Workspace record sizes in 32-bit words.
+constexpr int kRec1Words = 32;   // pass-1 chunk record, word 31 = epoch
+constexpr int kRec2Words = 16;   // pass-2 chunk record, word 15 = epoch
+constexpr int kRowWords = 32;    // settled row, word 31 = epoch
+
+struct KArgs {
+  const void* t; const void* a; const void* b;
+  const int32_t* d; const float* dp; const float* u; const float* tau;
+  int32_t* acc_out; int32_t* next_out; float* flp_out; float* gate_out;
+  uint32_t* rec1; uint32_t* rec2; uint32_t* rowres;
+  uint32_t* err;
+  unsigned long long stream_bytes;   // bytes of each logit array
+  int B, K, V, S, n_teams, rows;
+  float beta, gamma; int gate_mode; int want_gate;
+  double ln_gamma;
+  uint32_t epoch;
+};
+
+// ------------------------------------------------------------------ memory
+DEV void st_sc1(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+DEV uint32_t ld_sc1(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+DEV void st_sc1_d(uint32_t* p, double v) {
+  uint64_t x = __builtin_bit_cast(uint64_t, v);
+  st_sc1(p, (uint32_t)x);
+  st_sc1(p + 1, (uint32_t)(x >> 32));
+}
+DEV double ld_sc1_d(const uint32_t* p) {
+  uint64_t lo = ld_sc1(p), hi = ld_sc1(p + 1);
+  return __builtin_bit_cast(double, lo | (hi << 32));
+}
+DEV void st_sc1_f(uint32_t* p, float v) { st_sc1(p, __float_as_uint(v)); }
+DEV float ld_sc1_f(const uint32_t* p) { return __uint_as_float(ld_sc1(p)); }
+// Wait until this wave's stores are performed (s_waitcnt vmcnt(0)).
+DEV void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+DEV uint32_t atom_add(uint32_t* p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+DEV __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned long long nbytes) {
+  unsigned long long n = nbytes > 0xFFFFFFFFull ? 0xFFFFFFFFull : nbytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)(uint32_t)n, 0x00020000);
+}
+DEV u4 buf_load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+}
+
+// ------------------------------------------------------------------ decode
+template <int DT> struct Elem;
+template <> struct Elem<ASYMSPEC_BF16> {
+  static constexpr int VE = 8;
+  DEV static float get(const u4& v, int e) {
+    uint32_t w = v[e >> 1];
+    return __uint_as_float((e & 1) ? (w & 0xFFFF0000u) : (w << 16));
+  }
+  DEV static float load_one(const void* base, long long idx) {
+    uint32_t h = reinterpret_cast<const uint16_t*>(base)[idx];
+    return __uint_as_float(h << 16);
+  }
+  DEV static void mask_to_neginf(u4& v, int lo, int hi) {
+    #pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t w = v[j];
+      if (2 * j < lo || 2 * j >= hi) w = (w & 0xFFFF0000u) | kBf16NegInf;
+      if (2 * j + 1 < lo || 2 * j + 1 >= hi) w = (w & 0x0000FFFFu) | (kBf16NegInf << 16);
+      v[j] = w;
+    }
+  }
+};
+template <> struct Elem<ASYMSPEC_FP32> {
+  static constexpr int VE = 4;
+  DEV static float get(const u4& v, int e) { return __uint_as_float(v[e]); }
+  DEV static float load_one(const void* base, long long idx) {
+    return reinterpret_cast<const float*>(base)[idx];
+  }
+  DEV static void mask_to_neginf(u4& v, int lo, int hi) {
+    #pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (j < lo || j >= hi) v[j] = kF32NegInf;
+  }
+};
+
+// Fused logit of Eq. 2 in fp32, t + beta * (a - b) in that order, no
+// contraction.  A NaN (a = b = -inf) stays NaN here and is treated as masked
+// by every consumer (max ignores it, exp arguments are clamped).
+DEV float fuse(float t, float a, float b, float beta) {
+  float d = __fsub_rn(a, b);
+  return __fadd_rn(t, __fmul_rn(beta, d));
+}
+DEV float fuse_masked(float t, float a, float b, float beta) {
+  float f = fuse(t, a, b, beta);
+  return (f != f) ? -INFINITY : f;
+}
+
+// ------------------------------------------------------------- reductions
+// Wave64 reductions with gfx9 DPP patterns: xor-1 and xor-2 quad
+// permutations, half-row and row mirrors, then row_bcast15 / row_bcast31.
+// The complete result lands in lane 63 and is read back as a wave-uniform
+// value.  Must be called with all 64 lanes active.
+template <int CTRL, int ROWMASK = 0xF>
+DEV float dppf(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, x),
+                                                              __builtin_bit_cast(int, x),
+                                                              CTRL, ROWMASK, 0xF, false));
+}
+template <int CTRL, int ROWMASK = 0xF>
+DEV int dppi(int x) {
+  return __builtin_amdgcn_update_dpp(x, x, CTRL, ROWMASK, 0xF, false);
+}
+DEV float lane63f(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
+}
+DEV float wave_max(float x) {
+  x = fmaxf(x, dppf<0xB1>(x));
+  x = fmaxf(x, dppf<0x4E>(x));
+  x = fmaxf(x, dppf<0x141>(x));
+  x = fmaxf(x, dppf<0x140>(x));
+  x = fmaxf(x, dppf<0x142, 0xA>(x));
+  x = fmaxf(x, dppf<0x143, 0xC>(x));
+  return lane63f(x);
+}
+DEV float wave_sum(float x) {
+  x += dppf<0xB1>(x);
+  x += dppf<0x4E>(x);
+  x += dppf<0x141>(x);
+  x += dppf<0x140>(x);
+  x += dppf<0x142, 0xA>(x);
+  x += dppf<0x143, 0xC>(x);
+  return lane63f(x);
+}
+DEV int wave_min_i(int x) {
+  x = min(x, dppi<0xB1>(x));
+  x = min(x, dppi<0x4E>(x));
+  x = min(x, dppi<0x141>(x));
+  x = min(x, dppi<0x140>(x));
+  x = min(x, dppi<0x142, 0xA>(x));
+  x = min(x, dppi<0x143, 0xC>(x));
+  return __builtin_amdgcn_readlane(x, 63);
+}
+// fp64 wave sum over lanes (rare paths only).
+DEV double wave_sum_d(double x) {
+  #pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// ----------------------------------------------------------- row geometry
+struct RowGeo {
+  int row, req, pos, kind;
+  float tau, c;               // c = log2(e) / tau for sampling, log2(e) for greedy
+  long long e0;               // flat index of the row's first element
+  long long vbeg, vend;       // row's 16-B vector range (vend exclusive)
+};
+
+template <int DT>
+DEV RowGeo row_geo(const KArgs& A, int row) {
+  constexpr int VE = Elem<DT>::VE;
+  RowGeo g;
+  g.row = row;
+  g.req = row / (A.K + 1);
+  g.pos = row - g.req * (A.K + 1);
+  g.tau = A.tau[g.req];
+  const bool samp = g.tau > 0.0f;
+  const bool bonus = g.pos == A.K;
+  g.kind = bonus ? (samp ? kSampleBonus : kGreedyBonus) : (samp ? kSampleDraft : kGreedyDraft);
+  g.c = samp ? (kL2E / g.tau) : kL2E;
+  g.e0 = (long long)row * A.V;
+  g.vbeg = g.e0 / VE;
+  g.vend = (g.e0 + A.V + VE - 1) / VE;
+  return g;
+}
+DEV bool is_draft(int kind) { return kind == kGreedyDraft || kind == kSampleDraft; }
+
+// Loads this thread's vectors of chunk `mem` of row g into buf (t always, a
+// and b for draft rows).  Loads are bounds-checked by the buffer resource;
+// the one vector that may run past the end of an array is read by element.
+template <int DT>
+DEV void issue_loads(const KArgs& A, const RowGeo& g, int mem, u4 (&buf)[3][kNV]) {
+  constexpr int VE = Elem<DT>::VE;
+  constexpr int ES = 16 / VE;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const long long cv0 = g.vbeg + (long long)mem * kChunkVec + (long long)w * kSegVec;
+  const unsigned long long rbase = (unsigned long long)g.vbeg * 16ull;
+  const unsigned long long rem = A.stream_bytes - rbase;
+  const int ns = is_draft(g.kind) ? 3 : 1;
+  const long long last_full = (long long)(A.stream_bytes / 16ull);   // vectors fully inside
+  #pragma unroll
+  for (int s = 0; s < 3; ++s) {
+    if (s < ns) {
+      const void* src = s == 0 ? A.t : (s == 1 ? A.a : A.b);
+      __amdgpu_buffer_rsrc_t r = make_rsrc((const char*)src + rbase, rem);
+      #pragma unroll
+      for (int k = 0; k < kNV; ++k) {
+        const long long vi = cv0 + (long long)k * 64 + lane;
+        const uint32_t off = (uint32_t)((vi - g.vbeg) * 16);
+        if (vi < last_full || vi >= g.vend) {
+          buf[s][k] = buf_load(r, off);
+        } else {
+          // the array's final, partial vector: read element by element
+          u4 v = {0, 0, 0, 0};
+          const long long n_el = (long long)(A.stream_bytes / ES);
+          #pragma unroll
+          for (int e = 0; e < VE; ++e) {
+            const long long idx = vi * VE + e;
+            if (idx < n_el) {
+              const uint32_t bits = __float_as_uint(Elem<DT>::load_one(src, idx));
+              if (DT == ASYMSPEC_BF16) {
+                const uint32_t h = bits >> 16;
+                v[e >> 1] |= (e & 1) ? (h << 16) : h;
+              } else {
+                v[e] = bits;
+              }
+            }
+          }
+          buf[s][k] = v;
+        }
+      }
+    }
+  }
+}
+
+// Replace elements outside [row start, row end) by -inf (a masked token).
+template <int DT>
+DEV void sanitize(const RowGeo& g, const KArgs& A, int mem, u4 (&buf)[3][kNV]) {
+  constexpr int VE = Elem<DT>::VE;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const long long cv0 = g.vbeg + (long long)mem * kChunkVec + (long long)w * kSegVec;
+  const int ns = is_draft(g.kind) ? 3 : 1;
+  #pragma unroll
+  for (int k = 0; k < kNV; ++k) {
+    const long long first = (cv0 + (long long)k * 64 + lane) * VE;
+    const long long lo = g.e0 - first;
+    const long long hi = g.e0 + A.V - first;
+    if (lo > 0 || hi < VE) {
+      const int ilo = (int)(lo < 0 ? 0 : (lo > VE ? VE : lo));
+      const int ihi = (int)(hi < 0 ? 0 : (hi > VE ? VE : hi));
+      #pragma unroll
+      for (int s = 0; s < 3; ++s)
+        if (s < ns) Elem<DT>::mask_to_neginf(buf[s][k], ilo, ihi);
+    }
+  }
+}
+
+// Running (max, sum of exp2(x*c - R)) with R = fl(max * c), updated one
+// vector at a time; kb records the first vector that raised the maximum.
+struct Acc { float m, R, s; int kb; };
+DEV void acc_init(Acc& q, float c) { q.m = kFloorM; q.R = kFloorM * c; q.s = 0.0f; q.kb = 0; }
+
+template <int VE, bool kClampNaN>
+DEV void acc_vec(Acc& q, const float (&x)[VE], float c, int k) {
+  float vm = x[0];
+  #pragma unroll
+  for (int e = 1; e < VE; ++e) vm = fmaxf(vm, x[e]);
+  if (vm > q.m) q.kb = k;
+  const float mn = fmaxf(q.m, vm);
+  const float Rn = mn * c;
+  const float scale = __builtin_amdgcn_exp2f(q.R - Rn);
+  float ex[VE];
+  #pragma unroll
+  for (int e = 0; e < VE; ++e) {
+    float arg = __builtin_fmaf(x[e], c, -Rn);
+    if (kClampNaN) arg = fmaxf(arg, -200.0f);
+    ex[e] = __builtin_amdgcn_exp2f(arg);
+  }
+  #pragma unroll
+  for (int st = 1; st < VE; st <<= 1)
+    #pragma unroll
+    for (int e = 0; e + st < VE; e += 2 * st) ex[e] += ex[e + st];
+  q.s = __builtin_fmaf(q.s, scale, ex[0]);
+  q.m = mn;
+  q.R = Rn;
+}
+
+// Pass-2 element functions, shared by pass 2 and the epilogue scan so that
+// both see bit-identical values.
+struct ResidConst { float beta, c, Rf, isf, Rq, isq; };
+DEV float resid_elem(float t, float a, float b, const ResidConst& k) {
+  const float f = fuse(t, a, b, k.beta);
+  const float p = __builtin_amdgcn_exp2f(fmaxf(__builtin_fmaf(f, k.c, -k.Rf), -200.0f)) * k.isf;
+  const float q = __builtin_amdgcn_exp2f(__builtin_fmaf(a, k.c, -k.Rq)) * k.isq;
+  return fmaxf(p - q, 0.0f);
+}
+struct BonusConst { float c, Rt; };
+DEV float bonus_elem(float t, const BonusConst& k) {
+  return __builtin_amdgcn_exp2f(__builtin_fmaf(t, k.c, -k.Rt));
+}
+
+// log2 of a positive double to ~1e-7 absolute: exact exponent split plus the
+// hardware log2 of the mantissa.
+DEV double log2_dbl(double x) {
+  int e;
+  const double m = frexp(x, &e);            // x = m * 2^e, m in [0.5, 1)
+  return (double)e + (double)__builtin_amdgcn_logf((float)m);
+}
+DEV double ln_f(float x) { return (double)__builtin_amdgcn_logf(x) * kLn2; }
+
+// Per-row scalars, computed once by thread 0 after the team barrier.
+struct RowScal {
+  float M[kSlots], R[kSlots];
+  double S[kSlots], L2[kSlots];   // L2 = R + log2 S: log2-domain LSE at the slot scale
+  float khi[2], klo[2];           // log2 S of a and b split in two floats (JSD)
+  float isF, isQ, Rq;             // residual constants
+  int arg;                        // argmax (greedy draft: f; greedy bonus: t)
+  int neq;                        // a and b differ somewhere in the row
+  int needD, needRes, needBonus, decided, accept;
+  double margin;                  // greedy: log Eq.-4 ratio without D; sampling: x
+  double lp_d, lp_emit, lnu;
+};
+
+struct Smem {
+  float wm[kWaves][kSlots];
+  float ws[kWaves][kSlots];
+  int   warg[kWaves];
+  int   wneq[kWaves];
+  float wj[kWaves];
+  float wseg[kWaves];
+  uint32_t rec[kRec1Words];
+  RowScal rs;
+  int   flags[8];
+  double dd[8];
+  double scan[kWaves];
+};
+
+// Inclusive and exclusive prefix sums over the workgroup, in thread order.
+DEV void block_scan(double x, Smem& sm, double& incl, double& excl) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  double v = x;
+  #pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double y = __shfl_up(v, o, 64);
+    if (lane >= o) v += y;
+  }
+  double prev = __shfl_up(v, 1, 64);
+  if (lane == 0) prev = 0.0;
+  __syncthreads();
+  if (lane == 63) sm.scan[w] = v;
+  __syncthreads();
+  double off = 0.0;
+  for (int i = 0; i < w; ++i) off += sm.scan[i];
+  incl = off + v;
+  excl = off + prev;
+}
+DEV int block_min_i(int x, Smem& sm) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  x = wave_min_i(x);
+  __syncthreads();
+  if (lane == 0) sm.warg[w] = x;
+  __syncthreads();
+  int r = sm.warg[0];
+  #pragma unroll
+  for (int i = 1; i < kWaves; ++i) r = min(r, sm.warg[i]);
+  return r;
+}
+
+// Settled-row record layout (words).
+enum {
+  RW_ACCEPT = 0, RW_EMIT = 1, RW_LPD = 2, RW_LPEMIT = 3, RW_D = 4, RW_GEFF = 5,
+  RW_C = 6, RW_R1 = 7, RW_IS1 = 8, RW_R2 = 9, RW_IS2 = 10, RW_KIND = 11,
+  RW_L2P = 12 /* double, 12-13 */, RW_TOTAL = 14 /* double, 14-15 */
+};
+
+// Lane 0 of wave 0: decide the row from the combined statistics (Eq. 3-4 or
+// the sampling form) given D, write the settled-row record, then its epoch.
+template <int DT>
+DEV void write_row_t0(const KArgs& A, const RowGeo& g, const RowScal& rs, double D, double total) {
+  bool accept = rs.accept != 0;
+  const bool cda = A.gate_mode == ASYMSPEC_GATE_CDA;
+  if (!rs.decided) {
+    if (g.kind == kGreedyDraft) accept = (rs.margin + (cda ? D : 0.0)) > 0.0;
+    else if (g.kind == kSampleDraft) accept = rs.lnu < rs.margin + (cda ? D : 0.0);
+  }
+  const double geff = cda ? (double)A.gamma * (double)__builtin_amdgcn_exp2f((float)(-D * 1.4426950408889634)) : (double)A.gamma;
+  uint32_t* rw = A.rowres + (size_t)g.row * kRowWords;
+  st_sc1(rw + RW_ACCEPT, accept ? 1u : 0u);
+  st_sc1(rw + RW_EMIT, (uint32_t)rs.arg);
+  st_sc1_f(rw + RW_LPD, (float)rs.lp_d);
+  st_sc1_f(rw + RW_LPEMIT, (float)rs.lp_emit);
+  st_sc1_f(rw + RW_D, (float)D);
+  st_sc1_f(rw + RW_GEFF, (float)geff);
+  st_sc1(rw + RW_KIND, (uint32_t)g.kind);
+  st_sc1_d(rw + RW_TOTAL, total);
+  if (g.kind == kSampleDraft) {
+    st_sc1_f(rw + RW_C, g.c);
+    st_sc1_f(rw + RW_R1, rs.R[sF]);
+    st_sc1_f(rw + RW_IS1, rs.isF);
+    st_sc1_f(rw + RW_R2, rs.Rq);
+    st_sc1_f(rw + RW_IS2, rs.isQ);
+    st_sc1_d(rw + RW_L2P, rs.L2[sF]);
+  } else if (g.kind == kSampleBonus) {
+    st_sc1_f(rw + RW_C, g.c);
+    st_sc1_f(rw + RW_R1, rs.R[sT]);
+    st_sc1_d(rw + RW_L2P, rs.L2[sT]);
+  }
+  wait_vm();
+  st_sc1(rw + (kRowWords - 1), A.epoch);
+  wait_vm();
+}
+
+// Wave 0: true when every row of request `req` carries this launch's epoch.
+// Each settling row writes its epoch (and waits for it to be performed)
+// before checking, so the last row to settle always sees all of them; two
+// rows settling together may both see them, which only repeats the
+// (deterministic) epilogue.
+DEV bool request_complete(const KArgs& A, int req) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t* base = A.rowres + (size_t)req * (A.K + 1) * kRowWords + (kRowWords - 1);
+  bool ok = true;
+  for (int i = lane; i <= A.K; i += 64) ok = ok && (ld_sc1(base + (size_t)i * kRowWords) == A.epoch);
+  return __all(ok);
+}
+
+// Inverse-CDF emission: the first element x of row `row` whose cumulative
+// weight exceeds u * total; weights are the residual (draft rows) or the
+// bonus weights, recomputed with the same element functions as pass 2.
+// Returns -1 when no element carries weight.  Whole workgroup.
+template <int DT>
+DEV int cdf_pick(const KArgs& A, int row, double u, double total, const uint32_t* rw,
+                 bool bonus, Smem& sm) {
+  constexpr int VE = Elem<DT>::VE;
+  const int tid = threadIdx.x;
+  const RowGeo g = row_geo<DT>(A, row);
+  const double target = u * total;
+  const int nseg = A.S * kWaves;
+  const uint32_t* base2 = A.rec2 + (size_t)row * A.S * kRec2Words;
+  // 1. the segment holding the target: scan of segment sums in index order
+  double carry = 0.0;
+  int sel = 0x7FFFFFFF, last_nz = -1;
+  for (int s0 = 0; s0 < nseg && sel == 0x7FFFFFFF; s0 += kThreads) {
+    const int sg = s0 + tid;
+    double v = 0.0;
+    if (sg < nseg) v = ld_sc1_d(base2 + (size_t)(sg / kWaves) * kRec2Words + 2 + 2 * (sg % kWaves));
+    double incl, excl;
+    block_scan(v, sm, incl, excl);
+    incl += carry;
+    excl += carry;
+    const int cand = block_min_i((v > 0.0 && incl > target) ? sg : 0x7FFFFFFF, sm);
+    const int lnz = block_min_i(v > 0.0 ? -sg : 0x7FFFFFFF, sm);
+    if (lnz != 0x7FFFFFFF) last_nz = -lnz;
+    __syncthreads();
+    if (sg == cand) sm.dd[6] = excl;
+    if (sg == last_nz) sm.dd[7] = excl;
+    if (tid == kThreads - 1) sm.dd[5] = incl;
+    __syncthreads();
+    carry = sm.dd[5];
+    sel = cand;
+  }
+  if (sel == 0x7FFFFFFF) {
+    if (last_nz < 0) return -1;
+    sel = last_nz;
+    if (tid == 0) sm.dd[6] = sm.dd[7];
+  }
+  __syncthreads();
+  const double before = sm.dd[6];
+  // 2. scan inside the segment: thread tid < kSegVec takes its vector tid
+  static_assert(kSegVec <= kThreads, "at most one segment vector per thread");
+  const int c = sel / kWaves, ww = sel % kWaves;
+  ResidConst rk{A.beta, ld_sc1_f(rw + RW_C), ld_sc1_f(rw + RW_R1), ld_sc1_f(rw + RW_IS1),
+                ld_sc1_f(rw + RW_R2), ld_sc1_f(rw + RW_IS2)};
+  BonusConst bk{rk.c, rk.Rf};
+  const long long vi = g.vbeg + (long long)c * kChunkVec + (long long)ww * kSegVec + tid;
+  float w8[VE];
+  double tsum = 0.0;
+  int last_pos = -1;
+  #pragma unroll
+  for (int e = 0; e < VE; ++e) {
+    const long long idx = vi * VE + e;
+    float wv = 0.0f;
+    if (tid < kSegVec && idx >= g.e0 && idx < g.e0 + A.V) {
+      const float xt = Elem<DT>::load_one(A.t, idx);
+      if (bonus) {
+        wv = bonus_elem(xt, bk);
+      } else {
+        const float xa = Elem<DT>::load_one(A.a, idx);
+        const float xb = Elem<DT>::load_one(A.b, idx);
+        wv = resid_elem(xt, xa, xb, rk);
+      }
+    }
+    w8[e] = wv;
+    tsum += (double)wv;
+    if (wv > 0.0f) last_pos = (int)(idx - g.e0);
+  }
+  double incl, excl;
+  block_scan(tsum, sm, incl, excl);
+  double run = before + excl;
+  int first_ok = 0x7FFFFFFF;
+  #pragma unroll
+  for (int e = 0; e < VE; ++e) {
+    run += (double)w8[e];
+    if (w8[e] > 0.0f && run > target && first_ok == 0x7FFFFFFF)
+      first_ok = (int)(vi * VE + e - g.e0);
+  }
+  int pick = block_min_i(first_ok, sm);
+  if (pick == 0x7FFFFFFF) {
+    // rounding left the target past the segment's own sum: its last nonzero
+    const int neg = block_min_i(last_pos >= 0 ? -last_pos : 0x7FFFFFFF, sm);
+    pick = (neg == 0x7FFFFFFF) ? -1 : -neg;
+  }
+  return pick;
+}
+
+// Argmax of the fused logits of one row by a full scan (whole workgroup);
+// only used when a residual is empty (p~ equal to q in fp32).
+template <int DT>
+DEV int row_argmax_f(const KArgs& A, const RowGeo& g, Smem& sm) {
+  float best = kFloorM;
+  int bi = 0x7FFFFFFF;
+  for (int x = threadIdx.x; x < A.V; x += kThreads) {
+    const long long idx = g.e0 + x;
+    const float f = fuse(Elem<DT>::load_one(A.t, idx), Elem<DT>::load_one(A.a, idx),
+                         Elem<DT>::load_one(A.b, idx), A.beta);
+    if (f > best) { best = f; bi = x; }
+  }
+  const float M = wave_max(best);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sm.wm[threadIdx.x >> 6][0] = M;
+  __syncthreads();
+  float Mb = sm.wm[0][0];
+  #pragma unroll
+  for (int i = 1; i < kWaves; ++i) Mb = fmaxf(Mb, sm.wm[i][0]);
+  return block_min_i(best == Mb ? bi : 0x7FFFFFFF, sm);
+}
+
+template <int DT>
+DEV void request_epilogue(const KArgs& A, int req, Smem& sm) {
+  const int tid = threadIdx.x;
+  const int K = A.K;
+  const size_t row0 = (size_t)req * (K + 1);
+  // accept_len = first rejected draft (Alg. 1); threads read rows in parallel
+  int rej = 0x7FFFFFFF;
+  for (int i = tid; i < K; i += kThreads)
+    if (ld_sc1(A.rowres + (row0 + i) * kRowWords + RW_ACCEPT) == 0u) rej = min(rej, i);
+  rej = block_min_i(rej, sm);
+  const int j = (rej == 0x7FFFFFFF) ? K : rej;
+  const uint32_t* rw = A.rowres + (row0 + j) * kRowWords;
+  const uint32_t kind = ld_sc1(rw + RW_KIND);
+  int next = 0;
+  double lpn = 0.0;
+  if (kind == kGreedyDraft || kind == kGreedyBonus) {
+    next = (int)ld_sc1(rw + RW_EMIT);
+    lpn = (double)ld_sc1_f(rw + RW_LPEMIT);
+  } else {
+    const double u = (double)A.u[req * (K + 1) + K];
+    const double total = ld_sc1_d(rw + RW_TOTAL);
+    const bool bonus = kind == kSampleBonus;
+    int pick = -1;
+    if (total > 0.0) pick = cdf_pick<DT>(A, (int)(row0 + j), u, total, rw, bonus, sm);
+    if (pick < 0) pick = row_argmax_f<DT>(A, row_geo<DT>(A, (int)(row0 + j)), sm);
+    next = pick;
+    const long long idx = (long long)(row0 + j) * A.V + next;
+    const float xt = Elem<DT>::load_one(A.t, idx);
+    float x = xt;
+    if (!bonus) {
+      const float xa = Elem<DT>::load_one(A.a, idx);
+      const float xb = Elem<DT>::load_one(A.b, idx);
+      x = fuse_masked(xt, xa, xb, A.beta);
+    }
+    const double c = (double)ld_sc1_f(rw + RW_C);
+    lpn = ((double)x * c - ld_sc1_d(rw + RW_L2P)) * kLn2;
+  }
+  for (int i = tid; i < K; i += kThreads) {
+    const uint32_t* ri = A.rowres + (row0 + i) * kRowWords;
+    A.flp_out[req * (K + 1) + i] = ld_sc1_f(ri + RW_LPD);
+    if (A.gate_out != nullptr) {
+      A.gate_out[(req * K + i) * 2 + 0] = ld_sc1_f(ri + RW_D);
+      A.gate_out[(req * K + i) * 2 + 1] = ld_sc1_f(ri + RW_GEFF);
+    }
+  }
+  if (tid == 0) {
+    A.acc_out[req] = j;
+    A.next_out[req] = next;
+    A.flp_out[req * (K + 1) + K] = (float)lpn;
+  }
+}
+
+// Thread 0, after the team barrier: combine the S chunk records of the row
+// into RowScal and classify the row (Eq. 3-4; the sampling form for tau > 0).
+template <int DT>
+DEV void combine_and_classify(const KArgs& A, const RowGeo& g, Smem& sm) {
+  RowScal& rs = sm.rs;
+  const bool draft = is_draft(g.kind);
+  const bool samp = g.kind == kSampleDraft || g.kind == kSampleBonus;
+  const bool tau1 = g.tau == 1.0f;
+  float cs[kSlots];
+  cs[sT] = samp ? g.c : kL2E;
+  cs[sA] = kL2E;
+  cs[sB] = kL2E;
+  cs[sF] = samp ? g.c : kL2E;
+  cs[sAT] = g.c;
+  const uint32_t* base = A.rec1 + (size_t)g.row * A.S * kRec1Words;
+  const int asl = draft ? sF : sT;
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) rs.M[s] = kFloorM;
+  for (int c = 0; c < A.S; ++c) {
+    const uint32_t* rc = base + (size_t)c * kRec1Words;
+    #pragma unroll
+    for (int s = 0; s < kSlots; ++s) rs.M[s] = fmaxf(rs.M[s], ld_sc1_f(rc + s));
+  }
+  int arg = 0x7FFFFFFF;
+  int nq = 0;
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) { rs.R[s] = rs.M[s] * cs[s]; rs.S[s] = 0.0; }
+  for (int c = 0; c < A.S; ++c) {
+    const uint32_t* rc = base + (size_t)c * kRec1Words;
+    #pragma unroll
+    for (int s = 0; s < kSlots; ++s) {
+      const float mc = ld_sc1_f(rc + s);
+      const double sc = ld_sc1_d(rc + 6 + 2 * s);
+      rs.S[s] += sc * (double)__builtin_amdgcn_exp2f(mc * cs[s] - rs.R[s]);
+    }
+    if (ld_sc1_f(rc + asl) == rs.M[asl]) arg = min(arg, (int)ld_sc1(rc + 16));
+    nq |= (int)ld_sc1(rc + 17);
+  }
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) rs.L2[s] = (double)rs.R[s] + log2_dbl(rs.S[s]);
+  rs.arg = arg;
+  rs.neq = nq != 0;
+  const bool cda = A.gate_mode == ASYMSPEC_GATE_CDA;
+  rs.decided = 1;
+  rs.accept = 0;
+  rs.needD = rs.needRes = 0;
+  rs.needBonus = g.kind == kSampleBonus;
+  rs.margin = rs.lp_d = rs.lp_emit = rs.lnu = 0.0;
+  rs.isF = rs.isQ = rs.Rq = 0.0f;
+  if (draft) {
+    const double ka = log2_dbl(rs.S[sA]), kb = log2_dbl(rs.S[sB]);
+    rs.khi[0] = (float)ka; rs.klo[0] = (float)(ka - (double)rs.khi[0]);
+    rs.khi[1] = (float)kb; rs.klo[1] = (float)(kb - (double)rs.khi[1]);
+    int dtok = A.d[g.req * A.K + g.pos];
+    dtok = dtok < 0 ? 0 : (dtok >= A.V ? A.V - 1 : dtok);
+    const long long idx = g.e0 + dtok;
+    const float td = Elem<DT>::load_one(A.t, idx);
+    const float ad = Elem<DT>::load_one(A.a, idx);
+    const float bd = Elem<DT>::load_one(A.b, idx);
+    const float fd = fuse_masked(td, ad, bd, A.beta);
+    if (g.kind == kGreedyDraft) {
+      const double lpt = ((double)td * (double)kL2E - rs.L2[sT]) * kLn2;
+      const double lpb = ((double)bd * (double)kL2E - rs.L2[sB]) * kLn2;
+      double m0 = lpt - lpb - A.ln_gamma;
+      if (m0 != m0) m0 = -INFINITY;
+      rs.margin = m0;
+      rs.lp_d = ((double)fd * (double)kL2E - rs.L2[sF]) * kLn2;
+      rs.lp_emit = ((double)rs.M[sF] * (double)kL2E - rs.L2[sF]) * kLn2;
+      if (!cda || !rs.neq) rs.accept = m0 > 0.0;
+      else if (m0 > 0.0) rs.accept = 1;
+      else if (m0 + kLn2 <= 0.0) rs.accept = 0;
+      else rs.decided = 0;
+      rs.needD = rs.neq && (!rs.decided || A.want_gate);
+    } else {
+      const int qs = tau1 ? sA : sAT;
+      rs.lp_d = ((double)fd * (double)g.c - rs.L2[sF]) * kLn2;
+      double lq;
+      if (A.dp != nullptr) {
+        const float pq = A.dp[g.req * A.K + g.pos];
+        lq = pq > 0.0f ? ln_f(pq) : -INFINITY;
+      } else {
+        lq = ((double)ad * (double)g.c - rs.L2[qs]) * kLn2;
+      }
+      double x;
+      if (rs.lp_d == -INFINITY) x = -INFINITY;
+      else if (lq == -INFINITY) x = INFINITY;
+      else x = rs.lp_d - lq - A.ln_gamma;
+      rs.margin = x;
+      const float u = A.u[g.req * (A.K + 1) + g.pos];
+      rs.lnu = u > 0.0f ? ln_f(u) : -INFINITY;
+      // accept iff ln u < x + D (u < min(1, exp(x + D)) for u in [0, 1))
+      if (!cda || !rs.neq) rs.accept = rs.lnu < x;
+      else if (rs.lnu < x) rs.accept = 1;
+      else if (rs.lnu >= x + kLn2) rs.accept = 0;
+      else rs.decided = 0;
+      rs.needD = rs.neq && (!rs.decided || A.want_gate);
+      rs.needRes = !(rs.decided && rs.accept);
+      rs.isF = (float)(1.0 / rs.S[sF]);
+      rs.isQ = (float)(1.0 / rs.S[qs]);
+      rs.Rq = rs.R[qs];
+    }
+  } else if (g.kind == kGreedyBonus) {
+    rs.lp_emit = ((double)rs.M[sT] * (double)kL2E - rs.L2[sT]) * kLn2;
+  }
+}
+
+template <int DT>
+DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
+                     u4 (&nxt)[3][kNV], bool has_next, int next_row, Smem& sm) {
+  constexpr int VE = Elem<DT>::VE;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const RowGeo g = row_geo<DT>(A, row);
+  if (has_next) {
+    const RowGeo gn = row_geo<DT>(A, next_row);
+    issue_loads<DT>(A, gn, mem, nxt);
+  }
+  sanitize<DT>(g, A, mem, cur);
+
+  const bool draft = is_draft(g.kind);
+  const bool samp = g.kind == kSampleDraft || g.kind == kSampleBonus;
+  const bool greedy_draft = g.kind == kGreedyDraft;
+  const bool needT = !draft || greedy_draft;
+  const bool needAT = g.kind == kSampleDraft && g.tau != 1.0f;
+  const float cT = samp ? g.c : kL2E;
+  const float cF = samp ? g.c : kL2E;
+
+  // ---------------------------------------------------------- pass 1
+  Acc qT, qA, qB, qF, qAT;
+  acc_init(qT, cT); acc_init(qA, kL2E); acc_init(qB, kL2E); acc_init(qF, cF); acc_init(qAT, g.c);
+  uint32_t neq = 0;
+  if (draft) {
+    #pragma unroll
+    for (int k = 0; k < kNV; ++k) {
+      float xt[VE], xa[VE], xb[VE], xf[VE];
+      #pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        xt[e] = Elem<DT>::get(cur[0][k], e);
+        xa[e] = Elem<DT>::get(cur[1][k], e);
+        xb[e] = Elem<DT>::get(cur[2][k], e);
+        xf[e] = fuse(xt[e], xa[e], xb[e], A.beta);
+      }
+      #pragma unroll
+      for (int j = 0; j < 4; ++j) neq |= cur[1][k][j] ^ cur[2][k][j];
+      if (greedy_draft) acc_vec<VE, false>(qT, xt, cT, k);
+      acc_vec<VE, false>(qA, xa, kL2E, k);
+      acc_vec<VE, false>(qB, xb, kL2E, k);
+      acc_vec<VE, true>(qF, xf, cF, k);
+      if (needAT) acc_vec<VE, false>(qAT, xa, g.c, k);
+    }
+  } else {
+    #pragma unroll
+    for (int k = 0; k < kNV; ++k) {
+      float xt[VE];
+      #pragma unroll
+      for (int e = 0; e < VE; ++e) xt[e] = Elem<DT>::get(cur[0][k], e);
+      acc_vec<VE, false>(qT, xt, cT, k);
+    }
+  }
+
+  // wave level: max, sums rescaled to the wave max, argmax candidate
+  {
+    Acc* qs[kSlots] = {&qT, &qA, &qB, &qF, &qAT};
+    const float cs[kSlots] = {cT, kL2E, kL2E, cF, g.c};
+    #pragma unroll
+    for (int s = 0; s < kSlots; ++s) {
+      const bool used = (s == sT) ? needT : (s == sAT ? needAT : draft);
+      float mw = kFloorM, sw = 0.0f;
+      if (used) {
+        mw = wave_max(qs[s]->m);
+        const float sr = qs[s]->s * __builtin_amdgcn_exp2f(qs[s]->R - mw * cs[s]);
+        sw = wave_sum(sr);
+      }
+      if (lane == 0) { sm.wm[w][s] = mw; sm.ws[w][s] = sw; }
+    }
+    const bool need_arg = greedy_draft || g.kind == kGreedyBonus;
+    int cand = 0x7FFFFFFF;
+    if (need_arg) {
+      const Acc& qa = greedy_draft ? qF : qT;
+      const float mw = wave_max(qa.m);
+      // lowest vector position (k*64 + lane) whose maximum equals the wave's
+      int pos = (qa.m == mw && mw > kFloorM) ? (qa.kb * 64 + lane) : 0x7FFFFFFF;
+      pos = wave_min_i(pos);
+      if (pos != 0x7FFFFFFF && lane == (pos & 63)) {
+        const int kk = pos >> 6;
+        u4 vt = kk == 0 ? cur[0][0] : cur[0][kNV - 1];
+        u4 va = kk == 0 ? cur[1][0] : cur[1][kNV - 1];
+        u4 vb = kk == 0 ? cur[2][0] : cur[2][kNV - 1];
+        #pragma unroll
+        for (int e = VE - 1; e >= 0; --e) {
+          const float x = greedy_draft ? fuse(Elem<DT>::get(vt, e), Elem<DT>::get(va, e),
+                                              Elem<DT>::get(vb, e), A.beta)
+                                       : Elem<DT>::get(vt, e);
+          if (x == mw) {
+            const long long vi = g.vbeg + (long long)mem * kChunkVec + (long long)w * kSegVec +
+                                 (long long)kk * 64 + lane;
+            cand = (int)(vi * VE + e - g.e0);
+          }
+        }
+      }
+      cand = wave_min_i(cand);
+    }
+    const int wn = __any(neq != 0) ? 1 : 0;       // whole wave votes
+    if (lane == 0) { sm.warg[w] = cand; sm.wneq[w] = wn; }
+  }
+  __syncthreads();
+  // thread 0: chunk record (fp64 across waves)
+  uint32_t* r1 = A.rec1 + ((size_t)row * A.S + mem) * kRec1Words;
+  if (tid == 0) {
+    const float cs[kSlots] = {cT, kL2E, kL2E, cF, g.c};
+    int arg = 0x7FFFFFFF, nq = 0;
+    const int asl = draft ? sF : sT;
+    float Mall = kFloorM;
+    #pragma unroll
+    for (int i = 0; i < kWaves; ++i) Mall = fmaxf(Mall, sm.wm[i][asl]);
+    #pragma unroll
+    for (int s = 0; s < kSlots; ++s) {
+      float M = kFloorM;
+      #pragma unroll
+      for (int i = 0; i < kWaves; ++i) M = fmaxf(M, sm.wm[i][s]);
+      const float R = M * cs[s];
+      double S = 0.0;
+      #pragma unroll
+      for (int i = 0; i < kWaves; ++i)
+        S += (double)sm.ws[i][s] * (double)__builtin_amdgcn_exp2f(sm.wm[i][s] * cs[s] - R);
+      sm.rec[s] = __float_as_uint(M);
+      const uint64_t x = __builtin_bit_cast(uint64_t, S);
+      sm.rec[6 + 2 * s] = (uint32_t)x;
+      sm.rec[7 + 2 * s] = (uint32_t)(x >> 32);
+    }
+    #pragma unroll
+    for (int i = 0; i < kWaves; ++i) {
+      if (sm.wm[i][asl] == Mall) arg = min(arg, sm.warg[i]);
+      nq |= sm.wneq[i];
+    }
+    sm.rec[5] = 0;
+    sm.rec[16] = (uint32_t)arg;
+    sm.rec[17] = (uint32_t)nq;
+  }
+  __syncthreads();
+  if (w == 0) {
+    if (lane < 18) st_sc1(r1 + lane, sm.rec[lane]);
+    wait_vm();
+    if (lane == 0) st_sc1(r1 + (kRec1Words - 1), A.epoch);
+
+    // ------------------------------------------------ team barrier
+    const uint32_t* base = A.rec1 + (size_t)row * A.S * kRec1Words;
+    long spins = 0;
+    while (true) {
+      bool ok = true;
+      for (int c = lane; c < A.S; c += 64)
+        ok = ok && (ld_sc1(base + (size_t)c * kRec1Words + (kRec1Words - 1)) == A.epoch);
+      if (__all(ok)) break;
+      __builtin_amdgcn_s_sleep(1);
+      if (++spins > kSpinLimit) {
+        if (lane == 0) atom_add(A.err, 1u);
+        break;
+      }
+    }
+    if (lane == 0) combine_and_classify<DT>(A, g, sm);
+  }
+  __syncthreads();
+
+  // ------------------------------------------------------------ pass 2
+  const int needD = sm.rs.needD, needRes = sm.rs.needRes, needBonus = sm.rs.needBonus;
+  if (needD || needRes || needBonus) {
+    float accj = 0.0f, seg = 0.0f;
+    if (needD || needRes) {
+      const float kahi = sm.rs.khi[0], kalo = sm.rs.klo[0];
+      const float kbhi = sm.rs.khi[1], kblo = sm.rs.klo[1];
+      const float Ra = sm.rs.R[sA], Rb = sm.rs.R[sB];
+      const ResidConst rk{A.beta, g.c, sm.rs.R[sF], sm.rs.isF, sm.rs.Rq, sm.rs.isQ};
+      #pragma unroll
+      for (int k = 0; k < kNV; ++k) {
+        float vj[VE], vr[VE];
+        #pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const float xt = Elem<DT>::get(cur[0][k], e);
+          const float xa = Elem<DT>::get(cur[1][k], e);
+          const float xb = Elem<DT>::get(cur[2][k], e);
+          vj[e] = 0.0f;
+          vr[e] = 0.0f;
+          if (needD) {
+            // P log2(2P/(P+Q)) + Q log2(2Q/(P+Q)) with lp = log2 P, lq = log2 Q
+            const float lp = (fmaxf(__builtin_fmaf(xa, kL2E, -Ra), kFloorM) - kahi) - kalo;
+            const float lq = (fmaxf(__builtin_fmaf(xb, kL2E, -Rb), kFloorM) - kbhi) - kblo;
+            const float P = __builtin_amdgcn_exp2f(lp);
+            const float Q = __builtin_amdgcn_exp2f(lq);
+            const float gg = 1.0f - __builtin_amdgcn_logf(fmaxf(P + Q, 1e-37f));
+            vj[e] = __builtin_fmaf(P, lp + gg, Q * (lq + gg));
+          }
+          if (needRes) vr[e] = resid_elem(xt, xa, xb, rk);
+        }
+        #pragma unroll
+        for (int st = 1; st < VE; st <<= 1)
+          #pragma unroll
+          for (int e = 0; e + st < VE; e += 2 * st) { vj[e] += vj[e + st]; vr[e] += vr[e + st]; }
+        accj += vj[0];
+        seg += vr[0];
+      }
+    } else {
+      const BonusConst bk{g.c, sm.rs.R[sT]};
+      #pragma unroll
+      for (int k = 0; k < kNV; ++k) {
+        float vb[VE];
+        #pragma unroll
+        for (int e = 0; e < VE; ++e) vb[e] = bonus_elem(Elem<DT>::get(cur[0][k], e), bk);
+        #pragma unroll
+        for (int st = 1; st < VE; st <<= 1)
+          #pragma unroll
+          for (int e = 0; e + st < VE; e += 2 * st) vb[e] += vb[e + st];
+        seg += vb[0];
+      }
+    }
+    const float wj = needD ? wave_sum(accj) : 0.0f;
+    const float wseg = (needRes || needBonus) ? wave_sum(seg) : 0.0f;
+    if (lane == 0) { sm.wj[w] = wj; sm.wseg[w] = wseg; }
+    __syncthreads();
+    uint32_t* r2 = A.rec2 + ((size_t)row * A.S + mem) * kRec2Words;
+    if (w == 0) {
+      if (lane == 0) {
+        double j = 0.0;
+        #pragma unroll
+        for (int i = 0; i < kWaves; ++i) j += (double)sm.wj[i];
+        st_sc1_d(r2 + 0, j);
+      }
+      if (lane >= 1 && lane <= kWaves) st_sc1_d(r2 + 2 * lane, (double)sm.wseg[lane - 1]);
+      wait_vm();
+      if (lane == 0) st_sc1(r2 + (kRec2Words - 1), A.epoch);
+      wait_vm();
+      // settle if every member's pass-2 record is in (see request_complete
+      // for why at least one member sees them all)
+      const uint32_t* base2 = A.rec2 + (size_t)row * A.S * kRec2Words;
+      bool ok = true;
+      for (int c = lane; c < A.S; c += 64)
+        ok = ok && (ld_sc1(base2 + (size_t)c * kRec2Words + (kRec2Words - 1)) == A.epoch);
+      int done = 0;
+      if (__all(ok)) {
+        double dj = 0.0, tt = 0.0;
+        for (int c = lane; c < A.S; c += 64) {
+          dj += ld_sc1_d(base2 + (size_t)c * kRec2Words);
+          #pragma unroll
+          for (int i = 0; i < kWaves; ++i) tt += ld_sc1_d(base2 + (size_t)c * kRec2Words + 2 + 2 * i);
+        }
+        dj = wave_sum_d(dj);
+        tt = wave_sum_d(tt);
+        if (lane == 0) {
+          double D = 0.0;
+          if (needD) {
+            D = 0.5 * kLn2 * dj;
+            D = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
+          }
+          write_row_t0<DT>(A, g, sm.rs, D, tt);
+        }
+        done = request_complete(A, g.req) ? 1 : 0;
+      }
+      if (lane == 0) sm.flags[0] = done;
+    }
+  } else {
+    if (w == 0) {
+      int done = 0;
+      if (mem == 0) {
+        if (lane == 0) write_row_t0<DT>(A, g, sm.rs, 0.0, 0.0);
+        done = request_complete(A, g.req) ? 1 : 0;
+      }
+      if (lane == 0) sm.flags[0] = done;
+    }
+  }
+  __syncthreads();
+  if (sm.flags[0]) request_epilogue<DT>(A, g.req, sm);
+  __syncthreads();
+}
+
+template <int DT>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void fuse_verify_kernel(KArgs A) {
+  __shared__ Smem sm;
+  const int team = blockIdx.x / A.S;
+  const int mem = blockIdx.x - team * A.S;
+  const int nrows = (A.rows - team + A.n_teams - 1) / A.n_teams;
+  if (team >= A.n_teams || nrows <= 0) return;
+  u4 cur[3][kNV], nxt[3][kNV];
+  {
+    const RowGeo g0 = row_geo<DT>(A, team);
+    issue_loads<DT>(A, g0, mem, cur);
+  }
+  for (int it = 0; it < nrows; ++it) {
+    const int r = team + it * A.n_teams;
+    const bool hn = it + 1 < nrows;
+    process_row<DT>(A, r, mem, cur, nxt, hn, r + A.n_teams, sm);
+    if (hn) {
+      #pragma unroll
+      for (int s = 0; s < 3; ++s)
+        #pragma unroll
+        for (int k = 0; k < kNV; ++k) cur[s][k] = nxt[s][k];
+    }
+  }
+}
+
+__global__ void fill_zero_kernel(uint32_t* p, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+// ---------------------------------------------------------------- host side
+struct Layout {
+  int S, VE;
+  size_t rows;
+  size_t off_rec1, off_rec2, off_row, off_err, total;
+};
+
+static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+static bool make_layout(int B, int K, int V, int dtype, Layout& L) {
+  if (B < 1 || K < 0 || V < 1) return false;
+  if (dtype != ASYMSPEC_BF16 && dtype != ASYMSPEC_FP32) return false;
+  const long double elems = (long double)B * (K + 1) * V;
+  if (elems >= (long double)(1ull << 40)) return false;
+  L.VE = dtype == ASYMSPEC_BF16 ? 8 : 4;
+  const long long nvec_max = ((long long)V + 2LL * L.VE - 2) / L.VE;
+  L.S = (int)((nvec_max + kChunkVec - 1) / kChunkVec);
+  L.rows = (size_t)B * (K + 1);
+  size_t off = 0;
+  L.off_rec1 = off; off = align_up(off + L.rows * L.S * kRec1Words * 4, 256);
+  L.off_rec2 = off; off = align_up(off + L.rows * L.S * kRec2Words * 4, 256);
+  L.off_row = off;  off = align_up(off + L.rows * kRowWords * 4, 256);
+  L.off_err = off; off = align_up(off + 256, 256);
+  L.total = off;
+  return true;
+}
+
+struct DevInfo {
+  int ok = 0;
+  int n_cu = 0;
+  int max_blocks[2] = {0, 0};
+};
+
+static DevInfo g_dev[64];
+static std::mutex g_dev_mu;
+
+static const DevInfo* device_info() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lk(g_dev_mu);
+  DevInfo& di = g_dev[dev];
+  if (di.ok) return &di;
+  hipDeviceProp_t pr;
+  if (hipGetDeviceProperties(&pr, dev) != hipSuccess) return nullptr;
+  if (std::strncmp(pr.gcnArchName, "gfx950", 6) != 0) return nullptr;
+  if (!pr.cooperativeLaunch) return nullptr;
+  di.n_cu = pr.multiProcessorCount;
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fuse_verify_kernel<ASYMSPEC_BF16>, kThreads, 0) != hipSuccess)
+    return nullptr;
+  di.max_blocks[ASYMSPEC_BF16] = nb * di.n_cu;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fuse_verify_kernel<ASYMSPEC_FP32>, kThreads, 0) != hipSuccess)
+    return nullptr;
+  di.max_blocks[ASYMSPEC_FP32] = nb * di.n_cu;
+  di.ok = 1;
+  return &di;
+}
+
+static uint32_t next_epoch() {
+  static std::atomic<uint32_t> ctr{0};
+  static std::once_flag once;
+  std::call_once(once, [] {
+    const uint64_t t = (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count();
+    ctr.store((uint32_t)(t ^ (t >> 32) ^ ((uint64_t)getpid() << 16)) | 1u);
+  });
+  uint32_t e;
+  do { e = ctr.fetch_add(1u); } while (e == 0u);
+  return e;
+}
+
+static bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+}  // namespace asym
+
+using namespace asym;
+
+extern "C" {
+
+size_t asymspec_workspace_size(int B, int K, int V, int dtype) {
+  Layout L;
+  if (!make_layout(B, K, V, dtype, L)) return 0;
+  return L.total;
+}
+
+int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stream) {
+  if (workspace == nullptr || workspace_bytes % 4 != 0 || !aligned(workspace, 4)) return ASYMSPEC_E_ARG;
+  if (workspace_bytes == 0) return ASYMSPEC_OK;
+  const size_t n = workspace_bytes / 4;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream,
+                     (uint32_t*)workspace, n);
+  return hipGetLastError() == hipSuccess ? ASYMSPEC_OK : ASYMSPEC_E_DEVICE;
+}
+
+int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
+                         const int32_t* draft_tokens, const float* draft_probs,
+                         const float* uniforms, const float* temperature,
+                         int B, int K, int V, const asymspec_params* params,
+                         int32_t* accept_len, int32_t* next_token, float* fused_logprobs,
+                         float* gate_out, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  Layout L;
+  if (params == nullptr) return ASYMSPEC_E_ARG;
+  if (!make_layout(B, K, V, dtype, L)) return ASYMSPEC_E_ARG;
+  if (t == nullptr || uniforms == nullptr || temperature == nullptr || accept_len == nullptr ||
+      next_token == nullptr || fused_logprobs == nullptr || workspace == nullptr)
+    return ASYMSPEC_E_ARG;
+  if (K > 0 && (a == nullptr || b == nullptr || draft_tokens == nullptr)) return ASYMSPEC_E_ARG;
+  if (!std::isfinite(params->beta) || params->beta < 0.0f) return ASYMSPEC_E_ARG;
+  if (!(params->gamma > 0.0f && params->gamma <= 1.0f)) return ASYMSPEC_E_ARG;
+  if (params->gate_mode != ASYMSPEC_GATE_CDA && params->gate_mode != ASYMSPEC_GATE_FIXED) return ASYMSPEC_E_ARG;
+  if (params->flags != 0u) return ASYMSPEC_E_ARG;
+  if (!aligned(t, 16) || (K > 0 && (!aligned(a, 16) || !aligned(b, 16)))) return ASYMSPEC_E_ALIGN;
+  if (!aligned(uniforms, 4) || !aligned(temperature, 4) || !aligned(accept_len, 4) ||
+      !aligned(next_token, 4) || !aligned(fused_logprobs, 4) ||
+      (draft_tokens && !aligned(draft_tokens, 4)) || (draft_probs && !aligned(draft_probs, 4)) ||
+      (gate_out && !aligned(gate_out, 4)))
+    return ASYMSPEC_E_ALIGN;
+  if (!aligned(workspace, 256)) return ASYMSPEC_E_ALIGN;
+  if (workspace_bytes < L.total) return ASYMSPEC_E_WORKSPACE;
+  const DevInfo* di = device_info();
+  if (di == nullptr) return ASYMSPEC_E_DEVICE;
+  const int gmax = di->max_blocks[dtype];
+  if (L.S > gmax) return ASYMSPEC_E_ARG;
+
+  KArgs A;
+  A.t = t; A.a = (K > 0) ? a : t; A.b = (K > 0) ? b : t;
+  A.d = draft_tokens; A.dp = draft_probs; A.u = uniforms; A.tau = temperature;
+  A.acc_out = accept_len; A.next_out = next_token; A.flp_out = fused_logprobs; A.gate_out = gate_out;
+  char* ws = (char*)workspace;
+  A.rec1 = (uint32_t*)(ws + L.off_rec1);
+  A.rec2 = (uint32_t*)(ws + L.off_rec2);
+  A.rowres = (uint32_t*)(ws + L.off_row);
+  A.err = (uint32_t*)(ws + L.off_err);
+  A.stream_bytes = (unsigned long long)B * (K + 1) * (unsigned long long)V * (dtype == ASYMSPEC_BF16 ? 2ull : 4ull);
+  A.B = B; A.K = K; A.V = V; A.S = L.S;
+  A.rows = (int)L.rows;
+  const int teams_fit = gmax / L.S;
+  A.n_teams = (int)std::min<long long>((long long)L.rows, teams_fit);
+  A.beta = params->beta; A.gamma = params->gamma; A.gate_mode = params->gate_mode;
+  A.want_gate = gate_out != nullptr;
+  A.ln_gamma = std::log((double)params->gamma);
+  A.epoch = next_epoch();
+
+  const dim3 grid(A.n_teams * A.S), block(kThreads);
+  void* args[] = {&A};
+  hipError_t e;
+  if (dtype == ASYMSPEC_BF16)
+    e = hipLaunchCooperativeKernel((const void*)fuse_verify_kernel<ASYMSPEC_BF16>, grid, block, args, 0,
+                                   (hipStream_t)stream);
+  else
+    e = hipLaunchCooperativeKernel((const void*)fuse_verify_kernel<ASYMSPEC_FP32>, grid, block, args, 0,
+                                   (hipStream_t)stream);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return ASYMSPEC_E_DEVICE;
+  }
+  return ASYMSPEC_OK;
+}
+
+const char* asymspec_status_string(int status) {
+  switch (status) {
+    case ASYMSPEC_OK: return "ok";
+    case ASYMSPEC_E_ARG: return "invalid argument";
+    case ASYMSPEC_E_ALIGN: return "misaligned pointer";
+    case ASYMSPEC_E_WORKSPACE: return "workspace too small";
+    case ASYMSPEC_E_DEVICE: return "device error (no gfx950 device current, or launch failed)";
+    default: return "unknown status";
+  }
+}
+
+int asymspec_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,83 @@
+"""Shared helpers for the GPU parity tests: numpy inputs -> device tensors,
+one call through the C ABI, and the comparison with the CPU oracle.
+
+Parity protocol
+  * accept_len and next_token bit-exact, except requests whose decisions lie
+    within NEAR_TIE of a threshold in the oracle (|ratio - u| for sampling
+    acceptance, |exp(margin) - 1| for Eq. 4, the distance of u_K from an
+    inverse-CDF step boundary for sampled emissions); those are counted and
+    reported separately;
+  * fused_logprobs within LP_TOL absolute (entry K only for requests whose
+    outcome matches);
+  * gate (D, gamma_eff) within LP_TOL absolute.
+"""
+
+import numpy as np
+
+import oracle as O
+
+NEAR_TIE = 1e-6
+LP_TOL = 1e-5
+
+
+def to_device(x, device="cuda"):
+    import torch
+    if x.dtype == np.uint16:
+        return torch.from_numpy(x.view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(x)).to(device)
+
+
+def run_gpu(inp, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True, want_gate=True,
+            device="cuda"):
+    import torch
+    import paper_2608_26004_amd as asp
+    t, a, b = (to_device(x, device) for x in (inp.t, inp.a, inp.b))
+    d = to_device(inp.draft_tokens.astype(np.int32), device)
+    q = to_device(inp.draft_probs.astype(np.float32), device) if with_probs else None
+    u = to_device(inp.uniforms.astype(np.float32), device)
+    tau = to_device(inp.temperature.astype(np.float32), device)
+    out = asp.fuse_verify(t, a, b, d, q, u, tau, beta=beta, gamma=gamma,
+                          gate_mode=gate_mode, return_gate=want_gate)
+    torch.cuda.synchronize()
+    res = [x.cpu().numpy() for x in out]
+    if not want_gate:
+        res.append(None)
+    return res
+
+
+def compare(inp, gpu, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True,
+            requests=None, label=""):
+    """Run the oracle on `requests` (all by default) and compare.  Returns a
+    dict report; raises AssertionError on a parity failure."""
+    acc_g, nxt_g, flp_g, gate_g = gpu
+    idx = list(range(inp.B)) if requests is None else list(requests)
+    acc_o, nxt_o, flp_o, gate_o, res = O.fuse_verify(
+        inp.t, inp.a, inp.b, inp.draft_tokens, inp.draft_probs if with_probs else None,
+        inp.uniforms, inp.temperature, beta=beta, gamma=gamma, gate_mode=gate_mode,
+        requests=idx)
+    K = inp.K
+    near, bad = [], []
+    max_lp = 0.0
+    max_gate = 0.0
+    for k, bi in enumerate(idx):
+        same = acc_g[bi] == acc_o[k] and nxt_g[bi] == nxt_o[k]
+        tie = res[k].near_tie(NEAR_TIE)
+        if not same:
+            (near if tie else bad).append((bi, int(acc_g[bi]), int(nxt_g[bi]),
+                                           int(acc_o[k]), int(nxt_o[k])))
+        hi = K + 1 if same else K
+        if hi > 0:
+            d = np.abs(flp_g[bi, :hi].astype(np.float64) - flp_o[k, :hi])
+            finite = np.isfinite(flp_o[k, :hi])
+            if np.any(finite != np.isfinite(flp_g[bi, :hi])):
+                bad.append((bi, "non-finite mismatch", flp_g[bi, :hi].tolist(), flp_o[k, :hi].tolist()))
+            elif finite.any():
+                max_lp = max(max_lp, float(d[finite].max()))
+        if gate_g is not None and K > 0:
+            max_gate = max(max_gate, float(np.abs(gate_g[bi].astype(np.float64) - gate_o[k]).max()))
+    report = dict(label=label, requests=len(idx), mismatches=bad, near_ties=near,
+                  max_lp_err=max_lp, max_gate_err=max_gate)
+    assert not bad, f"{label}: parity failures {bad[:5]} (report {report})"
+    assert max_lp <= LP_TOL, f"{label}: fused_logprobs error {max_lp}"
+    assert max_gate <= LP_TOL, f"{label}: gate error {max_gate}"
+    return report

@@ -1,0 +1,130 @@
+"""GPU parity of the HIP decision step against the CPU oracle, through the
+C ABI, on the seeded workloads and on edge shapes."""
+
+import numpy as np
+import pytest
+
+from paper_2608_26004_amd import synth
+
+from parity_util import compare, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _note(report):
+    print(f"[parity] {report['label']}: {report['requests']} requests, "
+          f"near-ties {len(report['near_ties'])}, max lp err {report['max_lp_err']:.2e}, "
+          f"max gate err {report['max_gate_err']:.2e}", flush=True)
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_26004_amd as asp
+    asp.load_library()
+    return torch.device("cuda")
+
+
+# ------------------------------------------------------------ small cases --
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("tau", [0.0, 1.0, 0.7])
+def test_small_mixed(gpu, dtype, tau):
+    x = synth.generate(B=6, K=3, V=5000, dtype=dtype, rho=("uniform", 0.0, 2.0), tau=tau, seed=11)
+    for mode in (0, 1):
+        g = run_gpu(x, gate_mode=mode)
+        _note(compare(x, g, gate_mode=mode, label=f"small {dtype} tau={tau} mode={mode}"))
+
+
+@pytest.mark.parametrize("V", [1, 2, 3, 5, 8, 4095, 4097, 8193, 32000])
+@pytest.mark.parametrize("K", [0, 1, 4])
+def test_edge_shapes(gpu, V, K):
+    for dtype in ("bf16", "fp32"):
+        x = synth.generate(B=5, K=K, V=V, dtype=dtype, rho=("uniform", 0.0, 2.0),
+                           tau=("alternate", 0.0, 1.0), seed=V * 10 + K)
+        g = run_gpu(x)
+        _note(compare(x, g, label=f"edge V={V} K={K} {dtype}"))
+
+
+def test_masked_tokens_and_identical_views(gpu):
+    x = synth.generate(B=8, K=3, V=3001, dtype="bf16", rho=("alternate", 0.0, 1.5),
+                       tau=("alternate", 0.0, 0.9), seed=5, mask_frac=0.1)
+    g = run_gpu(x)
+    r = compare(x, g, label="masked")
+    _note(r)
+    # identical drafter views: D = 0 and gamma_eff = gamma exactly
+    gate = g[3]
+    for bi in range(0, 8, 2):
+        assert np.all(gate[bi, :, 0] == 0.0) and np.all(gate[bi, :, 1] == np.float32(0.5))
+
+
+def test_shifted_comp_view_gives_zero_divergence(gpu):
+    x = synth.generate(B=4, K=3, V=20000, dtype="fp32", rho=0.0, tau=0.0, seed=9)
+    x.b[:] = (x.a.astype(np.float64) + 2.0).astype(np.float32)
+    g = run_gpu(x)
+    _note(compare(x, g, label="shifted b"))
+    assert np.abs(g[3][:, :, 0]).max() < 1e-6
+
+
+@pytest.mark.parametrize("beta,gamma", [(0.0, 1.0), (2.0, 0.5), (1.0, 1.0), (0.5, 0.25)])
+def test_beta_gamma_grid(gpu, beta, gamma):
+    x = synth.generate(B=8, K=4, V=7000, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=int(beta * 10 + gamma * 100))
+    for mode in (0, 1):
+        g = run_gpu(x, beta=beta, gamma=gamma, gate_mode=mode)
+        _note(compare(x, g, beta=beta, gamma=gamma, gate_mode=mode,
+                      label=f"beta={beta} gamma={gamma} mode={mode}"))
+
+
+def test_draft_probs_null(gpu):
+    x = synth.generate(B=8, K=4, V=9000, dtype="bf16", rho=1.0, tau=0.8, seed=21)
+    g = run_gpu(x, with_probs=False)
+    _note(compare(x, g, with_probs=False, label="draft_probs NULL"))
+
+
+def test_without_gate_output_matches(gpu):
+    x = synth.generate(B=12, K=4, V=6000, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=3)
+    g1 = run_gpu(x, want_gate=True)
+    g2 = run_gpu(x, want_gate=False)
+    assert np.array_equal(g1[0], g2[0]) and np.array_equal(g1[1], g2[1])
+    assert np.array_equal(g1[2], g2[2])
+    _note(compare(x, g2, label="no gate"))
+
+
+def test_determinism(gpu):
+    x = synth.generate(B=16, K=5, V=12000, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=8)
+    g1 = run_gpu(x)
+    g2 = run_gpu(x)
+    for u, v in zip(g1, g2):
+        assert np.array_equal(u, v)
+
+
+# --------------------------------------------------------------- workloads --
+@pytest.mark.parametrize("w", [0, 1, 2])
+def test_workload_full(gpu, w):
+    x = synth.workload_inputs(w)
+    g = run_gpu(x)
+    r = compare(x, g, label=f"workload {w} ({synth.WORKLOADS[w].name})")
+    _note(r)
+    assert len(r["near_ties"]) <= max(1, int(1e-4 * x.B * (x.K + 1)))
+
+
+def test_workload_3_full(gpu):
+    x = synth.workload_inputs(3)
+    for want_gate in (True, False):
+        g = run_gpu(x, want_gate=want_gate)
+        r = compare(x, g, label=f"workload 3 gate={want_gate}")
+        _note(r)
+
+
+def test_workload_4_sampled(gpu):
+    """Full-size launch (B=512, K=8, V=256000); the oracle checks a sample of
+    requests, half greedy and half sampling."""
+    x = synth.workload_inputs(4)
+    g = run_gpu(x)
+    sample = list(range(0, 8)) + list(range(250, 254)) + list(range(504, 512))
+    r = compare(x, g, requests=sample, label="workload 4 sampled")
+    _note(r)
