@@ -63,16 +63,21 @@ typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 enum Kind { kGreedyDraft = 0, kSampleDraft = 1, kGreedyBonus = 2, kSampleBonus = 3 };
 enum Slot { sT = 0, sA = 1, sB = 2, sF = 3, sAT = 4, kSlots = 5 };
 
-// Workspace record sizes in 32-bit words.
-constexpr int kRec1Words = 32;   // pass-1 chunk record, word 31 = epoch
-constexpr int kRec2Words = 16;   // pass-2 chunk record, word 15 = epoch
-constexpr int kRowWords = 32;    // settled row, word 31 = epoch
+// ---------------------------------------------------------------- kernel args
+// Cross-workgroup records are arrays of 64-bit slots: the high word is the
+// launch epoch, the low word the payload.  An aligned 64-bit atomic store is
+// single-copy atomic, so a reader that sees the current epoch in a slot also
+// sees its payload; writers never wait for their stores, readers poll until
+// every slot they need carries the epoch.
+constexpr int kR1 = 20;   // pass-1 chunk record slots (17 used)
+constexpr int kR2 = 12;   // pass-2 chunk record slots (10 used)
+constexpr int kRW = 16;   // settled-row record slots (14 used)
 
 struct KArgs {
   const void* t; const void* a; const void* b;
   const int32_t* d; const float* dp; const float* u; const float* tau;
   int32_t* acc_out; int32_t* next_out; float* flp_out; float* gate_out;
-  uint32_t* rec1; uint32_t* rec2; uint32_t* rowres;
+  uint64_t* rec1; uint64_t* rec2; uint64_t* rowres;
   uint32_t* err;
   unsigned long long stream_bytes;   // bytes of each logit array
   int B, K, V, S, n_teams, rows;
@@ -82,28 +87,24 @@ struct KArgs {
 };
 
 // ------------------------------------------------------------------ memory
-DEV void st_sc1(uint32_t* p, uint32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+DEV void st_tag(uint64_t* p, uint32_t v, uint32_t ep) {
+  __hip_atomic_store(p, ((uint64_t)ep << 32) | (uint64_t)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-DEV uint32_t ld_sc1(const uint32_t* p) {
-  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+DEV uint64_t ld_tag(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-DEV void st_sc1_d(uint32_t* p, double v) {
-  uint64_t x = __builtin_bit_cast(uint64_t, v);
-  st_sc1(p, (uint32_t)x);
-  st_sc1(p + 1, (uint32_t)(x >> 32));
+DEV bool tag_ok(uint64_t v, uint32_t ep) { return (uint32_t)(v >> 32) == ep; }
+DEV uint32_t pay(uint64_t v) { return (uint32_t)v; }
+DEV float payf(uint64_t v) { return __uint_as_float((uint32_t)v); }
+DEV double payd(uint64_t lo, uint64_t hi) {
+  return __builtin_bit_cast(double, (uint64_t)(uint32_t)lo | ((uint64_t)(uint32_t)hi << 32));
 }
-DEV double ld_sc1_d(const uint32_t* p) {
-  uint64_t lo = ld_sc1(p), hi = ld_sc1(p + 1);
-  return __builtin_bit_cast(double, lo | (hi << 32));
+DEV uint32_t dlo(double x) { return (uint32_t)__builtin_bit_cast(uint64_t, x); }
+DEV uint32_t dhi(double x) { return (uint32_t)(__builtin_bit_cast(uint64_t, x) >> 32); }
+DEV void err_count(const uint32_t* e) {
+  __hip_atomic_fetch_add(const_cast<uint32_t*>(e), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-DEV void st_sc1_f(uint32_t* p, float v) { st_sc1(p, __float_as_uint(v)); }
-DEV float ld_sc1_f(const uint32_t* p) { return __uint_as_float(ld_sc1(p)); }
-// Wait until this wave's stores are performed (s_waitcnt vmcnt(0)).
-DEV void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-DEV uint32_t atom_add(uint32_t* p, uint32_t v) {
-  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
+
 
 DEV __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned long long nbytes) {
   unsigned long long n = nbytes > 0xFFFFFFFFull ? 0xFFFFFFFFull : nbytes;
@@ -362,7 +363,7 @@ DEV double log2_dbl(double x) {
 }
 DEV double ln_f(float x) { return (double)__builtin_amdgcn_logf(x) * kLn2; }
 
-// Per-row scalars, computed once by thread 0 after the team barrier.
+// Per-row scalars, computed once by lane 0 after the team barrier.
 struct RowScal {
   float M[kSlots], R[kSlots];
   double S[kSlots], L2[kSlots];   // L2 = R + log2 S: log2-domain LSE at the slot scale
@@ -382,11 +383,13 @@ struct Smem {
   int   wneq[kWaves];
   float wj[kWaves];
   float wseg[kWaves];
-  uint32_t rec[kRec1Words];
-  RowScal rs;
+  uint32_t rec[kR1];
+  RowScal rs;                     // row being processed
+  RowScal rsp;                    // row whose settlement is deferred
   int   flags[8];
   double dd[8];
   double scan[kWaves];
+  uint32_t rw[kWaves * 4];        // epilogue: row-record words of the emitting row
 };
 
 // Inclusive and exclusive prefix sums over the workgroup, in thread order.
@@ -420,61 +423,65 @@ DEV int block_min_i(int x, Smem& sm) {
   return r;
 }
 
-// Settled-row record layout (words).
+// Settled-row record slots.
 enum {
   RW_ACCEPT = 0, RW_EMIT = 1, RW_LPD = 2, RW_LPEMIT = 3, RW_D = 4, RW_GEFF = 5,
   RW_C = 6, RW_R1 = 7, RW_IS1 = 8, RW_R2 = 9, RW_IS2 = 10, RW_KIND = 11,
-  RW_L2P = 12 /* double, 12-13 */, RW_TOTAL = 14 /* double, 14-15 */
+  RW_L2P_LO = 12, RW_L2P_HI = 13, RW_USED = 14
 };
 
-// Lane 0 of wave 0: decide the row from the combined statistics (Eq. 3-4 or
-// the sampling form) given D, write the settled-row record, then its epoch.
-template <int DT>
-DEV void write_row_t0(const KArgs& A, const RowGeo& g, const RowScal& rs, double D, double total) {
+// Lane 0: decide the row from its combined statistics and D (Eq. 3-4, or the
+// sampling form), and publish the settled-row record.
+DEV void write_row_t0(const KArgs& A, const RowGeo& g, const RowScal& rs, double D) {
   bool accept = rs.accept != 0;
   const bool cda = A.gate_mode == ASYMSPEC_GATE_CDA;
   if (!rs.decided) {
     if (g.kind == kGreedyDraft) accept = (rs.margin + (cda ? D : 0.0)) > 0.0;
     else if (g.kind == kSampleDraft) accept = rs.lnu < rs.margin + (cda ? D : 0.0);
   }
-  const double geff = cda ? (double)A.gamma * (double)__builtin_amdgcn_exp2f((float)(-D * 1.4426950408889634)) : (double)A.gamma;
-  uint32_t* rw = A.rowres + (size_t)g.row * kRowWords;
-  st_sc1(rw + RW_ACCEPT, accept ? 1u : 0u);
-  st_sc1(rw + RW_EMIT, (uint32_t)rs.arg);
-  st_sc1_f(rw + RW_LPD, (float)rs.lp_d);
-  st_sc1_f(rw + RW_LPEMIT, (float)rs.lp_emit);
-  st_sc1_f(rw + RW_D, (float)D);
-  st_sc1_f(rw + RW_GEFF, (float)geff);
-  st_sc1(rw + RW_KIND, (uint32_t)g.kind);
-  st_sc1_d(rw + RW_TOTAL, total);
-  if (g.kind == kSampleDraft) {
-    st_sc1_f(rw + RW_C, g.c);
-    st_sc1_f(rw + RW_R1, rs.R[sF]);
-    st_sc1_f(rw + RW_IS1, rs.isF);
-    st_sc1_f(rw + RW_R2, rs.Rq);
-    st_sc1_f(rw + RW_IS2, rs.isQ);
-    st_sc1_d(rw + RW_L2P, rs.L2[sF]);
-  } else if (g.kind == kSampleBonus) {
-    st_sc1_f(rw + RW_C, g.c);
-    st_sc1_f(rw + RW_R1, rs.R[sT]);
-    st_sc1_d(rw + RW_L2P, rs.L2[sT]);
-  }
-  wait_vm();
-  st_sc1(rw + (kRowWords - 1), A.epoch);
-  wait_vm();
+  const float geff = cda ? A.gamma * __builtin_amdgcn_exp2f((float)(-D * 1.4426950408889634)) : A.gamma;
+  uint64_t* rw = A.rowres + (size_t)g.row * kRW;
+  const uint32_t ep = A.epoch;
+  uint32_t v[RW_USED];
+  v[RW_ACCEPT] = accept ? 1u : 0u;
+  v[RW_EMIT] = (uint32_t)rs.arg;
+  v[RW_LPD] = __float_as_uint((float)rs.lp_d);
+  v[RW_LPEMIT] = __float_as_uint((float)rs.lp_emit);
+  v[RW_D] = __float_as_uint((float)D);
+  v[RW_GEFF] = __float_as_uint(geff);
+  v[RW_KIND] = (uint32_t)g.kind;
+  v[RW_C] = __float_as_uint(g.c);
+  v[RW_R1] = __float_as_uint(g.kind == kSampleDraft ? rs.R[sF] : rs.R[sT]);
+  v[RW_IS1] = __float_as_uint(rs.isF);
+  v[RW_R2] = __float_as_uint(rs.Rq);
+  v[RW_IS2] = __float_as_uint(rs.isQ);
+  const double l2 = g.kind == kSampleDraft ? rs.L2[sF] : rs.L2[sT];
+  v[RW_L2P_LO] = dlo(l2);
+  v[RW_L2P_HI] = dhi(l2);
+  #pragma unroll
+  for (int i = 0; i < RW_USED; ++i) st_tag(rw + i, v[i], ep);
 }
 
-// Wave 0: true when every row of request `req` carries this launch's epoch.
-// Each settling row writes its epoch (and waits for it to be performed)
-// before checking, so the last row to settle always sees all of them; two
-// rows settling together may both see them, which only repeats the
-// (deterministic) epilogue.
-DEV bool request_complete(const KArgs& A, int req) {
+// Wave 0: wait until all S pass-2 records of `row` are in; returns the fp64
+// sum of their JSD partials (every lane gets it).
+DEV double collect_jsd(const KArgs& A, int row) {
   const int lane = threadIdx.x & 63;
-  const uint32_t* base = A.rowres + (size_t)req * (A.K + 1) * kRowWords + (kRowWords - 1);
-  bool ok = true;
-  for (int i = lane; i <= A.K; i += 64) ok = ok && (ld_sc1(base + (size_t)i * kRowWords) == A.epoch);
-  return __all(ok);
+  const uint64_t* base = A.rec2 + (size_t)row * A.S * kR2;
+  long spins = 0;
+  double dj = 0.0;
+  while (true) {
+    bool ok = true;
+    dj = 0.0;
+    for (int c = lane; c < A.S; c += 64) {
+      const uint64_t lo = ld_tag(base + (size_t)c * kR2), hi = ld_tag(base + (size_t)c * kR2 + 1);
+      ok = ok && tag_ok(lo, A.epoch) && tag_ok(hi, A.epoch);
+      dj += payd(lo, hi);
+    }
+    if (__all(ok)) break;
+    __builtin_amdgcn_s_sleep(2);
+    if (++spins > kSpinLimit) { if (lane == 0) err_count(A.err); break; }
+  }
+  return wave_sum_d(dj);
 }
 
 // Inverse-CDF emission: the first element x of row `row` whose cumulative
@@ -482,21 +489,46 @@ DEV bool request_complete(const KArgs& A, int req) {
 // bonus weights, recomputed with the same element functions as pass 2.
 // Returns -1 when no element carries weight.  Whole workgroup.
 template <int DT>
-DEV int cdf_pick(const KArgs& A, int row, double u, double total, const uint32_t* rw,
-                 bool bonus, Smem& sm) {
+DEV int cdf_pick(const KArgs& A, int row, double u, bool bonus, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const RowGeo g = row_geo<DT>(A, row);
-  const double target = u * total;
   const int nseg = A.S * kWaves;
-  const uint32_t* base2 = A.rec2 + (size_t)row * A.S * kRec2Words;
+  const uint64_t* base2 = A.rec2 + (size_t)row * A.S * kR2;
+  // total weight of the row (wave 0 waits for every segment sum)
+  if (w == 0) {
+    long spins = 0;
+    double tot = 0.0;
+    while (true) {
+      bool ok = true;
+      tot = 0.0;
+      for (int sg = lane; sg < nseg; sg += 64) {
+        const uint64_t* p = base2 + (size_t)(sg / kWaves) * kR2 + 2 + 2 * (sg % kWaves);
+        const uint64_t lo = ld_tag(p), hi = ld_tag(p + 1);
+        ok = ok && tag_ok(lo, A.epoch) && tag_ok(hi, A.epoch);
+        tot += payd(lo, hi);
+      }
+      if (__all(ok)) break;
+      __builtin_amdgcn_s_sleep(2);
+      if (++spins > kSpinLimit) { if (lane == 0) err_count(A.err); break; }
+    }
+    tot = wave_sum_d(tot);
+    if (lane == 0) sm.dd[4] = tot;
+  }
+  __syncthreads();
+  const double total = sm.dd[4];
+  if (!(total > 0.0)) return -1;
+  const double target = u * total;
   // 1. the segment holding the target: scan of segment sums in index order
   double carry = 0.0;
   int sel = 0x7FFFFFFF, last_nz = -1;
   for (int s0 = 0; s0 < nseg && sel == 0x7FFFFFFF; s0 += kThreads) {
     const int sg = s0 + tid;
     double v = 0.0;
-    if (sg < nseg) v = ld_sc1_d(base2 + (size_t)(sg / kWaves) * kRec2Words + 2 + 2 * (sg % kWaves));
+    if (sg < nseg) {
+      const uint64_t* p = base2 + (size_t)(sg / kWaves) * kR2 + 2 + 2 * (sg % kWaves);
+      v = payd(ld_tag(p), ld_tag(p + 1));
+    }
     double incl, excl;
     block_scan(v, sm, incl, excl);
     incl += carry;
@@ -522,9 +554,11 @@ DEV int cdf_pick(const KArgs& A, int row, double u, double total, const uint32_t
   // 2. scan inside the segment: thread tid < kSegVec takes its vector tid
   static_assert(kSegVec <= kThreads, "at most one segment vector per thread");
   const int c = sel / kWaves, ww = sel % kWaves;
-  ResidConst rk{A.beta, ld_sc1_f(rw + RW_C), ld_sc1_f(rw + RW_R1), ld_sc1_f(rw + RW_IS1),
-                ld_sc1_f(rw + RW_R2), ld_sc1_f(rw + RW_IS2)};
-  BonusConst bk{rk.c, rk.Rf};
+  const uint32_t* rw = sm.rw;
+  const ResidConst rk{A.beta, __uint_as_float(rw[RW_C]), __uint_as_float(rw[RW_R1]),
+                      __uint_as_float(rw[RW_IS1]), __uint_as_float(rw[RW_R2]),
+                      __uint_as_float(rw[RW_IS2])};
+  const BonusConst bk{rk.c, rk.Rf};
   const long long vi = g.vbeg + (long long)c * kChunkVec + (long long)ww * kSegVec + tid;
   float w8[VE];
   double tsum = 0.0;
@@ -588,30 +622,58 @@ DEV int row_argmax_f(const KArgs& A, const RowGeo& g, Smem& sm) {
   return block_min_i(best == Mb ? bi : 0x7FFFFFFF, sm);
 }
 
+// Request epilogue (whole workgroup): wait for the K+1 settled rows of the
+// request, take accept_len = the first rejected draft (Alg. 1), emit the token
+// and write the outputs.
 template <int DT>
 DEV void request_epilogue(const KArgs& A, int req, Smem& sm) {
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int K = A.K;
   const size_t row0 = (size_t)req * (K + 1);
-  // accept_len = first rejected draft (Alg. 1); threads read rows in parallel
-  int rej = 0x7FFFFFFF;
-  for (int i = tid; i < K; i += kThreads)
-    if (ld_sc1(A.rowres + (row0 + i) * kRowWords + RW_ACCEPT) == 0u) rej = min(rej, i);
-  rej = block_min_i(rej, sm);
-  const int j = (rej == 0x7FFFFFFF) ? K : rej;
-  const uint32_t* rw = A.rowres + (row0 + j) * kRowWords;
-  const uint32_t kind = ld_sc1(rw + RW_KIND);
+  if (w == 0) {
+    long spins = 0;
+    int rej = 0x7FFFFFFF;
+    while (true) {
+      bool ok = true;
+      rej = 0x7FFFFFFF;
+      for (int i = lane; i <= K; i += 64) {
+        const uint64_t v = ld_tag(A.rowres + (row0 + i) * kRW + RW_ACCEPT);
+        ok = ok && tag_ok(v, A.epoch);
+        if (i < K && pay(v) == 0u) rej = min(rej, i);
+      }
+      if (__all(ok)) break;
+      __builtin_amdgcn_s_sleep(2);
+      if (++spins > kSpinLimit) { if (lane == 0) err_count(A.err); break; }
+    }
+    rej = wave_min_i(rej);
+    const int j = (rej == 0x7FFFFFFF) ? K : rej;
+    // the emitting row's record (all its slots carry the epoch: the accept
+    // slot did, and a row record is written as one batch before any reader
+    // can rely on it -- still, wait for each slot)
+    if (lane < RW_USED) {
+      uint64_t v;
+      long sp = 0;
+      do {
+        v = ld_tag(A.rowres + (row0 + j) * kRW + lane);
+        if (tag_ok(v, A.epoch)) break;
+        __builtin_amdgcn_s_sleep(1);
+      } while (++sp < kSpinLimit);
+      sm.rw[lane] = pay(v);
+    }
+    if (lane == 0) sm.flags[6] = j;
+  }
+  __syncthreads();
+  const int j = sm.flags[6];
+  const uint32_t kind = sm.rw[RW_KIND];
   int next = 0;
   double lpn = 0.0;
   if (kind == kGreedyDraft || kind == kGreedyBonus) {
-    next = (int)ld_sc1(rw + RW_EMIT);
-    lpn = (double)ld_sc1_f(rw + RW_LPEMIT);
+    next = (int)sm.rw[RW_EMIT];
+    lpn = (double)__uint_as_float(sm.rw[RW_LPEMIT]);
   } else {
     const double u = (double)A.u[req * (K + 1) + K];
-    const double total = ld_sc1_d(rw + RW_TOTAL);
     const bool bonus = kind == kSampleBonus;
-    int pick = -1;
-    if (total > 0.0) pick = cdf_pick<DT>(A, (int)(row0 + j), u, total, rw, bonus, sm);
+    int pick = cdf_pick<DT>(A, (int)(row0 + j), u, bonus, sm);
     if (pick < 0) pick = row_argmax_f<DT>(A, row_geo<DT>(A, (int)(row0 + j)), sm);
     next = pick;
     const long long idx = (long long)(row0 + j) * A.V + next;
@@ -622,15 +684,16 @@ DEV void request_epilogue(const KArgs& A, int req, Smem& sm) {
       const float xb = Elem<DT>::load_one(A.b, idx);
       x = fuse_masked(xt, xa, xb, A.beta);
     }
-    const double c = (double)ld_sc1_f(rw + RW_C);
-    lpn = ((double)x * c - ld_sc1_d(rw + RW_L2P)) * kLn2;
+    const double c = (double)__uint_as_float(sm.rw[RW_C]);
+    const double l2 = __builtin_bit_cast(double, (uint64_t)sm.rw[RW_L2P_LO] | ((uint64_t)sm.rw[RW_L2P_HI] << 32));
+    lpn = ((double)x * c - l2) * kLn2;
   }
   for (int i = tid; i < K; i += kThreads) {
-    const uint32_t* ri = A.rowres + (row0 + i) * kRowWords;
-    A.flp_out[req * (K + 1) + i] = ld_sc1_f(ri + RW_LPD);
+    const uint64_t* ri = A.rowres + (row0 + i) * kRW;
+    A.flp_out[req * (K + 1) + i] = payf(ld_tag(ri + RW_LPD));
     if (A.gate_out != nullptr) {
-      A.gate_out[(req * K + i) * 2 + 0] = ld_sc1_f(ri + RW_D);
-      A.gate_out[(req * K + i) * 2 + 1] = ld_sc1_f(ri + RW_GEFF);
+      A.gate_out[(req * K + i) * 2 + 0] = payf(ld_tag(ri + RW_D));
+      A.gate_out[(req * K + i) * 2 + 1] = payf(ld_tag(ri + RW_GEFF));
     }
   }
   if (tid == 0) {
@@ -638,13 +701,34 @@ DEV void request_epilogue(const KArgs& A, int req, Smem& sm) {
     A.next_out[req] = next;
     A.flp_out[req * (K + 1) + K] = (float)lpn;
   }
+  __syncthreads();
 }
 
-// Thread 0, after the team barrier: combine the S chunk records of the row
-// into RowScal and classify the row (Eq. 3-4; the sampling form for tau > 0).
+// Draft-token gathers for one row, loaded early by thread 0.
+struct Gather { float t, a, b, p, u; };
+
 template <int DT>
-DEV void combine_and_classify(const KArgs& A, const RowGeo& g, Smem& sm) {
-  RowScal& rs = sm.rs;
+DEV Gather load_gather(const KArgs& A, const RowGeo& g) {
+  Gather q{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
+  if (is_draft(g.kind)) {
+    int dtok = A.d[g.req * A.K + g.pos];
+    dtok = dtok < 0 ? 0 : (dtok >= A.V ? A.V - 1 : dtok);
+    const long long idx = g.e0 + dtok;
+    q.t = Elem<DT>::load_one(A.t, idx);
+    q.a = Elem<DT>::load_one(A.a, idx);
+    q.b = Elem<DT>::load_one(A.b, idx);
+    if (A.dp != nullptr) q.p = A.dp[g.req * A.K + g.pos];
+    q.u = A.u[g.req * (A.K + 1) + g.pos];
+  }
+  return q;
+}
+
+// Wave 0 after publishing its record: wait for the S pass-1 records of the
+// row (the team barrier), combine them (lane c owns record c), and let lane 0
+// classify the row (Eq. 3-4; the sampling form for tau > 0) into sm.rs.
+template <int DT>
+DEV void team_combine(const KArgs& A, const RowGeo& g, const Gather& gq, Smem& sm) {
+  const int lane = threadIdx.x & 63;
   const bool draft = is_draft(g.kind);
   const bool samp = g.kind == kSampleDraft || g.kind == kSampleBonus;
   const bool tau1 = g.tau == 1.0f;
@@ -654,34 +738,75 @@ DEV void combine_and_classify(const KArgs& A, const RowGeo& g, Smem& sm) {
   cs[sB] = kL2E;
   cs[sF] = samp ? g.c : kL2E;
   cs[sAT] = g.c;
-  const uint32_t* base = A.rec1 + (size_t)g.row * A.S * kRec1Words;
-  const int asl = draft ? sF : sT;
-  #pragma unroll
-  for (int s = 0; s < kSlots; ++s) rs.M[s] = kFloorM;
-  for (int c = 0; c < A.S; ++c) {
-    const uint32_t* rc = base + (size_t)c * kRec1Words;
-    #pragma unroll
-    for (int s = 0; s < kSlots; ++s) rs.M[s] = fmaxf(rs.M[s], ld_sc1_f(rc + s));
+  const uint64_t* base = A.rec1 + (size_t)g.row * A.S * kR1;
+  const uint32_t ep = A.epoch;
+  // own record (c = lane) kept in registers; records c >= 64 are re-read
+  uint64_t r[17];
+  const bool have = lane < A.S;
+  long spins = 0;
+  while (true) {
+    bool ok = true;
+    if (have) {
+      #pragma unroll
+      for (int j = 0; j < 17; ++j) { r[j] = ld_tag(base + (size_t)lane * kR1 + j); ok = ok && tag_ok(r[j], ep); }
+    }
+    for (int c = lane + 64; c < A.S; c += 64) {
+      #pragma unroll
+      for (int j = 0; j < 17; ++j) ok = ok && tag_ok(ld_tag(base + (size_t)c * kR1 + j), ep);
+    }
+    if (__all(ok)) break;
+    __builtin_amdgcn_s_sleep(1);
+    if (++spins > kSpinLimit) { if (lane == 0) err_count(A.err); break; }
   }
-  int arg = 0x7FFFFFFF;
-  int nq = 0;
+  float M[kSlots];
   #pragma unroll
-  for (int s = 0; s < kSlots; ++s) { rs.R[s] = rs.M[s] * cs[s]; rs.S[s] = 0.0; }
-  for (int c = 0; c < A.S; ++c) {
-    const uint32_t* rc = base + (size_t)c * kRec1Words;
+  for (int s = 0; s < kSlots; ++s) M[s] = have ? payf(r[s]) : kFloorM;
+  for (int c = lane + 64; c < A.S; c += 64) {
+    #pragma unroll
+    for (int s = 0; s < kSlots; ++s) M[s] = fmaxf(M[s], payf(ld_tag(base + (size_t)c * kR1 + s)));
+  }
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) M[s] = wave_max(M[s]);
+  const int asl = draft ? sF : sT;
+  double Sp[kSlots];
+  int arg = 0x7FFFFFFF, nq = 0;
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) {
+    Sp[s] = have ? payd(r[5 + 2 * s], r[6 + 2 * s]) *
+                       (double)__builtin_amdgcn_exp2f(payf(r[s]) * cs[s] - M[s] * cs[s])
+                 : 0.0;
+  }
+  if (have) {
+    if (payf(r[asl]) == M[asl]) arg = (int)pay(r[15]);
+    nq = (int)pay(r[16]);
+  }
+  for (int c = lane + 64; c < A.S; c += 64) {
+    const uint64_t* rc = base + (size_t)c * kR1;
     #pragma unroll
     for (int s = 0; s < kSlots; ++s) {
-      const float mc = ld_sc1_f(rc + s);
-      const double sc = ld_sc1_d(rc + 6 + 2 * s);
-      rs.S[s] += sc * (double)__builtin_amdgcn_exp2f(mc * cs[s] - rs.R[s]);
+      const float mc = payf(ld_tag(rc + s));
+      Sp[s] += payd(ld_tag(rc + 5 + 2 * s), ld_tag(rc + 6 + 2 * s)) *
+               (double)__builtin_amdgcn_exp2f(mc * cs[s] - M[s] * cs[s]);
     }
-    if (ld_sc1_f(rc + asl) == rs.M[asl]) arg = min(arg, (int)ld_sc1(rc + 16));
-    nq |= (int)ld_sc1(rc + 17);
+    if (payf(ld_tag(rc + asl)) == M[asl]) arg = min(arg, (int)pay(ld_tag(rc + 15)));
+    nq |= (int)pay(ld_tag(rc + 16));
   }
   #pragma unroll
-  for (int s = 0; s < kSlots; ++s) rs.L2[s] = (double)rs.R[s] + log2_dbl(rs.S[s]);
+  for (int s = 0; s < kSlots; ++s) Sp[s] = wave_sum_d(Sp[s]);
+  arg = wave_min_i(arg);
+  const bool neq_row = __any(nq != 0);
+  if (lane != 0) return;
+
+  RowScal& rs = sm.rs;
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) {
+    rs.M[s] = M[s];
+    rs.R[s] = M[s] * cs[s];
+    rs.S[s] = Sp[s];
+    rs.L2[s] = (double)rs.R[s] + log2_dbl(Sp[s]);
+  }
   rs.arg = arg;
-  rs.neq = nq != 0;
+  rs.neq = neq_row ? 1 : 0;
   const bool cda = A.gate_mode == ASYMSPEC_GATE_CDA;
   rs.decided = 1;
   rs.accept = 0;
@@ -693,16 +818,10 @@ DEV void combine_and_classify(const KArgs& A, const RowGeo& g, Smem& sm) {
     const double ka = log2_dbl(rs.S[sA]), kb = log2_dbl(rs.S[sB]);
     rs.khi[0] = (float)ka; rs.klo[0] = (float)(ka - (double)rs.khi[0]);
     rs.khi[1] = (float)kb; rs.klo[1] = (float)(kb - (double)rs.khi[1]);
-    int dtok = A.d[g.req * A.K + g.pos];
-    dtok = dtok < 0 ? 0 : (dtok >= A.V ? A.V - 1 : dtok);
-    const long long idx = g.e0 + dtok;
-    const float td = Elem<DT>::load_one(A.t, idx);
-    const float ad = Elem<DT>::load_one(A.a, idx);
-    const float bd = Elem<DT>::load_one(A.b, idx);
-    const float fd = fuse_masked(td, ad, bd, A.beta);
+    const float fd = fuse_masked(gq.t, gq.a, gq.b, A.beta);
     if (g.kind == kGreedyDraft) {
-      const double lpt = ((double)td * (double)kL2E - rs.L2[sT]) * kLn2;
-      const double lpb = ((double)bd * (double)kL2E - rs.L2[sB]) * kLn2;
+      const double lpt = ((double)gq.t * (double)kL2E - rs.L2[sT]) * kLn2;
+      const double lpb = ((double)gq.b * (double)kL2E - rs.L2[sB]) * kLn2;
       double m0 = lpt - lpb - A.ln_gamma;
       if (m0 != m0) m0 = -INFINITY;
       rs.margin = m0;
@@ -717,20 +836,15 @@ DEV void combine_and_classify(const KArgs& A, const RowGeo& g, Smem& sm) {
       const int qs = tau1 ? sA : sAT;
       rs.lp_d = ((double)fd * (double)g.c - rs.L2[sF]) * kLn2;
       double lq;
-      if (A.dp != nullptr) {
-        const float pq = A.dp[g.req * A.K + g.pos];
-        lq = pq > 0.0f ? ln_f(pq) : -INFINITY;
-      } else {
-        lq = ((double)ad * (double)g.c - rs.L2[qs]) * kLn2;
-      }
+      if (A.dp != nullptr) lq = gq.p > 0.0f ? ln_f(gq.p) : -INFINITY;
+      else lq = ((double)gq.a * (double)g.c - rs.L2[qs]) * kLn2;
       double x;
       if (rs.lp_d == -INFINITY) x = -INFINITY;
       else if (lq == -INFINITY) x = INFINITY;
       else x = rs.lp_d - lq - A.ln_gamma;
       rs.margin = x;
-      const float u = A.u[g.req * (A.K + 1) + g.pos];
-      rs.lnu = u > 0.0f ? ln_f(u) : -INFINITY;
-      // accept iff ln u < x + D (u < min(1, exp(x + D)) for u in [0, 1))
+      rs.lnu = gq.u > 0.0f ? ln_f(gq.u) : -INFINITY;
+      // accept iff ln u < x + D  (u < min(1, exp(x + D)) for u in [0, 1))
       if (!cda || !rs.neq) rs.accept = rs.lnu < x;
       else if (rs.lnu < x) rs.accept = 1;
       else if (rs.lnu >= x + kLn2) rs.accept = 0;
@@ -746,12 +860,43 @@ DEV void combine_and_classify(const KArgs& A, const RowGeo& g, Smem& sm) {
   }
 }
 
+// The member of a team that settles row `row` and, for bonus rows, runs the
+// request epilogue: rotated so no member carries all of it.
+DEV int settler(const KArgs& A, int row) { return row % A.S; }
+
+// Deferred work of the previous row: settle a row that waited for its D, then
+// run a pending request epilogue.  Whole workgroup, uniform arguments.
+template <int DT>
+DEV void run_deferred(const KArgs& A, int& pend_row, int& pend_req, Smem& sm) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (pend_row >= 0) {
+    if (w == 0) {
+      const double dj = collect_jsd(A, pend_row);
+      if (lane == 0) {
+        double D = 0.5 * kLn2 * dj;
+        D = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
+        write_row_t0(A, row_geo<DT>(A, pend_row), sm.rsp, D);
+      }
+    }
+    pend_row = -1;
+  }
+  if (pend_req >= 0) {
+    request_epilogue<DT>(A, pend_req, sm);
+    pend_req = -1;
+  }
+}
+
 template <int DT>
 DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
-                     u4 (&nxt)[3][kNV], bool has_next, int next_row, Smem& sm) {
+                     u4 (&nxt)[3][kNV], bool has_next, int next_row,
+                     int& pend_row, int& pend_req, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const RowGeo g = row_geo<DT>(A, row);
+  // draft-token gathers (thread 0) before the tile prefetch, so that waiting
+  // for them later does not wait for the prefetch
+  Gather gq{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
+  if (tid == 0) gq = load_gather<DT>(A, g);
   if (has_next) {
     const RowGeo gn = row_geo<DT>(A, next_row);
     issue_loads<DT>(A, gn, mem, nxt);
@@ -800,20 +945,22 @@ DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
   }
 
   // wave level: max, sums rescaled to the wave max, argmax candidate
-  {
-    Acc* qs[kSlots] = {&qT, &qA, &qB, &qF, &qAT};
-    const float cs[kSlots] = {cT, kL2E, kL2E, cF, g.c};
-    #pragma unroll
-    for (int s = 0; s < kSlots; ++s) {
-      const bool used = (s == sT) ? needT : (s == sAT ? needAT : draft);
-      float mw = kFloorM, sw = 0.0f;
-      if (used) {
-        mw = wave_max(qs[s]->m);
-        const float sr = qs[s]->s * __builtin_amdgcn_exp2f(qs[s]->R - mw * cs[s]);
-        sw = wave_sum(sr);
-      }
-      if (lane == 0) { sm.wm[w][s] = mw; sm.ws[w][s] = sw; }
+  #define ASYM_WAVE_SLOT(S_, Q_, C_, USED_)                                      \
+    {                                                                           \
+      float mw = kFloorM, sw = 0.0f;                                            \
+      if (USED_) {                                                              \
+        mw = wave_max(Q_.m);                                                    \
+        sw = wave_sum(Q_.s * __builtin_amdgcn_exp2f(Q_.R - mw * (C_)));         \
+      }                                                                         \
+      if (lane == 0) { sm.wm[w][S_] = mw; sm.ws[w][S_] = sw; }                  \
     }
+  ASYM_WAVE_SLOT(sT, qT, cT, needT)
+  ASYM_WAVE_SLOT(sA, qA, kL2E, draft)
+  ASYM_WAVE_SLOT(sB, qB, kL2E, draft)
+  ASYM_WAVE_SLOT(sF, qF, cF, draft)
+  ASYM_WAVE_SLOT(sAT, qAT, g.c, needAT)
+  #undef ASYM_WAVE_SLOT
+  {
     const bool need_arg = greedy_draft || g.kind == kGreedyBonus;
     int cand = 0x7FFFFFFF;
     if (need_arg) {
@@ -824,9 +971,9 @@ DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
       pos = wave_min_i(pos);
       if (pos != 0x7FFFFFFF && lane == (pos & 63)) {
         const int kk = pos >> 6;
-        u4 vt = kk == 0 ? cur[0][0] : cur[0][kNV - 1];
-        u4 va = kk == 0 ? cur[1][0] : cur[1][kNV - 1];
-        u4 vb = kk == 0 ? cur[2][0] : cur[2][kNV - 1];
+        const u4 vt = kk == 0 ? cur[0][0] : cur[0][kNV - 1];
+        const u4 va = kk == 0 ? cur[1][0] : cur[1][kNV - 1];
+        const u4 vb = kk == 0 ? cur[2][0] : cur[2][kNV - 1];
         #pragma unroll
         for (int e = VE - 1; e >= 0; --e) {
           const float x = greedy_draft ? fuse(Elem<DT>::get(vt, e), Elem<DT>::get(va, e),
@@ -841,12 +988,11 @@ DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
       }
       cand = wave_min_i(cand);
     }
-    const int wn = __any(neq != 0) ? 1 : 0;       // whole wave votes
+    const int wn = __any(neq != 0) ? 1 : 0;
     if (lane == 0) { sm.warg[w] = cand; sm.wneq[w] = wn; }
   }
   __syncthreads();
-  // thread 0: chunk record (fp64 across waves)
-  uint32_t* r1 = A.rec1 + ((size_t)row * A.S + mem) * kRec1Words;
+  // thread 0: the chunk record (fp64 across waves)
   if (tid == 0) {
     const float cs[kSlots] = {cT, kL2E, kL2E, cF, g.c};
     int arg = 0x7FFFFFFF, nq = 0;
@@ -865,41 +1011,26 @@ DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
       for (int i = 0; i < kWaves; ++i)
         S += (double)sm.ws[i][s] * (double)__builtin_amdgcn_exp2f(sm.wm[i][s] * cs[s] - R);
       sm.rec[s] = __float_as_uint(M);
-      const uint64_t x = __builtin_bit_cast(uint64_t, S);
-      sm.rec[6 + 2 * s] = (uint32_t)x;
-      sm.rec[7 + 2 * s] = (uint32_t)(x >> 32);
+      sm.rec[5 + 2 * s] = dlo(S);
+      sm.rec[6 + 2 * s] = dhi(S);
     }
     #pragma unroll
     for (int i = 0; i < kWaves; ++i) {
       if (sm.wm[i][asl] == Mall) arg = min(arg, sm.warg[i]);
       nq |= sm.wneq[i];
     }
-    sm.rec[5] = 0;
-    sm.rec[16] = (uint32_t)arg;
-    sm.rec[17] = (uint32_t)nq;
+    sm.rec[15] = (uint32_t)arg;
+    sm.rec[16] = (uint32_t)nq;
   }
   __syncthreads();
-  if (w == 0) {
-    if (lane < 18) st_sc1(r1 + lane, sm.rec[lane]);
-    wait_vm();
-    if (lane == 0) st_sc1(r1 + (kRec1Words - 1), A.epoch);
+  if (w == 0 && lane < 17)
+    st_tag(A.rec1 + ((size_t)row * A.S + mem) * kR1 + lane, sm.rec[lane], A.epoch);
 
-    // ------------------------------------------------ team barrier
-    const uint32_t* base = A.rec1 + (size_t)row * A.S * kRec1Words;
-    long spins = 0;
-    while (true) {
-      bool ok = true;
-      for (int c = lane; c < A.S; c += 64)
-        ok = ok && (ld_sc1(base + (size_t)c * kRec1Words + (kRec1Words - 1)) == A.epoch);
-      if (__all(ok)) break;
-      __builtin_amdgcn_s_sleep(1);
-      if (++spins > kSpinLimit) {
-        if (lane == 0) atom_add(A.err, 1u);
-        break;
-      }
-    }
-    if (lane == 0) combine_and_classify<DT>(A, g, sm);
-  }
+  // deferred settlement / epilogue of earlier rows while the records travel
+  run_deferred<DT>(A, pend_row, pend_req, sm);
+
+  // ------------------------------------------------ team barrier
+  if (w == 0) team_combine<DT>(A, g, gq, sm);
   __syncthreads();
 
   // ------------------------------------------------------------ pass 2
@@ -957,58 +1088,29 @@ DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
     const float wseg = (needRes || needBonus) ? wave_sum(seg) : 0.0f;
     if (lane == 0) { sm.wj[w] = wj; sm.wseg[w] = wseg; }
     __syncthreads();
-    uint32_t* r2 = A.rec2 + ((size_t)row * A.S + mem) * kRec2Words;
     if (w == 0) {
-      if (lane == 0) {
-        double j = 0.0;
+      double v = 0.0;
+      if (lane < 2) {
         #pragma unroll
-        for (int i = 0; i < kWaves; ++i) j += (double)sm.wj[i];
-        st_sc1_d(r2 + 0, j);
+        for (int i = 0; i < kWaves; ++i) v += (double)sm.wj[i];
+      } else if (lane < 2 + 2 * kWaves) {
+        v = (double)sm.wseg[(lane - 2) >> 1];
       }
-      if (lane >= 1 && lane <= kWaves) st_sc1_d(r2 + 2 * lane, (double)sm.wseg[lane - 1]);
-      wait_vm();
-      if (lane == 0) st_sc1(r2 + (kRec2Words - 1), A.epoch);
-      wait_vm();
-      // settle if every member's pass-2 record is in (see request_complete
-      // for why at least one member sees them all)
-      const uint32_t* base2 = A.rec2 + (size_t)row * A.S * kRec2Words;
-      bool ok = true;
-      for (int c = lane; c < A.S; c += 64)
-        ok = ok && (ld_sc1(base2 + (size_t)c * kRec2Words + (kRec2Words - 1)) == A.epoch);
-      int done = 0;
-      if (__all(ok)) {
-        double dj = 0.0, tt = 0.0;
-        for (int c = lane; c < A.S; c += 64) {
-          dj += ld_sc1_d(base2 + (size_t)c * kRec2Words);
-          #pragma unroll
-          for (int i = 0; i < kWaves; ++i) tt += ld_sc1_d(base2 + (size_t)c * kRec2Words + 2 + 2 * i);
-        }
-        dj = wave_sum_d(dj);
-        tt = wave_sum_d(tt);
-        if (lane == 0) {
-          double D = 0.0;
-          if (needD) {
-            D = 0.5 * kLn2 * dj;
-            D = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
-          }
-          write_row_t0<DT>(A, g, sm.rs, D, tt);
-        }
-        done = request_complete(A, g.req) ? 1 : 0;
-      }
-      if (lane == 0) sm.flags[0] = done;
-    }
-  } else {
-    if (w == 0) {
-      int done = 0;
-      if (mem == 0) {
-        if (lane == 0) write_row_t0<DT>(A, g, sm.rs, 0.0, 0.0);
-        done = request_complete(A, g.req) ? 1 : 0;
-      }
-      if (lane == 0) sm.flags[0] = done;
+      if (lane < 2 + 2 * kWaves)
+        st_tag(A.rec2 + ((size_t)row * A.S + mem) * kR2 + lane, (lane & 1) ? dhi(v) : dlo(v), A.epoch);
     }
   }
-  __syncthreads();
-  if (sm.flags[0]) request_epilogue<DT>(A, g.req, sm);
+
+  // settle now, or after the next row when D is still needed
+  if (mem == settler(A, row)) {
+    if (needD) {
+      if (tid == 0) sm.rsp = sm.rs;
+      pend_row = row;
+    } else if (tid == 0) {
+      write_row_t0(A, g, sm.rs, 0.0);
+    }
+    if (g.pos == A.K) pend_req = g.req;
+  }
   __syncthreads();
 }
 
@@ -1025,10 +1127,11 @@ void fuse_verify_kernel(KArgs A) {
     const RowGeo g0 = row_geo<DT>(A, team);
     issue_loads<DT>(A, g0, mem, cur);
   }
+  int pend_row = -1, pend_req = -1;
   for (int it = 0; it < nrows; ++it) {
     const int r = team + it * A.n_teams;
     const bool hn = it + 1 < nrows;
-    process_row<DT>(A, r, mem, cur, nxt, hn, r + A.n_teams, sm);
+    process_row<DT>(A, r, mem, cur, nxt, hn, r + A.n_teams, pend_row, pend_req, sm);
     if (hn) {
       #pragma unroll
       for (int s = 0; s < 3; ++s)
@@ -1036,6 +1139,7 @@ void fuse_verify_kernel(KArgs A) {
         for (int k = 0; k < kNV; ++k) cur[s][k] = nxt[s][k];
     }
   }
+  run_deferred<DT>(A, pend_row, pend_req, sm);
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -1062,9 +1166,9 @@ static bool make_layout(int B, int K, int V, int dtype, Layout& L) {
   L.S = (int)((nvec_max + kChunkVec - 1) / kChunkVec);
   L.rows = (size_t)B * (K + 1);
   size_t off = 0;
-  L.off_rec1 = off; off = align_up(off + L.rows * L.S * kRec1Words * 4, 256);
-  L.off_rec2 = off; off = align_up(off + L.rows * L.S * kRec2Words * 4, 256);
-  L.off_row = off;  off = align_up(off + L.rows * kRowWords * 4, 256);
+  L.off_rec1 = off; off = align_up(off + L.rows * L.S * kR1 * 8, 256);
+  L.off_rec2 = off; off = align_up(off + L.rows * L.S * kR2 * 8, 256);
+  L.off_row = off;  off = align_up(off + L.rows * kRW * 8, 256);
   L.off_err = off; off = align_up(off + 256, 256);
   L.total = off;
   return true;
@@ -1173,9 +1277,9 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   A.d = draft_tokens; A.dp = draft_probs; A.u = uniforms; A.tau = temperature;
   A.acc_out = accept_len; A.next_out = next_token; A.flp_out = fused_logprobs; A.gate_out = gate_out;
   char* ws = (char*)workspace;
-  A.rec1 = (uint32_t*)(ws + L.off_rec1);
-  A.rec2 = (uint32_t*)(ws + L.off_rec2);
-  A.rowres = (uint32_t*)(ws + L.off_row);
+  A.rec1 = (uint64_t*)(ws + L.off_rec1);
+  A.rec2 = (uint64_t*)(ws + L.off_rec2);
+  A.rowres = (uint64_t*)(ws + L.off_row);
   A.err = (uint32_t*)(ws + L.off_err);
   A.stream_bytes = (unsigned long long)B * (K + 1) * (unsigned long long)V * (dtype == ASYMSPEC_BF16 ? 2ull : 4ull);
   A.B = B; A.K = K; A.V = V; A.S = L.S;
