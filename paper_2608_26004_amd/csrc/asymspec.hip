@@ -9,29 +9,35 @@
 // the first rejection or the bonus token.
 //
 // Work decomposition.  A logit row [V] is cut into S chunks of
-// kThreads * kNV 16-byte vectors.  A team of S workgroups owns a sequence of
-// rows; member m always takes chunk m.  Per row:
-//   pass 1   the chunk, loaded once into VGPRs, yields per-chunk max / sum-exp
-//            statistics, fused-logit argmax and an a-vs-b bitwise flag;
-//   barrier  members publish 128-byte records tagged with the launch epoch and
-//            wait for all S of the row (relaxed agent-scope loads, no cache
-//            flushes: every cross-workgroup word goes through sc1 accesses);
-//   decide   each member combines the S records and classifies the row as
-//            surely accepted / surely rejected / open, using D in [0, ln 2];
-//   pass 2   only where needed, on the still-resident chunk: the JSD term
-//            (open rows, or when the caller asks for D) and the per-wave sums
-//            of the residual max(0, p~ - q) (sampling rows that may reject) or
-//            of the bonus weights;
-//   finalize the last member to finish pass 2 (atomic counter) settles the
-//            row; the last row of a request to settle runs the request
-//            epilogue: accept_len, the inverse-CDF scan of one 2048-element
-//            segment for sampled emissions, and the outputs.
-// The next row's chunk is prefetched into a second register buffer before
-// pass 1 of the current one, so its HBM latency overlaps pass 1, the barrier
-// and pass 2.
+// kThreads * NV 16-byte vectors.  A team of S workgroups owns a sequence of
+// rows; member m always takes chunk m.  Each workgroup runs a two-stage row
+// pipeline; iteration i
+//   * prefetches the tile of row i+1 into registers,
+//   * runs pass 1 on the tile of row i: per-chunk max / sum-exp statistics
+//     of t, a, b and f, the fused-logit argmax and an a-vs-b bitwise flag,
+//     and publishes them as an epoch-tagged record;
+//   * combines the S records of row i-1 (published one iteration ago, so the
+//     team barrier rarely waits) and classifies that row as surely accepted,
+//     surely rejected or open, using D in [0, ln 2];
+//   * runs pass 2 of row i-1 on its tile, stashed in LDS, only where needed:
+//     the JSD term (open rows, or when the caller asks for D) and per-wave
+//     sums of the residual max(0, p~ - q) (sampling rows that may reject) or
+//     of the bonus weights;
+//   * settles row i-1 (or, when it needed D, row i-2 from its JSD partials);
+//   * stashes the tile of row i in LDS.
+// After the last row each workgroup runs the request epilogues assigned to
+// it: accept_len, the inverse-CDF scan of one wave segment for sampled
+// emissions, and the outputs.
+//
+// Cross-workgroup records are arrays of 64-bit slots whose high word is the
+// launch epoch and low word a payload, written and read with relaxed
+// agent-scope atomics (sc1, no cache flushes).  An aligned 64-bit atomic is
+// single-copy atomic, so a reader that sees the epoch in a slot sees its
+// payload; writers never wait, readers poll until every slot they need is in.
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <chrono>
 #include <cmath>
@@ -48,30 +54,31 @@ namespace asym {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kNV = 2;                         // 16-B vectors per thread per stream
-constexpr int kChunkVec = kThreads * kNV;      // vectors per chunk
-constexpr int kSegVec = 64 * kNV;              // vectors per wave segment
 constexpr float kL2E = 1.44269504088896340736f;
 constexpr double kLn2 = 0.693147180559945309417232121458;
 constexpr float kFloorM = -1.0e30f;            // start value of running maxima
 constexpr uint32_t kBf16NegInf = 0xFF80u;
 constexpr uint32_t kF32NegInf = 0xFF800000u;
-constexpr long kSpinLimit = 1L << 17;          // bounded barrier polls (~0.1 s)
+constexpr long kSpinLimit = 1L << 20;          // bounded polls (tens of ms)
 
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(4))) uint32_t* cptr32;
 
 enum Kind { kGreedyDraft = 0, kSampleDraft = 1, kGreedyBonus = 2, kSampleBonus = 3 };
 enum Slot { sT = 0, sA = 1, sB = 2, sF = 3, sAT = 4, kSlots = 5 };
+// What a team knows, at a row, about the earlier drafts of the same request
+// it processed: all accepted so far, some still open (waiting for D), or one
+// surely rejected.
+enum { kReqOpen = 0, kReqUnknown = 1, kReqRejected = 2 };
 
-// ---------------------------------------------------------------- kernel args
-// Cross-workgroup records are arrays of 64-bit slots: the high word is the
-// launch epoch, the low word the payload.  An aligned 64-bit atomic store is
-// single-copy atomic, so a reader that sees the current epoch in a slot also
-// sees its payload; writers never wait for their stores, readers poll until
-// every slot they need carries the epoch.
-constexpr int kR1 = 20;   // pass-1 chunk record slots (17 used)
+
+constexpr int kR1 = 16;   // pass-1 chunk record slots (12 used)
 constexpr int kR2 = 12;   // pass-2 chunk record slots (10 used)
 constexpr int kRW = 16;   // settled-row record slots (14 used)
+
+// pass-1 record payloads: M[5] (fp32 max), S[5] (fp32 sum-exp relative to
+// fl(M * c)), argmax, a-vs-b flag
+enum { P1_M = 0, P1_S = 5, P1_ARG = 10, P1_NEQ = 11, P1_USED = 12 };
 
 struct KArgs {
   const void* t; const void* a; const void* b;
@@ -80,7 +87,7 @@ struct KArgs {
   uint64_t* rec1; uint64_t* rec2; uint64_t* rowres;
   uint32_t* err;
   unsigned long long stream_bytes;   // bytes of each logit array
-  int B, K, V, S, n_teams, rows;
+  int B, K, V, S, n_teams, rows, grid;
   float beta, gamma; int gate_mode; int want_gate;
   double ln_gamma;
   uint32_t epoch;
@@ -104,7 +111,6 @@ DEV uint32_t dhi(double x) { return (uint32_t)(__builtin_bit_cast(uint64_t, x) >
 DEV void err_count(const uint32_t* e) {
   __hip_atomic_fetch_add(const_cast<uint32_t*>(e), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-
 
 DEV __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned long long nbytes) {
   unsigned long long n = nbytes > 0xFFFFFFFFull ? 0xFFFFFFFFull : nbytes;
@@ -160,6 +166,8 @@ DEV float fuse_masked(float t, float a, float b, float beta) {
   float f = fuse(t, a, b, beta);
   return (f != f) ? -INFINITY : f;
 }
+
+// ------------------------------------------------------------- reductions
 
 // ------------------------------------------------------------- reductions
 // Wave64 reductions with gfx9 DPP patterns: xor-1 and xor-2 quad
@@ -221,6 +229,10 @@ struct RowGeo {
   long long vbeg, vend;       // row's 16-B vector range (vend exclusive)
 };
 
+DEV float sload_f32(const void* base, long long idx) {
+  return __uint_as_float(((cptr32)base)[idx]);
+}
+
 template <int DT>
 DEV RowGeo row_geo(const KArgs& A, int row) {
   constexpr int VE = Elem<DT>::VE;
@@ -228,7 +240,7 @@ DEV RowGeo row_geo(const KArgs& A, int row) {
   g.row = row;
   g.req = row / (A.K + 1);
   g.pos = row - g.req * (A.K + 1);
-  g.tau = A.tau[g.req];
+  g.tau = sload_f32(A.tau, g.req);
   const bool samp = g.tau > 0.0f;
   const bool bonus = g.pos == A.K;
   g.kind = bonus ? (samp ? kSampleBonus : kGreedyBonus) : (samp ? kSampleDraft : kGreedyDraft);
@@ -239,35 +251,55 @@ DEV RowGeo row_geo(const KArgs& A, int row) {
   return g;
 }
 DEV bool is_draft(int kind) { return kind == kGreedyDraft || kind == kSampleDraft; }
+DEV int n_streams(int kind) { return is_draft(kind) ? 3 : 1; }
 
-// Loads this thread's vectors of chunk `mem` of row g into buf (t always, a
-// and b for draft rows).  Loads are bounds-checked by the buffer resource;
-// the one vector that may run past the end of an array is read by element.
-template <int DT>
-DEV void issue_loads(const KArgs& A, const RowGeo& g, int mem, u4 (&buf)[3][kNV]) {
+// Issues this thread's vector loads of chunk `mem` of row g into buf: t, a
+// and b for draft rows.  Every row issues the same number of loads (bonus
+// rows point the a and b loads at the row's first 16 bytes), so the compiler
+// can wait for a tile without waiting for the prefetch issued after it.
+// Loads are bounds-checked by the buffer resource; the one vector that may
+// run past the end of an array is repaired in sanitize().
+template <int DT, int NV>
+DEV void issue_loads(const KArgs& A, const RowGeo& g, int mem, u4 (&buf)[3][NV]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const long long cv0 = g.vbeg + (long long)mem * (kThreads * NV) + (long long)w * (64 * NV);
+  const unsigned long long rbase = (unsigned long long)g.vbeg * 16ull;
+  const unsigned long long rem = A.stream_bytes - rbase;
+  const bool draft = is_draft(g.kind);
+  const __amdgpu_buffer_rsrc_t r0 = make_rsrc((const char*)A.t + rbase, rem);
+  const __amdgpu_buffer_rsrc_t r1 = make_rsrc((const char*)(draft ? A.a : A.t) + rbase, rem);
+  const __amdgpu_buffer_rsrc_t r2 = make_rsrc((const char*)(draft ? A.b : A.t) + rbase, rem);
+  #pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const uint32_t off = (uint32_t)((cv0 + (long long)k * 64 + lane - g.vbeg) * 16);
+    const uint32_t offab = draft ? off : 0u;
+    buf[0][k] = buf_load(r0, off);
+    buf[1][k] = buf_load(r1, offab);
+    buf[2][k] = buf_load(r2, offab);
+  }
+}
+
+// Replace elements outside [row start, row end) by -inf (a masked token).
+// The vector holding the last bytes of an array, when the array size is not
+// a multiple of 16 bytes, is re-read element by element first.
+template <int DT, int NV>
+DEV void sanitize(const RowGeo& g, const KArgs& A, int mem, u4 (&buf)[3][NV]) {
   constexpr int VE = Elem<DT>::VE;
   constexpr int ES = 16 / VE;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const long long cv0 = g.vbeg + (long long)mem * kChunkVec + (long long)w * kSegVec;
-  const unsigned long long rbase = (unsigned long long)g.vbeg * 16ull;
-  const unsigned long long rem = A.stream_bytes - rbase;
-  const int ns = is_draft(g.kind) ? 3 : 1;
-  const long long last_full = (long long)(A.stream_bytes / 16ull);   // vectors fully inside
+  const long long cv0 = g.vbeg + (long long)mem * (kThreads * NV) + (long long)w * (64 * NV);
+  const int ns = n_streams(g.kind);
+  const long long last_full = (long long)(A.stream_bytes / 16ull);
+  const long long n_el = (long long)(A.stream_bytes / ES);
   #pragma unroll
-  for (int s = 0; s < 3; ++s) {
-    if (s < ns) {
-      const void* src = s == 0 ? A.t : (s == 1 ? A.a : A.b);
-      __amdgpu_buffer_rsrc_t r = make_rsrc((const char*)src + rbase, rem);
+  for (int k = 0; k < NV; ++k) {
+    const long long vi = cv0 + (long long)k * 64 + lane;
+    if (vi >= last_full && vi < g.vend) {
       #pragma unroll
-      for (int k = 0; k < kNV; ++k) {
-        const long long vi = cv0 + (long long)k * 64 + lane;
-        const uint32_t off = (uint32_t)((vi - g.vbeg) * 16);
-        if (vi < last_full || vi >= g.vend) {
-          buf[s][k] = buf_load(r, off);
-        } else {
-          // the array's final, partial vector: read element by element
+      for (int s = 0; s < 3; ++s) {
+        if (s < ns) {
+          const void* src = s == 0 ? A.t : (s == 1 ? A.a : A.b);
           u4 v = {0, 0, 0, 0};
-          const long long n_el = (long long)(A.stream_bytes / ES);
           #pragma unroll
           for (int e = 0; e < VE; ++e) {
             const long long idx = vi * VE + e;
@@ -285,19 +317,7 @@ DEV void issue_loads(const KArgs& A, const RowGeo& g, int mem, u4 (&buf)[3][kNV]
         }
       }
     }
-  }
-}
-
-// Replace elements outside [row start, row end) by -inf (a masked token).
-template <int DT>
-DEV void sanitize(const RowGeo& g, const KArgs& A, int mem, u4 (&buf)[3][kNV]) {
-  constexpr int VE = Elem<DT>::VE;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const long long cv0 = g.vbeg + (long long)mem * kChunkVec + (long long)w * kSegVec;
-  const int ns = is_draft(g.kind) ? 3 : 1;
-  #pragma unroll
-  for (int k = 0; k < kNV; ++k) {
-    const long long first = (cv0 + (long long)k * 64 + lane) * VE;
+    const long long first = vi * VE;
     const long long lo = g.e0 - first;
     const long long hi = g.e0 + A.V - first;
     if (lo > 0 || hi < VE) {
@@ -311,16 +331,22 @@ DEV void sanitize(const RowGeo& g, const KArgs& A, int mem, u4 (&buf)[3][kNV]) {
 }
 
 // Running (max, sum of exp2(x*c - R)) with R = fl(max * c), updated one
-// vector at a time; kb records the first vector that raised the maximum.
-struct Acc { float m, R, s; int kb; };
-DEV void acc_init(Acc& q, float c) { q.m = kFloorM; q.R = kFloorM * c; q.s = 0.0f; q.kb = 0; }
+// vector at a time.  With kTrackArg, pos holds k * VE + e of the first
+// element (in this thread's order) that attains the running maximum.
+struct Acc { float m, R, s; int pos; };
+DEV void acc_init(Acc& q, float c) { q.m = kFloorM; q.R = kFloorM * c; q.s = 0.0f; q.pos = 0; }
 
-template <int VE, bool kClampNaN>
+template <int VE, bool kClampNaN, bool kTrackArg = false>
 DEV void acc_vec(Acc& q, const float (&x)[VE], float c, int k) {
   float vm = x[0];
   #pragma unroll
   for (int e = 1; e < VE; ++e) vm = fmaxf(vm, x[e]);
-  if (vm > q.m) q.kb = k;
+  if (kTrackArg) {
+    int ei = VE - 1;
+    #pragma unroll
+    for (int e = VE - 2; e >= 0; --e) ei = (x[e] == vm) ? e : ei;
+    if (vm > q.m) q.pos = k * VE + ei;
+  }
   const float mn = fmaxf(q.m, vm);
   const float Rn = mn * c;
   const float scale = __builtin_amdgcn_exp2f(q.R - Rn);
@@ -363,6 +389,35 @@ DEV double log2_dbl(double x) {
 }
 DEV double ln_f(float x) { return (double)__builtin_amdgcn_logf(x) * kLn2; }
 
+// Draft-token gathers of one row through the scalar cache (uniform
+// addresses), so that waiting for them never waits for tile loads.
+struct Gather { float t, a, b, p, u; };
+
+template <int DT>
+DEV float sload_elem(const void* base, long long idx) {
+  if (DT == ASYMSPEC_BF16) {
+    const uint32_t w = ((cptr32)base)[idx >> 1];
+    return __uint_as_float((idx & 1) ? (w & 0xFFFF0000u) : (w << 16));
+  }
+  return __uint_as_float(((cptr32)base)[idx]);
+}
+
+template <int DT>
+DEV Gather sgather(const KArgs& A, const RowGeo& g) {
+  Gather q{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
+  if (is_draft(g.kind)) {
+    int dtok = (int)((cptr32)(const void*)A.d)[g.req * A.K + g.pos];
+    dtok = dtok < 0 ? 0 : (dtok >= A.V ? A.V - 1 : dtok);
+    const long long idx = g.e0 + dtok;
+    q.t = sload_elem<DT>(A.t, idx);
+    q.a = sload_elem<DT>(A.a, idx);
+    q.b = sload_elem<DT>(A.b, idx);
+    if (A.dp != nullptr) q.p = sload_f32(A.dp, (long long)g.req * A.K + g.pos);
+    q.u = sload_f32(A.u, (long long)g.req * (A.K + 1) + g.pos);
+  }
+  return q;
+}
+
 // Per-row scalars, computed once by lane 0 after the team barrier.
 struct RowScal {
   float M[kSlots], R[kSlots];
@@ -384,12 +439,12 @@ struct Smem {
   float wj[kWaves];
   float wseg[kWaves];
   uint32_t rec[kR1];
-  RowScal rs;                     // row being processed
-  RowScal rsp;                    // row whose settlement is deferred
+  RowScal rs;                     // row in pass 2
+  RowScal rsp;                    // row whose settlement waits for its JSD partials
   int   flags[8];
   double dd[8];
   double scan[kWaves];
-  uint32_t rw[kWaves * 4];        // epilogue: row-record words of the emitting row
+  uint32_t rw[kWaves * 4];        // epilogue: record of the emitting row
 };
 
 // Inclusive and exclusive prefix sums over the workgroup, in thread order.
@@ -488,9 +543,10 @@ DEV double collect_jsd(const KArgs& A, int row) {
 // weight exceeds u * total; weights are the residual (draft rows) or the
 // bonus weights, recomputed with the same element functions as pass 2.
 // Returns -1 when no element carries weight.  Whole workgroup.
-template <int DT>
+template <int DT, int NV>
 DEV int cdf_pick(const KArgs& A, int row, double u, bool bonus, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
+  constexpr int kSegVec = 64 * NV;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const RowGeo g = row_geo<DT>(A, row);
   const int nseg = A.S * kWaves;
@@ -559,7 +615,7 @@ DEV int cdf_pick(const KArgs& A, int row, double u, bool bonus, Smem& sm) {
                       __uint_as_float(rw[RW_IS1]), __uint_as_float(rw[RW_R2]),
                       __uint_as_float(rw[RW_IS2])};
   const BonusConst bk{rk.c, rk.Rf};
-  const long long vi = g.vbeg + (long long)c * kChunkVec + (long long)ww * kSegVec + tid;
+  const long long vi = g.vbeg + (long long)c * (kThreads * NV) + (long long)ww * kSegVec + tid;
   float w8[VE];
   double tsum = 0.0;
   int last_pos = -1;
@@ -625,7 +681,7 @@ DEV int row_argmax_f(const KArgs& A, const RowGeo& g, Smem& sm) {
 // Request epilogue (whole workgroup): wait for the K+1 settled rows of the
 // request, take accept_len = the first rejected draft (Alg. 1), emit the token
 // and write the outputs.
-template <int DT>
+template <int DT, int NV>
 DEV void request_epilogue(const KArgs& A, int req, Smem& sm) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int K = A.K;
@@ -647,9 +703,6 @@ DEV void request_epilogue(const KArgs& A, int req, Smem& sm) {
     }
     rej = wave_min_i(rej);
     const int j = (rej == 0x7FFFFFFF) ? K : rej;
-    // the emitting row's record (all its slots carry the epoch: the accept
-    // slot did, and a row record is written as one batch before any reader
-    // can rely on it -- still, wait for each slot)
     if (lane < RW_USED) {
       uint64_t v;
       long sp = 0;
@@ -673,7 +726,7 @@ DEV void request_epilogue(const KArgs& A, int req, Smem& sm) {
   } else {
     const double u = (double)A.u[req * (K + 1) + K];
     const bool bonus = kind == kSampleBonus;
-    int pick = cdf_pick<DT>(A, (int)(row0 + j), u, bonus, sm);
+    int pick = cdf_pick<DT, NV>(A, (int)(row0 + j), u, bonus, sm);
     if (pick < 0) pick = row_argmax_f<DT>(A, row_geo<DT>(A, (int)(row0 + j)), sm);
     next = pick;
     const long long idx = (long long)(row0 + j) * A.V + next;
@@ -704,30 +757,11 @@ DEV void request_epilogue(const KArgs& A, int req, Smem& sm) {
   __syncthreads();
 }
 
-// Draft-token gathers for one row, loaded early by thread 0.
-struct Gather { float t, a, b, p, u; };
-
+// Wave 0: wait for the S pass-1 records of the row (the team barrier),
+// combine them (lane c owns record c), and let lane 0 classify the row
+// (Eq. 3-4; the sampling form for tau > 0) into sm.rs.
 template <int DT>
-DEV Gather load_gather(const KArgs& A, const RowGeo& g) {
-  Gather q{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
-  if (is_draft(g.kind)) {
-    int dtok = A.d[g.req * A.K + g.pos];
-    dtok = dtok < 0 ? 0 : (dtok >= A.V ? A.V - 1 : dtok);
-    const long long idx = g.e0 + dtok;
-    q.t = Elem<DT>::load_one(A.t, idx);
-    q.a = Elem<DT>::load_one(A.a, idx);
-    q.b = Elem<DT>::load_one(A.b, idx);
-    if (A.dp != nullptr) q.p = A.dp[g.req * A.K + g.pos];
-    q.u = A.u[g.req * (A.K + 1) + g.pos];
-  }
-  return q;
-}
-
-// Wave 0 after publishing its record: wait for the S pass-1 records of the
-// row (the team barrier), combine them (lane c owns record c), and let lane 0
-// classify the row (Eq. 3-4; the sampling form for tau > 0) into sm.rs.
-template <int DT>
-DEV void team_combine(const KArgs& A, const RowGeo& g, const Gather& gq, Smem& sm) {
+DEV void team_combine(const KArgs& A, const RowGeo& g, const Gather& gq, int status, Smem& sm) {
   const int lane = threadIdx.x & 63;
   const bool draft = is_draft(g.kind);
   const bool samp = g.kind == kSampleDraft || g.kind == kSampleBonus;
@@ -741,18 +775,18 @@ DEV void team_combine(const KArgs& A, const RowGeo& g, const Gather& gq, Smem& s
   const uint64_t* base = A.rec1 + (size_t)g.row * A.S * kR1;
   const uint32_t ep = A.epoch;
   // own record (c = lane) kept in registers; records c >= 64 are re-read
-  uint64_t r[17];
+  uint64_t r[P1_USED];
   const bool have = lane < A.S;
   long spins = 0;
   while (true) {
     bool ok = true;
     if (have) {
       #pragma unroll
-      for (int j = 0; j < 17; ++j) { r[j] = ld_tag(base + (size_t)lane * kR1 + j); ok = ok && tag_ok(r[j], ep); }
+      for (int j = 0; j < P1_USED; ++j) { r[j] = ld_tag(base + (size_t)lane * kR1 + j); ok = ok && tag_ok(r[j], ep); }
     }
     for (int c = lane + 64; c < A.S; c += 64) {
       #pragma unroll
-      for (int j = 0; j < 17; ++j) ok = ok && tag_ok(ld_tag(base + (size_t)c * kR1 + j), ep);
+      for (int j = 0; j < P1_USED; ++j) ok = ok && tag_ok(ld_tag(base + (size_t)c * kR1 + j), ep);
     }
     if (__all(ok)) break;
     __builtin_amdgcn_s_sleep(1);
@@ -760,10 +794,10 @@ DEV void team_combine(const KArgs& A, const RowGeo& g, const Gather& gq, Smem& s
   }
   float M[kSlots];
   #pragma unroll
-  for (int s = 0; s < kSlots; ++s) M[s] = have ? payf(r[s]) : kFloorM;
+  for (int s = 0; s < kSlots; ++s) M[s] = have ? payf(r[P1_M + s]) : kFloorM;
   for (int c = lane + 64; c < A.S; c += 64) {
     #pragma unroll
-    for (int s = 0; s < kSlots; ++s) M[s] = fmaxf(M[s], payf(ld_tag(base + (size_t)c * kR1 + s)));
+    for (int s = 0; s < kSlots; ++s) M[s] = fmaxf(M[s], payf(ld_tag(base + (size_t)c * kR1 + P1_M + s)));
   }
   #pragma unroll
   for (int s = 0; s < kSlots; ++s) M[s] = wave_max(M[s]);
@@ -772,24 +806,26 @@ DEV void team_combine(const KArgs& A, const RowGeo& g, const Gather& gq, Smem& s
   int arg = 0x7FFFFFFF, nq = 0;
   #pragma unroll
   for (int s = 0; s < kSlots; ++s) {
-    Sp[s] = have ? payd(r[5 + 2 * s], r[6 + 2 * s]) *
-                       (double)__builtin_amdgcn_exp2f(payf(r[s]) * cs[s] - M[s] * cs[s])
+    Sp[s] = have ? (double)payf(r[P1_S + s]) *
+                       (double)__builtin_amdgcn_exp2f(payf(r[P1_M + s]) * cs[s] - M[s] * cs[s])
                  : 0.0;
   }
+  const float Masl = draft ? M[sF] : M[sT];
   if (have) {
-    if (payf(r[asl]) == M[asl]) arg = (int)pay(r[15]);
-    nq = (int)pay(r[16]);
+    const float mine = draft ? payf(r[P1_M + sF]) : payf(r[P1_M + sT]);
+    if (mine == Masl) arg = (int)pay(r[P1_ARG]);
+    nq = (int)pay(r[P1_NEQ]);
   }
   for (int c = lane + 64; c < A.S; c += 64) {
     const uint64_t* rc = base + (size_t)c * kR1;
     #pragma unroll
     for (int s = 0; s < kSlots; ++s) {
-      const float mc = payf(ld_tag(rc + s));
-      Sp[s] += payd(ld_tag(rc + 5 + 2 * s), ld_tag(rc + 6 + 2 * s)) *
+      const float mc = payf(ld_tag(rc + P1_M + s));
+      Sp[s] += (double)payf(ld_tag(rc + P1_S + s)) *
                (double)__builtin_amdgcn_exp2f(mc * cs[s] - M[s] * cs[s]);
     }
-    if (payf(ld_tag(rc + asl)) == M[asl]) arg = min(arg, (int)pay(ld_tag(rc + 15)));
-    nq |= (int)pay(ld_tag(rc + 16));
+    if (payf(ld_tag(rc + P1_M + asl)) == Masl) arg = min(arg, (int)pay(ld_tag(rc + P1_ARG)));
+    nq |= (int)pay(ld_tag(rc + P1_NEQ));
   }
   #pragma unroll
   for (int s = 0; s < kSlots; ++s) Sp[s] = wave_sum_d(Sp[s]);
@@ -858,51 +894,31 @@ DEV void team_combine(const KArgs& A, const RowGeo& g, const Gather& gq, Smem& s
   } else if (g.kind == kGreedyBonus) {
     rs.lp_emit = ((double)rs.M[sT] * (double)kL2E - rs.L2[sT]) * kLn2;
   }
+  if (status == kReqRejected) {
+    // an earlier draft of this request is already rejected: this row cannot
+    // emit and its own decision does not matter (Alg. 1 stops at the first
+    // rejection); D is still computed when the caller asks for it
+    rs.decided = 1;
+    rs.accept = 0;
+    rs.needRes = 0;
+    rs.needBonus = 0;
+    rs.needD = draft && rs.neq && A.want_gate;
+  }
 }
 
-// The member of a team that settles row `row` and, for bonus rows, runs the
-// request epilogue: rotated so no member carries all of it.
+// The member of a team that settles a row: rotated over the members.
 DEV int settler(const KArgs& A, int row) { return row % A.S; }
 
-// Deferred work of the previous row: settle a row that waited for its D, then
-// run a pending request epilogue.  Whole workgroup, uniform arguments.
-template <int DT>
-DEV void run_deferred(const KArgs& A, int& pend_row, int& pend_req, Smem& sm) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (pend_row >= 0) {
-    if (w == 0) {
-      const double dj = collect_jsd(A, pend_row);
-      if (lane == 0) {
-        double D = 0.5 * kLn2 * dj;
-        D = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
-        write_row_t0(A, row_geo<DT>(A, pend_row), sm.rsp, D);
-      }
-    }
-    pend_row = -1;
-  }
-  if (pend_req >= 0) {
-    request_epilogue<DT>(A, pend_req, sm);
-    pend_req = -1;
-  }
-}
+// Fused logit with beta = 1: fl(1 * d) = d, so this is bit-identical to fuse().
+DEV float fuse1(float t, float a, float b) { return __fadd_rn(t, __fsub_rn(a, b)); }
 
-template <int DT>
-DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
-                     u4 (&nxt)[3][kNV], bool has_next, int next_row,
-                     int& pend_row, int& pend_req, Smem& sm) {
+typedef uint64_t u2l __attribute__((ext_vector_type(2)));
+
+// Pass 1 on the register tile of row g; publishes the chunk record.
+template <int DT, int NV, bool kBeta1>
+DEV void pass1(const KArgs& A, const RowGeo& g, int mem, const u4 (&cur)[3][NV], Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const RowGeo g = row_geo<DT>(A, row);
-  // draft-token gathers (thread 0) before the tile prefetch, so that waiting
-  // for them later does not wait for the prefetch
-  Gather gq{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
-  if (tid == 0) gq = load_gather<DT>(A, g);
-  if (has_next) {
-    const RowGeo gn = row_geo<DT>(A, next_row);
-    issue_loads<DT>(A, gn, mem, nxt);
-  }
-  sanitize<DT>(g, A, mem, cur);
-
   const bool draft = is_draft(g.kind);
   const bool samp = g.kind == kSampleDraft || g.kind == kSampleBonus;
   const bool greedy_draft = g.kind == kGreedyDraft;
@@ -911,36 +927,61 @@ DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
   const float cT = samp ? g.c : kL2E;
   const float cF = samp ? g.c : kL2E;
 
-  // ---------------------------------------------------------- pass 1
   Acc qT, qA, qB, qF, qAT;
   acc_init(qT, cT); acc_init(qA, kL2E); acc_init(qB, kL2E); acc_init(qF, cF); acc_init(qAT, g.c);
-  uint32_t neq = 0;
+  bool neqb = false;
   if (draft) {
     #pragma unroll
-    for (int k = 0; k < kNV; ++k) {
+    for (int k = 0; k < NV; ++k) {
       float xt[VE], xa[VE], xb[VE], xf[VE];
       #pragma unroll
       for (int e = 0; e < VE; ++e) {
         xt[e] = Elem<DT>::get(cur[0][k], e);
         xa[e] = Elem<DT>::get(cur[1][k], e);
         xb[e] = Elem<DT>::get(cur[2][k], e);
-        xf[e] = fuse(xt[e], xa[e], xb[e], A.beta);
+        xf[e] = kBeta1 ? fuse1(xt[e], xa[e], xb[e]) : fuse(xt[e], xa[e], xb[e], A.beta);
       }
-      #pragma unroll
-      for (int j = 0; j < 4; ++j) neq |= cur[1][k][j] ^ cur[2][k][j];
-      if (greedy_draft) acc_vec<VE, false>(qT, xt, cT, k);
+      const u2l va = __builtin_bit_cast(u2l, cur[1][k]), vb = __builtin_bit_cast(u2l, cur[2][k]);
+      neqb = neqb | (va.x != vb.x) | (va.y != vb.y);
+      if (greedy_draft) {
+        acc_vec<VE, false>(qT, xt, cT, k);
+        acc_vec<VE, false, true>(qF, xf, cF, k);
+      } else {
+        acc_vec<VE, false>(qF, xf, cF, k);
+      }
       acc_vec<VE, false>(qA, xa, kL2E, k);
       acc_vec<VE, false>(qB, xb, kL2E, k);
-      acc_vec<VE, true>(qF, xf, cF, k);
       if (needAT) acc_vec<VE, false>(qAT, xa, g.c, k);
+      // one vector's temporaries at a time: keeps the tile buffers in VGPRs
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // A fused logit that is not a number (a = b = -inf, a masked token) makes
+    // the f sum NaN; only then redo it with the NaN-clamping exponent.
+    // The tile is passed through an empty asm first: otherwise the compiler
+    // reuses the decoded elements of the loop above and keeps all of them
+    // live until this test.
+    if (qF.s != qF.s) {
+      acc_init(qF, cF);
+      #pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        u4 vt = cur[0][k], va = cur[1][k], vb = cur[2][k];
+        asm volatile("" : "+v"(vt), "+v"(va), "+v"(vb));
+        float xf[VE];
+        #pragma unroll
+        for (int e = 0; e < VE; ++e)
+          xf[e] = fuse(Elem<DT>::get(vt, e), Elem<DT>::get(va, e), Elem<DT>::get(vb, e), A.beta);
+        if (greedy_draft) acc_vec<VE, true, true>(qF, xf, cF, k);
+        else acc_vec<VE, true>(qF, xf, cF, k);
+      }
     }
   } else {
     #pragma unroll
-    for (int k = 0; k < kNV; ++k) {
+    for (int k = 0; k < NV; ++k) {
       float xt[VE];
       #pragma unroll
       for (int e = 0; e < VE; ++e) xt[e] = Elem<DT>::get(cur[0][k], e);
-      acc_vec<VE, false>(qT, xt, cT, k);
+      if (g.kind == kGreedyBonus) acc_vec<VE, false, true>(qT, xt, cT, k);
+      else acc_vec<VE, false>(qT, xt, cT, k);
     }
   }
 
@@ -964,35 +1005,22 @@ DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
     const bool need_arg = greedy_draft || g.kind == kGreedyBonus;
     int cand = 0x7FFFFFFF;
     if (need_arg) {
-      const Acc& qa = greedy_draft ? qF : qT;
-      const float mw = wave_max(qa.m);
-      // lowest vector position (k*64 + lane) whose maximum equals the wave's
-      int pos = (qa.m == mw && mw > kFloorM) ? (qa.kb * 64 + lane) : 0x7FFFFFFF;
-      pos = wave_min_i(pos);
-      if (pos != 0x7FFFFFFF && lane == (pos & 63)) {
-        const int kk = pos >> 6;
-        const u4 vt = kk == 0 ? cur[0][0] : cur[0][kNV - 1];
-        const u4 va = kk == 0 ? cur[1][0] : cur[1][kNV - 1];
-        const u4 vb = kk == 0 ? cur[2][0] : cur[2][kNV - 1];
-        #pragma unroll
-        for (int e = VE - 1; e >= 0; --e) {
-          const float x = greedy_draft ? fuse(Elem<DT>::get(vt, e), Elem<DT>::get(va, e),
-                                              Elem<DT>::get(vb, e), A.beta)
-                                       : Elem<DT>::get(vt, e);
-          if (x == mw) {
-            const long long vi = g.vbeg + (long long)mem * kChunkVec + (long long)w * kSegVec +
-                                 (long long)kk * 64 + lane;
-            cand = (int)(vi * VE + e - g.e0);
-          }
-        }
+      const float qam = greedy_draft ? qF.m : qT.m;
+      const int qpos = greedy_draft ? qF.pos : qT.pos;
+      const float mw = wave_max(qam);
+      if (qam == mw && mw > kFloorM) {
+        // this thread's first maximum: vector k = qpos / VE, element qpos % VE
+        const long long vi = g.vbeg + (long long)mem * (kThreads * NV) + (long long)w * (64 * NV) +
+                             (long long)(qpos / VE) * 64 + lane;
+        cand = (int)(vi * VE + (qpos % VE) - g.e0);
       }
       cand = wave_min_i(cand);
     }
-    const int wn = __any(neq != 0) ? 1 : 0;
+    const int wn = __any(neqb) ? 1 : 0;
     if (lane == 0) { sm.warg[w] = cand; sm.wneq[w] = wn; }
   }
   __syncthreads();
-  // thread 0: the chunk record (fp64 across waves)
+  // thread 0: the chunk record (fp64 across waves, fp32 payloads)
   if (tid == 0) {
     const float cs[kSlots] = {cT, kL2E, kL2E, cF, g.c};
     int arg = 0x7FFFFFFF, nq = 0;
@@ -1010,136 +1038,206 @@ DEV void process_row(const KArgs& A, int row, int mem, u4 (&cur)[3][kNV],
       #pragma unroll
       for (int i = 0; i < kWaves; ++i)
         S += (double)sm.ws[i][s] * (double)__builtin_amdgcn_exp2f(sm.wm[i][s] * cs[s] - R);
-      sm.rec[s] = __float_as_uint(M);
-      sm.rec[5 + 2 * s] = dlo(S);
-      sm.rec[6 + 2 * s] = dhi(S);
+      sm.rec[P1_M + s] = __float_as_uint(M);
+      sm.rec[P1_S + s] = __float_as_uint((float)S);
     }
     #pragma unroll
     for (int i = 0; i < kWaves; ++i) {
       if (sm.wm[i][asl] == Mall) arg = min(arg, sm.warg[i]);
       nq |= sm.wneq[i];
     }
-    sm.rec[15] = (uint32_t)arg;
-    sm.rec[16] = (uint32_t)nq;
+    sm.rec[P1_ARG] = (uint32_t)arg;
+    sm.rec[P1_NEQ] = (uint32_t)nq;
   }
   __syncthreads();
-  if (w == 0 && lane < 17)
-    st_tag(A.rec1 + ((size_t)row * A.S + mem) * kR1 + lane, sm.rec[lane], A.epoch);
-
-  // deferred settlement / epilogue of earlier rows while the records travel
-  run_deferred<DT>(A, pend_row, pend_req, sm);
-
-  // ------------------------------------------------ team barrier
-  if (w == 0) team_combine<DT>(A, g, gq, sm);
-  __syncthreads();
-
-  // ------------------------------------------------------------ pass 2
-  const int needD = sm.rs.needD, needRes = sm.rs.needRes, needBonus = sm.rs.needBonus;
-  if (needD || needRes || needBonus) {
-    float accj = 0.0f, seg = 0.0f;
-    if (needD || needRes) {
-      const float kahi = sm.rs.khi[0], kalo = sm.rs.klo[0];
-      const float kbhi = sm.rs.khi[1], kblo = sm.rs.klo[1];
-      const float Ra = sm.rs.R[sA], Rb = sm.rs.R[sB];
-      const ResidConst rk{A.beta, g.c, sm.rs.R[sF], sm.rs.isF, sm.rs.Rq, sm.rs.isQ};
-      #pragma unroll
-      for (int k = 0; k < kNV; ++k) {
-        float vj[VE], vr[VE];
-        #pragma unroll
-        for (int e = 0; e < VE; ++e) {
-          const float xt = Elem<DT>::get(cur[0][k], e);
-          const float xa = Elem<DT>::get(cur[1][k], e);
-          const float xb = Elem<DT>::get(cur[2][k], e);
-          vj[e] = 0.0f;
-          vr[e] = 0.0f;
-          if (needD) {
-            // P log2(2P/(P+Q)) + Q log2(2Q/(P+Q)) with lp = log2 P, lq = log2 Q
-            const float lp = (fmaxf(__builtin_fmaf(xa, kL2E, -Ra), kFloorM) - kahi) - kalo;
-            const float lq = (fmaxf(__builtin_fmaf(xb, kL2E, -Rb), kFloorM) - kbhi) - kblo;
-            const float P = __builtin_amdgcn_exp2f(lp);
-            const float Q = __builtin_amdgcn_exp2f(lq);
-            const float gg = 1.0f - __builtin_amdgcn_logf(fmaxf(P + Q, 1e-37f));
-            vj[e] = __builtin_fmaf(P, lp + gg, Q * (lq + gg));
-          }
-          if (needRes) vr[e] = resid_elem(xt, xa, xb, rk);
-        }
-        #pragma unroll
-        for (int st = 1; st < VE; st <<= 1)
-          #pragma unroll
-          for (int e = 0; e + st < VE; e += 2 * st) { vj[e] += vj[e + st]; vr[e] += vr[e + st]; }
-        accj += vj[0];
-        seg += vr[0];
-      }
-    } else {
-      const BonusConst bk{g.c, sm.rs.R[sT]};
-      #pragma unroll
-      for (int k = 0; k < kNV; ++k) {
-        float vb[VE];
-        #pragma unroll
-        for (int e = 0; e < VE; ++e) vb[e] = bonus_elem(Elem<DT>::get(cur[0][k], e), bk);
-        #pragma unroll
-        for (int st = 1; st < VE; st <<= 1)
-          #pragma unroll
-          for (int e = 0; e + st < VE; e += 2 * st) vb[e] += vb[e + st];
-        seg += vb[0];
-      }
-    }
-    const float wj = needD ? wave_sum(accj) : 0.0f;
-    const float wseg = (needRes || needBonus) ? wave_sum(seg) : 0.0f;
-    if (lane == 0) { sm.wj[w] = wj; sm.wseg[w] = wseg; }
-    __syncthreads();
-    if (w == 0) {
-      double v = 0.0;
-      if (lane < 2) {
-        #pragma unroll
-        for (int i = 0; i < kWaves; ++i) v += (double)sm.wj[i];
-      } else if (lane < 2 + 2 * kWaves) {
-        v = (double)sm.wseg[(lane - 2) >> 1];
-      }
-      if (lane < 2 + 2 * kWaves)
-        st_tag(A.rec2 + ((size_t)row * A.S + mem) * kR2 + lane, (lane & 1) ? dhi(v) : dlo(v), A.epoch);
-    }
-  }
-
-  // settle now, or after the next row when D is still needed
-  if (mem == settler(A, row)) {
-    if (needD) {
-      if (tid == 0) sm.rsp = sm.rs;
-      pend_row = row;
-    } else if (tid == 0) {
-      write_row_t0(A, g, sm.rs, 0.0);
-    }
-    if (g.pos == A.K) pend_req = g.req;
-  }
-  __syncthreads();
+  if (w == 0 && lane < P1_USED)
+    st_tag(A.rec1 + ((size_t)g.row * A.S + mem) * kR1 + lane, sm.rec[lane], A.epoch);
 }
 
+// Pass-2 partial sums of one thread over its stashed tile: the JSD term
+// (kD) and/or the residual weights (kR).
+template <int DT, int NV, bool kD, bool kR>
+DEV void pass2_sums(const KArgs& A, const RowGeo& g, const u4* stash, const Smem& sm,
+                    float& accj, float& seg) {
+  constexpr int VE = Elem<DT>::VE;
+  const int tid = threadIdx.x;
+  const float kahi = sm.rs.khi[0], kalo = sm.rs.klo[0];
+  const float kbhi = sm.rs.khi[1], kblo = sm.rs.klo[1];
+  const float Ra = sm.rs.R[sA], Rb = sm.rs.R[sB];
+  const ResidConst rk{A.beta, g.c, sm.rs.R[sF], sm.rs.isF, sm.rs.Rq, sm.rs.isQ};
+  #pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const u4 va = stash[(1 * NV + k) * kThreads + tid];
+    const u4 vb = stash[(2 * NV + k) * kThreads + tid];
+    u4 vt = va;
+    if (kR) vt = stash[(0 * NV + k) * kThreads + tid];
+    float vj[VE], vr[VE];
+    #pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      const float xa = Elem<DT>::get(va, e);
+      const float xb = Elem<DT>::get(vb, e);
+      vj[e] = 0.0f;
+      vr[e] = 0.0f;
+      if (kD) {
+        // P log2(2P/(P+Q)) + Q log2(2Q/(P+Q)) with lp = log2 P, lq = log2 Q
+        const float lp = (fmaxf(__builtin_fmaf(xa, kL2E, -Ra), kFloorM) - kahi) - kalo;
+        const float lq = (fmaxf(__builtin_fmaf(xb, kL2E, -Rb), kFloorM) - kbhi) - kblo;
+        const float P = __builtin_amdgcn_exp2f(lp);
+        const float Q = __builtin_amdgcn_exp2f(lq);
+        const float gg = 1.0f - __builtin_amdgcn_logf(fmaxf(P + Q, 1e-37f));
+        vj[e] = __builtin_fmaf(P, lp + gg, Q * (lq + gg));
+      }
+      if (kR) vr[e] = resid_elem(Elem<DT>::get(vt, e), xa, xb, rk);
+    }
+    #pragma unroll
+    for (int st = 1; st < VE; st <<= 1)
+      #pragma unroll
+      for (int e = 0; e + st < VE; e += 2 * st) { vj[e] += vj[e + st]; vr[e] += vr[e + st]; }
+    accj += vj[0];
+    seg += vr[0];
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Pass 2 of row g on its tile in the LDS stash (thread-private slots), when
+// the row needs it; publishes the chunk's pass-2 record.
+template <int DT, int NV>
+DEV void pass2(const KArgs& A, const RowGeo& g, int mem, const u4* stash, Smem& sm) {
+  constexpr int VE = Elem<DT>::VE;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int needD = sm.rs.needD, needRes = sm.rs.needRes, needBonus = sm.rs.needBonus;
+  if (!(needD || needRes || needBonus)) return;
+  float accj = 0.0f, seg = 0.0f;
+  if (needD && needRes) pass2_sums<DT, NV, true, true>(A, g, stash, sm, accj, seg);
+  else if (needD) pass2_sums<DT, NV, true, false>(A, g, stash, sm, accj, seg);
+  else if (needRes) pass2_sums<DT, NV, false, true>(A, g, stash, sm, accj, seg);
+  else {
+    const BonusConst bk{g.c, sm.rs.R[sT]};
+    #pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const u4 vt = stash[(0 * NV + k) * kThreads + tid];
+      float vb[VE];
+      #pragma unroll
+      for (int e = 0; e < VE; ++e) vb[e] = bonus_elem(Elem<DT>::get(vt, e), bk);
+      #pragma unroll
+      for (int st = 1; st < VE; st <<= 1)
+        #pragma unroll
+        for (int e = 0; e + st < VE; e += 2 * st) vb[e] += vb[e + st];
+      seg += vb[0];
+    }
+  }
+  const float wj = needD ? wave_sum(accj) : 0.0f;
+  const float wseg = (needRes || needBonus) ? wave_sum(seg) : 0.0f;
+  if (lane == 0) { sm.wj[w] = wj; sm.wseg[w] = wseg; }
+  __syncthreads();
+  if (w == 0) {
+    double v = 0.0;
+    if (lane < 2) {
+      #pragma unroll
+      for (int i = 0; i < kWaves; ++i) v += (double)sm.wj[i];
+    } else if (lane < 2 + 2 * kWaves) {
+      v = (double)sm.wseg[(lane - 2) >> 1];
+    }
+    if (lane < 2 + 2 * kWaves)
+      st_tag(A.rec2 + ((size_t)g.row * A.S + mem) * kR2 + lane, (lane & 1) ? dhi(v) : dlo(v), A.epoch);
+  }
+}
+
+// Settlement of a row whose D waited for the JSD partials of all members.
 template <int DT>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4)))
+DEV void settle_pending(const KArgs& A, int row, Smem& sm) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (w == 0) {
+    const double dj = collect_jsd(A, row);
+    if (lane == 0) {
+      double D = 0.5 * kLn2 * dj;
+      D = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
+      write_row_t0(A, row_geo<DT>(A, row), sm.rsp, D);
+    }
+  }
+}
+
+#ifndef ASYMSPEC_WAVES
+#define ASYMSPEC_WAVES 2
+#endif
+template <int DT, int NV, bool kBeta1>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ASYMSPEC_WAVES)))
 void fuse_verify_kernel(KArgs A) {
   __shared__ Smem sm;
+  __shared__ u4 stash[3 * NV * kThreads];
   const int team = blockIdx.x / A.S;
   const int mem = blockIdx.x - team * A.S;
-  const int nrows = (A.rows - team + A.n_teams - 1) / A.n_teams;
-  if (team >= A.n_teams || nrows <= 0) return;
-  u4 cur[3][kNV], nxt[3][kNV];
-  {
-    const RowGeo g0 = row_geo<DT>(A, team);
-    issue_loads<DT>(A, g0, mem, cur);
-  }
-  int pend_row = -1, pend_req = -1;
-  for (int it = 0; it < nrows; ++it) {
-    const int r = team + it * A.n_teams;
-    const bool hn = it + 1 < nrows;
-    process_row<DT>(A, r, mem, cur, nxt, hn, r + A.n_teams, pend_row, pend_req, sm);
-    if (hn) {
+  const int tid = threadIdx.x;
+  // each team owns a contiguous block of rows (request-major order), so the
+  // drafts of a request mostly pass through one team in order
+  const int lo = team < A.n_teams ? (int)((long long)team * A.rows / A.n_teams) : 0;
+  const int hi = team < A.n_teams ? (int)((long long)(team + 1) * A.rows / A.n_teams) : 0;
+  const int nrows = hi - lo;
+  u4 cur[3][NV], nxt[3][NV];
+  if (nrows > 0) issue_loads<DT, NV>(A, row_geo<DT>(A, lo), mem, cur);
+  int prev = -1;       // row whose pass 2 is pending (its tile is in the stash)
+  int pend = -1;       // row this workgroup settles once its JSD partials are in
+  int st_req = -1, status = kReqOpen;
+  for (int it = 0; it <= nrows && nrows > 0; ++it) {
+    const bool have = it < nrows;
+    const int r = lo + it;
+    RowGeo gp;
+    Gather gq{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
+    if (prev >= 0) {
+      gp = row_geo<DT>(A, prev);
+      gq = sgather<DT>(A, gp);
+    }
+    RowGeo g;
+    if (have) {
+      g = row_geo<DT>(A, r);
+      if (it + 1 < nrows) issue_loads<DT, NV>(A, row_geo<DT>(A, r + 1), mem, nxt);
+      sanitize<DT, NV>(g, A, mem, cur);
+      pass1<DT, NV, kBeta1>(A, g, mem, cur, sm);
+    }
+    if (pend >= 0) {
+      settle_pending<DT>(A, pend, sm);
+      pend = -1;
+    }
+    if (prev >= 0) {
+      if (gp.req != st_req) { st_req = gp.req; status = kReqOpen; }
+      if ((tid >> 6) == 0) team_combine<DT>(A, gp, gq, status, sm);
+      __syncthreads();
+      pass2<DT, NV>(A, gp, mem, stash, sm);
+      if (is_draft(gp.kind)) {
+        if (sm.rs.decided && !sm.rs.accept) status = kReqRejected;
+        else if (!sm.rs.decided && status == kReqOpen) status = kReqUnknown;
+      }
+      if (mem == settler(A, prev)) {
+        if (sm.rs.needD) {
+          if (tid == 0) sm.rsp = sm.rs;
+          pend = prev;
+        } else if (tid == 0) {
+          write_row_t0(A, gp, sm.rs, 0.0);
+        }
+      }
+    }
+    __syncthreads();
+    if (have) {
+      const int ns = n_streams(g.kind);
+      #pragma unroll
+      for (int s = 0; s < 3; ++s)
+        if (s < ns) {
+          #pragma unroll
+          for (int k = 0; k < NV; ++k) stash[(s * NV + k) * kThreads + tid] = cur[s][k];
+        }
       #pragma unroll
       for (int s = 0; s < 3; ++s)
         #pragma unroll
-        for (int k = 0; k < kNV; ++k) cur[s][k] = nxt[s][k];
+        for (int k = 0; k < NV; ++k) cur[s][k] = nxt[s][k];
     }
+    __syncthreads();
+    prev = have ? r : -1;
   }
-  run_deferred<DT>(A, pend_row, pend_req, sm);
+  if (pend >= 0) {
+    settle_pending<DT>(A, pend, sm);
+    __syncthreads();
+  }
+  for (int req = blockIdx.x; req < A.B; req += A.grid) request_epilogue<DT, NV>(A, req, sm);
 }
 
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -1148,6 +1246,13 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
 }
 
 // ---------------------------------------------------------------- host side
+// 16-byte vectors per thread per stream: four for bf16 (32 logits), four for
+// fp32 (16 logits); a chunk is kThreads * kNVHost vectors.
+#ifndef ASYMSPEC_NV
+#define ASYMSPEC_NV 4
+#endif
+constexpr int kNVHost = ASYMSPEC_NV;
+
 struct Layout {
   int S, VE;
   size_t rows;
@@ -1162,14 +1267,15 @@ static bool make_layout(int B, int K, int V, int dtype, Layout& L) {
   const long double elems = (long double)B * (K + 1) * V;
   if (elems >= (long double)(1ull << 40)) return false;
   L.VE = dtype == ASYMSPEC_BF16 ? 8 : 4;
+  const long long chunk_vec = (long long)kThreads * kNVHost;
   const long long nvec_max = ((long long)V + 2LL * L.VE - 2) / L.VE;
-  L.S = (int)((nvec_max + kChunkVec - 1) / kChunkVec);
+  L.S = (int)((nvec_max + chunk_vec - 1) / chunk_vec);
   L.rows = (size_t)B * (K + 1);
   size_t off = 0;
   L.off_rec1 = off; off = align_up(off + L.rows * L.S * kR1 * 8, 256);
   L.off_rec2 = off; off = align_up(off + L.rows * L.S * kR2 * 8, 256);
   L.off_row = off;  off = align_up(off + L.rows * kRW * 8, 256);
-  L.off_err = off; off = align_up(off + 256, 256);
+  L.off_err = off;  off = align_up(off + 256, 256);
   L.total = off;
   return true;
 }
@@ -1183,6 +1289,14 @@ struct DevInfo {
 static DevInfo g_dev[64];
 static std::mutex g_dev_mu;
 
+static const void* kernel_ptr(int dtype, bool beta1) {
+  if (dtype == ASYMSPEC_BF16)
+    return beta1 ? (const void*)fuse_verify_kernel<ASYMSPEC_BF16, kNVHost, true>
+                 : (const void*)fuse_verify_kernel<ASYMSPEC_BF16, kNVHost, false>;
+  return beta1 ? (const void*)fuse_verify_kernel<ASYMSPEC_FP32, kNVHost, true>
+               : (const void*)fuse_verify_kernel<ASYMSPEC_FP32, kNVHost, false>;
+}
+
 static const DevInfo* device_info() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
@@ -1194,13 +1308,16 @@ static const DevInfo* device_info() {
   if (std::strncmp(pr.gcnArchName, "gfx950", 6) != 0) return nullptr;
   if (!pr.cooperativeLaunch) return nullptr;
   di.n_cu = pr.multiProcessorCount;
-  int nb = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fuse_verify_kernel<ASYMSPEC_BF16>, kThreads, 0) != hipSuccess)
-    return nullptr;
-  di.max_blocks[ASYMSPEC_BF16] = nb * di.n_cu;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fuse_verify_kernel<ASYMSPEC_FP32>, kThreads, 0) != hipSuccess)
-    return nullptr;
-  di.max_blocks[ASYMSPEC_FP32] = nb * di.n_cu;
+  for (int dt = 0; dt < 2; ++dt) {
+    int lo = 1 << 30;
+    for (int b1 = 0; b1 < 2; ++b1) {
+      int nb = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel_ptr(dt, b1 != 0), kThreads, 0) != hipSuccess)
+        return nullptr;
+      lo = std::min(lo, nb);
+    }
+    di.max_blocks[dt] = lo * di.n_cu;
+  }
   di.ok = 1;
   return &di;
 }
@@ -1274,7 +1391,8 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
 
   KArgs A;
   A.t = t; A.a = (K > 0) ? a : t; A.b = (K > 0) ? b : t;
-  A.d = draft_tokens; A.dp = draft_probs; A.u = uniforms; A.tau = temperature;
+  A.d = (K > 0) ? draft_tokens : (const int32_t*)uniforms;
+  A.dp = draft_probs; A.u = uniforms; A.tau = temperature;
   A.acc_out = accept_len; A.next_out = next_token; A.flp_out = fused_logprobs; A.gate_out = gate_out;
   char* ws = (char*)workspace;
   A.rec1 = (uint64_t*)(ws + L.off_rec1);
@@ -1286,20 +1404,16 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   A.rows = (int)L.rows;
   const int teams_fit = gmax / L.S;
   A.n_teams = (int)std::min<long long>((long long)L.rows, teams_fit);
+  A.grid = A.n_teams * L.S;
   A.beta = params->beta; A.gamma = params->gamma; A.gate_mode = params->gate_mode;
   A.want_gate = gate_out != nullptr;
   A.ln_gamma = std::log((double)params->gamma);
   A.epoch = next_epoch();
 
-  const dim3 grid(A.n_teams * A.S), block(kThreads);
+  const dim3 grid(A.grid), block(kThreads);
   void* args[] = {&A};
-  hipError_t e;
-  if (dtype == ASYMSPEC_BF16)
-    e = hipLaunchCooperativeKernel((const void*)fuse_verify_kernel<ASYMSPEC_BF16>, grid, block, args, 0,
-                                   (hipStream_t)stream);
-  else
-    e = hipLaunchCooperativeKernel((const void*)fuse_verify_kernel<ASYMSPEC_FP32>, grid, block, args, 0,
-                                   (hipStream_t)stream);
+  const hipError_t e = hipLaunchCooperativeKernel(kernel_ptr(dtype, params->beta == 1.0f), grid, block, args, 0,
+                                                  (hipStream_t)stream);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return ASYMSPEC_E_DEVICE;
