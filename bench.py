@@ -32,9 +32,12 @@ METRIC = "fused-verify rows/s and achieved HBM GB/s (% of peak), B=128 V=151936 
 
 
 def lib_digest():
+    """Digest of the library sources: traffic figures measured on other
+    sources are not reported."""
     h = hashlib.sha256()
-    for p in (os.path.join(ROOT, "paper_2608_26004_amd", "csrc", "asymspec.hip"),
-              os.path.join(ROOT, "include", "asymspec.h")):
+    csrc = os.path.join(ROOT, "paper_2608_26004_amd", "csrc")
+    paths = sorted(os.path.join(csrc, n) for n in os.listdir(csrc) if n.endswith((".hip", ".h")))
+    for p in paths + [os.path.join(ROOT, "include", "asymspec.h")]:
         with open(p, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]

@@ -78,8 +78,8 @@ typedef struct asymspec_params {
 /* Bytes of device workspace asymspec_fuse_verify needs for this shape
  * (0 for invalid arguments).  The workspace needs no initialisation and may be
  * reused across calls of any shape: every record the kernel exchanges between
- * workgroups is tagged with a per-call epoch.  Calls that may run at the same
- * time need distinct workspaces. */
+ * workgroups, and its work-queue counter, is tagged with a per-call epoch.
+ * Calls that may run at the same time need distinct workspaces. */
 size_t asymspec_workspace_size(int B, int K, int V, int dtype);
 
 /* Zero-fill a workspace on `stream` with a fill kernel (never required for
@@ -103,7 +103,7 @@ int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stre
  *                       emission draw.  Unused for greedy requests, but required.
  *   temperature         tau [B] float; tau <= 0 selects greedy decoding for
  *                       that request (the paper's setting), tau > 0 sampling.
- *   B >= 1, K >= 0, V >= 1, B*(K+1)*V < 2^40
+ *   B >= 1, 0 <= K <= 63, V >= 1, B*(K+1)*V < 2^40
  *   params              see asymspec_params (host pointer)
  *   accept_len          [B] int32 out: number of accepted drafts, in [0, K]
  *   next_token          [B] int32 out: the token emitted after them

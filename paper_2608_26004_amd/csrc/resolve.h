@@ -1,0 +1,595 @@
+// Resolve items of one request: decide, pass 2 and pick.
+//
+// decide  combines the chunk statistics of the request's K+1 rows into their
+//         log-normalisers, gathers the draft tokens' logits, and classifies
+//         each draft with Eq. 4 (or its sampling form) using only the bound
+//         D in [0, ln 2] (Sec. 3.3): surely accepted, surely rejected, or
+//         open (the outcome depends on D).  Alg. 1 stops at the first
+//         rejection, so only the open drafts before the first sure rejection
+//         and the rows that can emit need a second look at the logits.  A
+//         greedy request with nothing open is finished here.
+// pass 2  one chunk of every row that needs it: the JSD partial of Eq. 3 and
+//         the four wave-segment sums of the residual max(0, p~ - q) (sampling
+//         drafts that can emit) or of the bonus weights of softmax(t_K / tau).
+// pick    D for the open drafts, the final accept length, and the emitted
+//         token: the fused argmax (greedy, Eq. 2) or an inverse-CDF draw with
+//         the caller's uniform u_K; then every output of the request.
+
+#ifndef ASYMSPEC_RESOLVE_H_
+#define ASYMSPEC_RESOLVE_H_
+
+#include "device.h"
+
+namespace asym {
+
+DEV uint64_t* dec_hdr(const KArgs& A, int req) {
+  return A.dec + (size_t)req * (kDecHdr + (size_t)(A.K + 1) * kDecRow);
+}
+DEV uint64_t* dec_row(const KArgs& A, int req, int i) {
+  return dec_hdr(A, req) + kDecHdr + (size_t)i * kDecRow;
+}
+DEV uint64_t* p2_rec(const KArgs& A, int req, int i, int m) {
+  return A.rec2 + (((size_t)req * (A.K + 1) + i) * A.S + m) * kR2;
+}
+
+// ------------------------------------------------------------------ decide
+// One wave combines the S chunk records of row g; lane 0 classifies the row
+// and fills sm.rowv[w] with its decision block.  All 64 lanes must call it.
+template <int DT>
+DEV void decide_row(const KArgs& A, const RowGeo& g, Smem& sm) {
+  const int lane = lane_id(), w = wave_id();
+  const int kind = g.kind;
+  const bool draft = kind_draft(kind);
+  const bool samp = kind_samp(kind);
+  float cs[kSlots];
+  cs[sT] = draft ? kL2E : g.c;
+  cs[sA] = kL2E;
+  cs[sB] = kL2E;
+  cs[sF] = g.c;
+  cs[sAT] = g.c;
+  const uint64_t* base = A.rec1 + (size_t)g.row * A.S * kR1;
+  const uint32_t ep = A.epoch;
+  // lane ch holds record ch (ch < 64); records past 64 are re-read below
+  uint64_t r[R1_USED];
+  const bool have = lane < A.S;
+  {
+    Poll pl;
+    while (true) {
+      bool ok = true;
+      if (have) {
+        #pragma unroll
+        for (int j = 0; j < R1_USED; ++j) {
+          r[j] = ld_tag(base + (size_t)lane * kR1 + j);
+          ok = ok && tag_ok(r[j], ep);
+        }
+      }
+      for (int ch = lane + 64; ch < A.S; ch += 64) {
+        #pragma unroll
+        for (int j = 0; j < R1_USED; ++j) ok = ok && tag_ok(ld_tag(base + (size_t)ch * kR1 + j), ep);
+      }
+      if (__all(ok) || !pl.again(A)) break;
+    }
+  }
+  float M[kSlots];
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) M[s] = have ? payf(r[R1_M + s]) : kFloorM;
+  for (int ch = lane + 64; ch < A.S; ch += 64) {
+    #pragma unroll
+    for (int s = 0; s < kSlots; ++s) M[s] = fmaxf(M[s], payf(ld_tag(base + (size_t)ch * kR1 + R1_M + s)));
+  }
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) M[s] = wave_max_all(M[s]);
+  float R[kSlots];
+  double Sp[kSlots];
+  // the argmax slot (f for drafts, t for the bonus row); selects, not
+  // runtime indices, keep the arrays in registers
+  const float Marg = draft ? M[sF] : M[sT];
+  int arg = 0x7FFFFFFF, nq = 0;
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) {
+    R[s] = M[s] * cs[s];
+    Sp[s] = have ? (double)payf(r[R1_S + s]) * exp2((double)(payf(r[R1_M + s]) * cs[s]) - (double)R[s]) : 0.0;
+  }
+  if (have) {
+    const float mine = draft ? payf(r[R1_M + sF]) : payf(r[R1_M + sT]);
+    if (mine == Marg) arg = (int)pay(r[R1_ARG]);
+    nq = (int)pay(r[R1_NEQ]);
+  }
+  for (int ch = lane + 64; ch < A.S; ch += 64) {
+    const uint64_t* rc = base + (size_t)ch * kR1;
+    #pragma unroll
+    for (int s = 0; s < kSlots; ++s) {
+      const float mc = payf(ld_tag(rc + R1_M + s));
+      Sp[s] += (double)payf(ld_tag(rc + R1_S + s)) * exp2((double)(mc * cs[s]) - (double)R[s]);
+    }
+    if (payf(ld_tag(rc + (draft ? R1_M + sF : R1_M + sT))) == Marg) arg = min(arg, (int)pay(ld_tag(rc + R1_ARG)));
+    nq |= (int)pay(ld_tag(rc + R1_NEQ));
+  }
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) Sp[s] = wave_sum_d(Sp[s]);
+  arg = wave_min_i(arg);
+  const bool neq = __any(nq != 0);
+  const Gather gq = sgather<DT>(A, g);
+  if (lane != 0) return;
+
+  double L2[kSlots];
+  #pragma unroll
+  for (int s = 0; s < kSlots; ++s) L2[s] = (double)R[s] + log2_dbl(Sp[s]);
+  const bool cda = A.gate_mode == ASYMSPEC_GATE_CDA;
+  uint32_t* v = sm.rowv[w];
+  #pragma unroll
+  for (int i = 0; i < kDecRow; ++i) v[i] = 0u;
+  int decided = 1, accept = 0;
+  double thr = 0.0;
+  v[D_C] = __float_as_uint(g.c);
+  if (draft) {
+    const double ka = log2_dbl(Sp[sA]), kb = log2_dbl(Sp[sB]);
+    const float kahi = (float)ka, kbhi = (float)kb;
+    v[D_RA] = __float_as_uint(R[sA]);
+    v[D_RB] = __float_as_uint(R[sB]);
+    v[D_KAHI] = __float_as_uint(kahi);
+    v[D_KALO] = __float_as_uint((float)(ka - (double)kahi));
+    v[D_KBHI] = __float_as_uint(kbhi);
+    v[D_KBLO] = __float_as_uint((float)(kb - (double)kbhi));
+    const float fd = fuse_masked(gq.t, gq.a, gq.b, A.beta);
+    if (!samp) {
+      // Eq. 4 in log form: ln p_t(d) - ln p_b(d) - ln gamma + D > 0
+      const double lpt = ((double)gq.t * (double)kL2E - L2[sT]) * kLn2;
+      const double lpb = ((double)gq.b * (double)kL2E - L2[sB]) * kLn2;
+      double m0 = lpt - lpb - A.ln_gamma;
+      if (m0 != m0) m0 = -INFINITY;
+      const double lpd = ((double)fd * (double)kL2E - L2[sF]) * kLn2;
+      v[D_LPD] = __float_as_uint((float)lpd);
+      v[D_LPEMIT] = __float_as_uint((float)(((double)M[sF] * (double)kL2E - L2[sF]) * kLn2));
+      v[D_ARG] = (uint32_t)arg;
+      if (!cda || !neq) accept = m0 > 0.0;
+      else if (m0 > 0.0) accept = 1;
+      else if (m0 + kLn2 <= 0.0) accept = 0;
+      else { decided = 0; thr = -m0; }
+    } else {
+      // accept iff u < min(1, p~(d) / (gamma_eff q(d))), i.e. ln u < x + D
+      const bool t1 = kind == kSampleDraft1;
+      const double L2q = t1 ? L2[sA] : L2[sAT];
+      const double Sq = t1 ? Sp[sA] : Sp[sAT];
+      const float Rq = t1 ? R[sA] : R[sAT];
+      const double lpd = ((double)fd * (double)g.c - L2[sF]) * kLn2;
+      v[D_LPD] = __float_as_uint((float)lpd);
+      double lq;
+      if (A.dp != nullptr) lq = gq.p > 0.0f ? ln_f(gq.p) : -INFINITY;
+      else lq = ((double)gq.a * (double)g.c - L2q) * kLn2;
+      double x;
+      if (lpd == -INFINITY) x = -INFINITY;
+      else if (lq == -INFINITY) x = INFINITY;
+      else x = lpd - lq - A.ln_gamma;
+      const double lnu = gq.u > 0.0f ? ln_f(gq.u) : -INFINITY;
+      if (!cda || !neq) accept = lnu < x;
+      else if (lnu < x) accept = 1;
+      else if (lnu >= x + kLn2) accept = 0;
+      else { decided = 0; thr = lnu - x; }
+      v[D_RF] = __float_as_uint(R[sF]);
+      v[D_ISF] = __float_as_uint((float)(1.0 / Sp[sF]));
+      v[D_RQ] = __float_as_uint(Rq);
+      v[D_ISQ] = __float_as_uint((float)(1.0 / Sq));
+      v[D_L2E_LO] = dlo(L2[sF]);
+      v[D_L2E_HI] = dhi(L2[sF]);
+    }
+  } else {
+    // bonus row (Alg. 1): greedy argmax of t, or a draw from softmax(t / tau)
+    v[D_RF] = __float_as_uint(R[sT]);
+    v[D_L2E_LO] = dlo(L2[sT]);
+    v[D_L2E_HI] = dhi(L2[sT]);
+    v[D_ARG] = (uint32_t)arg;
+    v[D_LPEMIT] = __float_as_uint((float)(((double)M[sT] * (double)g.c - L2[sT]) * kLn2));
+  }
+  v[D_THR_LO] = dlo(thr);
+  v[D_THR_HI] = dhi(thr);
+  v[D_STATUS] = (decided ? kStDecided : 0) | (accept ? kStAccept : 0) | (draft ? kStDraft : 0) |
+                (neq ? kStNeq : 0);
+}
+
+// Every output of request `req`, written by wave 0: lane i < K holds draft
+// i's fused log-probability and D_i.
+DEV void write_outputs(const KArgs& A, int req, int j, int next, float lp_next, float lpd_lane,
+                       double d_lane) {
+  const int lane = lane_id();
+  const int K = A.K;
+  if (lane < K) {
+    A.flp_out[(size_t)req * (K + 1) + lane] = lpd_lane;
+    if (A.gate_out != nullptr) {
+      const bool cda = A.gate_mode == ASYMSPEC_GATE_CDA;
+      const float ge = cda ? A.gamma * __builtin_amdgcn_exp2f((float)(-d_lane * 1.4426950408889634))
+                           : A.gamma;
+      A.gate_out[((size_t)req * K + lane) * 2 + 0] = (float)d_lane;
+      A.gate_out[((size_t)req * K + lane) * 2 + 1] = ge;
+    }
+  }
+  if (lane == 0) {
+    A.acc_out[req] = j;
+    A.next_out[req] = next;
+    A.flp_out[(size_t)req * (K + 1) + K] = lp_next;
+  }
+}
+
+template <int DT>
+DEV void decide_item(const KArgs& A, int req, Smem& sm) {
+  const int lane = lane_id(), w = wave_id();
+  const int K = A.K;
+  const int row0 = req * (K + 1);
+  for (int i = w; i <= K; i += kWaves) {
+    const RowGeo g = row_geo<DT>(A, row0 + i);
+    decide_row<DT>(A, g, sm);
+    __builtin_amdgcn_wave_barrier();
+    const uint32_t val = lane < kDecRow ? sm.rowv[w][lane] : 0u;
+    uint64_t* drow = dec_row(A, req, i);
+    if (lane < D_USED && lane != D_TASK) st_tag(drow + lane, val, A.epoch);
+    if (lane == 0) {
+      sm.rstat[i] = sm.rowv[w][D_STATUS];
+      sm.rarg[i] = sm.rowv[w][D_ARG];
+      sm.rlpe[i] = __uint_as_float(sm.rowv[w][D_LPEMIT]);
+      sm.rlpd[i] = __uint_as_float(sm.rowv[w][D_LPD]);
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+  __syncthreads();
+  if (w != 0) return;
+  // wave 0: lane i looks at row i
+  const float tau = sload_f32(A.tau, req);
+  const bool samp = tau > 0.0f;
+  const bool row_ok = lane <= K;
+  const uint32_t st = row_ok ? sm.rstat[lane] : 0u;
+  const bool is_draft = lane < K;
+  const bool decided = st & kStDecided, accept = st & kStAccept, neq = st & kStNeq;
+  const int jr = wave_min_i(is_draft && decided && !accept ? lane : 0x7FFFFFFF);
+  const int jstar = jr == 0x7FFFFFFF ? K : jr;
+  const bool open = is_draft && lane < jstar && !decided;
+  uint32_t task = 0;
+  if (is_draft && (open || (A.want_gate && neq))) task |= kTaskJsd;
+  if (samp && is_draft && (open || lane == jstar)) task |= kTaskRes;
+  if (samp && lane == K && jstar == K) task |= kTaskBonus;
+  const unsigned long long tmask = __ballot(task != 0);
+  const bool fin = !samp && !__any((task & kTaskJsd) != 0);
+  if (row_ok) st_tag(dec_row(A, req, lane) + D_TASK, task, A.epoch);
+  uint64_t* hdr = dec_hdr(A, req);
+  if (lane == 0) {
+    st_tag(hdr + H_J, (uint32_t)jstar, A.epoch);
+    st_tag(hdr + H_TASK_LO, (uint32_t)tmask, A.epoch);
+    st_tag(hdr + H_TASK_HI, (uint32_t)(tmask >> 32), A.epoch);
+    st_tag(hdr + H_STATE, fin ? kStateFinal : kStatePending, A.epoch);
+  }
+  if (fin) {
+    // greedy with no open draft: accept_len = j*, emit the fused argmax of
+    // row j* (Eq. 2) or the verifier argmax of the bonus row (Alg. 1)
+    const int next = (int)sm.rarg[jstar];
+    const float lpn = sm.rlpe[jstar];
+    write_outputs(A, req, jstar, next, lpn, is_draft ? sm.rlpd[lane] : 0.0f, 0.0);
+  }
+}
+
+// ------------------------------------------------------------------ pass 2
+// Header of request req into sm.hdr (wave 0 polls; whole workgroup returns
+// after a barrier).
+DEV void load_header(const KArgs& A, int req, Smem& sm) {
+  const int lane = lane_id(), w = wave_id();
+  if (w == 0 && lane < H_USED) sm.hdr[lane] = pay(wait_tag(dec_hdr(A, req) + lane, A));
+  __syncthreads();
+}
+// Decision block of row i of request req into sm.cst.
+DEV void load_row_block(const KArgs& A, int req, int i, Smem& sm) {
+  const int lane = lane_id(), w = wave_id();
+  if (w == 0 && lane < D_USED) sm.cst[lane] = pay(wait_tag(dec_row(A, req, i) + lane, A));
+  __syncthreads();
+}
+
+// Pass-2 sums of one thread over its kSegPerLane vectors of a chunk.
+// kMode 0: interior chunk (no masking); 1: masked, branch-free; 2: generic
+// (one vector at a time, array-end repair).
+template <int DT, int kMode>
+DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bool dr, bool db,
+                    const ResidConst& rk, const JsdConst& jk, float& accj, float& seg) {
+  constexpr int VE = Elem<DT>::VE;
+  constexpr int kG = kMode == 2 ? 1 : 4;      // vectors per group
+  const bool nt = dr || db, nab = dj || dr;
+  const __amdgpu_buffer_rsrc_t rt = row_rsrc(A, A.t, g);
+  const __amdgpu_buffer_rsrc_t ra = row_rsrc(A, nab ? A.a : A.t, g);
+  const __amdgpu_buffer_rsrc_t rb = row_rsrc(A, nab ? A.b : A.t, g);
+  #pragma unroll 1
+  for (int k0 = 0; k0 < kSegPerLane; k0 += kG) {
+    u4 vt[kG], va[kG], vb[kG];
+    #pragma unroll
+    for (int k = 0; k < kG; ++k) {
+      const uint32_t off = (uint32_t)((rel0 + (long long)(k0 + k) * 64) * 16);
+      vt[k] = nt ? buf_load(rt, off) : u4{0, 0, 0, 0};
+      va[k] = nab ? buf_load(ra, off) : u4{0, 0, 0, 0};
+      vb[k] = nab ? buf_load(rb, off) : u4{0, 0, 0, 0};
+    }
+    #pragma unroll
+    for (int k = 0; k < kG; ++k) {
+      const long long vi = g.vbeg + rel0 + (long long)(k0 + k) * 64;
+      if (kMode == 1) {
+        mask_vec<DT>(A, g, vi, vt[k]);
+        mask_vec<DT>(A, g, vi, va[k]);
+        mask_vec<DT>(A, g, vi, vb[k]);
+      } else if (kMode == 2) {
+        if (nt) fix_vec<DT>(A, g, A.t, vi, vt[k]);
+        if (nab) {
+          fix_vec<DT>(A, g, A.a, vi, va[k]);
+          fix_vec<DT>(A, g, A.b, vi, vb[k]);
+        }
+      }
+      float vj[VE], vr[VE];
+      #pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        const float xa = Elem<DT>::get(va[k], e), xb = Elem<DT>::get(vb[k], e);
+        const float xt = Elem<DT>::get(vt[k], e);
+        vj[e] = dj ? jsd_elem(xa, xb, jk) : 0.0f;
+        vr[e] = dr ? resid_elem(xt, xa, xb, rk) : (db ? bonus_elem(xt, rk.c, rk.Rf) : 0.0f);
+      }
+      #pragma unroll
+      for (int st = 1; st < VE; st <<= 1)
+        #pragma unroll
+        for (int e = 0; e + st < VE; e += 2 * st) { vj[e] += vj[e + st]; vr[e] += vr[e + st]; }
+      accj += vj[0];
+      seg += vr[0];
+    }
+  }
+}
+
+template <int DT>
+DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
+  constexpr int VE = Elem<DT>::VE;
+  const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
+  load_header(A, req, sm);
+  if (sm.hdr[H_STATE] != kStatePending) return;
+  unsigned long long tmask = (unsigned long long)sm.hdr[H_TASK_LO] | ((unsigned long long)sm.hdr[H_TASK_HI] << 32);
+  while (tmask != 0) {
+    const int i = __builtin_ctzll(tmask);
+    tmask &= tmask - 1;
+    load_row_block(A, req, i, sm);
+    const uint32_t task = sm.cst[D_TASK];
+    const RowGeo g = row_geo<DT>(A, req * (A.K + 1) + i);
+    const bool dj = task & kTaskJsd, dr = task & kTaskRes, db = task & kTaskBonus;
+    const ResidConst rk{A.beta, __uint_as_float(sm.cst[D_C]), __uint_as_float(sm.cst[D_RF]),
+                        __uint_as_float(sm.cst[D_ISF]), __uint_as_float(sm.cst[D_RQ]),
+                        __uint_as_float(sm.cst[D_ISQ])};
+    const JsdConst jk{__uint_as_float(sm.cst[D_RA]), __uint_as_float(sm.cst[D_RB]),
+                      __uint_as_float(sm.cst[D_KAHI]), __uint_as_float(sm.cst[D_KALO]),
+                      __uint_as_float(sm.cst[D_KBHI]), __uint_as_float(sm.cst[D_KBLO])};
+    const long long rel0 = (long long)m * kChunkVec + (long long)w * kSegVec + lane;
+    const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
+    float accj = 0.0f, seg = 0.0f;
+    if (task != 0) {
+      if (has_tail(A, c0, c1))
+        pass2_sums<DT, 2>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+      else if (c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
+        pass2_sums<DT, 0>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+      else
+        pass2_sums<DT, 1>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    }
+    const float wj = wave_sum(accj);
+    const float wseg = wave_sum(seg);
+    if (lane == 0) { sm.wj[w] = wj; sm.wseg[w] = wseg; }
+    __syncthreads();
+    if (w == 0 && lane < P2_USED) {
+      double v = 0.0;
+      if (lane < 2) {
+        #pragma unroll
+        for (int q = 0; q < kWaves; ++q) v += (double)sm.wj[q];
+      } else {
+        v = (double)sm.wseg[(lane - P2_SEG) >> 1];
+      }
+      st_tag(p2_rec(A, req, i, m) + lane, (lane & 1) ? dhi(v) : dlo(v), A.epoch);
+    }
+    __syncthreads();
+  }
+}
+
+// -------------------------------------------------------------------- pick
+// Inverse-CDF draw over row i of request req: the first element x whose
+// cumulative weight exceeds u * total, with the weights of pass 2 (residual
+// for drafts, bonus weights for the bonus row) recomputed by the same element
+// functions.  Row constants are in sm.cst.  Returns -1 when no element
+// carries weight.  Whole workgroup.
+template <int DT>
+DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm) {
+  constexpr int VE = Elem<DT>::VE;
+  constexpr int kPer = kSegVec / kThreads;   // vectors per thread in a segment
+  const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
+  const RowGeo g = row_geo<DT>(A, req * (A.K + 1) + i);
+  const int nseg = A.S * kWaves;
+  // total weight (wave 0 waits for every segment sum)
+  if (w == 0) {
+    double tot = 0.0;
+    for (int sg = lane; sg < nseg; sg += 64) {
+      const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
+      const uint64_t lo = wait_tag(p, A), hi = wait_tag(p + 1, A);
+      tot += payd(lo, hi);
+    }
+    tot = wave_sum_d(tot);
+    if (lane == 0) sm.dd[4] = tot;
+  }
+  __syncthreads();
+  const double total = sm.dd[4];
+  if (!(total > 0.0)) return -1;
+  const double target = u * total;
+  // 1. the segment holding the target: scan of segment sums in index order
+  double carry = 0.0;
+  int sel = 0x7FFFFFFF, last_nz = -1;
+  for (int s0 = 0; s0 < nseg && sel == 0x7FFFFFFF; s0 += kThreads) {
+    const int sg = s0 + tid;
+    double v = 0.0;
+    if (sg < nseg) {
+      const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
+      v = payd(ld_tag(p), ld_tag(p + 1));
+    }
+    double incl, excl;
+    block_scan(v, sm, incl, excl);
+    incl += carry;
+    excl += carry;
+    const int cand = block_min_i((v > 0.0 && incl > target) ? sg : 0x7FFFFFFF, sm);
+    const int lnz = block_min_i(v > 0.0 ? -sg : 0x7FFFFFFF, sm);
+    if (lnz != 0x7FFFFFFF) last_nz = -lnz;
+    __syncthreads();
+    if (sg == cand) sm.dd[6] = excl;
+    if (sg == last_nz) sm.dd[7] = excl;
+    if (tid == kThreads - 1) sm.dd[5] = incl;
+    __syncthreads();
+    carry = sm.dd[5];
+    sel = cand;
+  }
+  if (sel == 0x7FFFFFFF) {
+    if (last_nz < 0) return -1;
+    sel = last_nz;
+    if (tid == 0) sm.dd[6] = sm.dd[7];
+  }
+  __syncthreads();
+  const double before = sm.dd[6];
+  // 2. scan inside the segment: thread tid takes vectors kPer * tid ...
+  const int ch = sel / kWaves, ww = sel % kWaves;
+  const ResidConst rk{A.beta, __uint_as_float(sm.cst[D_C]), __uint_as_float(sm.cst[D_RF]),
+                      __uint_as_float(sm.cst[D_ISF]), __uint_as_float(sm.cst[D_RQ]),
+                      __uint_as_float(sm.cst[D_ISQ])};
+  const __amdgpu_buffer_rsrc_t rt = row_rsrc(A, A.t, g);
+  const __amdgpu_buffer_rsrc_t ra = row_rsrc(A, bonus ? A.t : A.a, g);
+  const __amdgpu_buffer_rsrc_t rb = row_rsrc(A, bonus ? A.t : A.b, g);
+  const long long rel = (long long)ch * kChunkVec + (long long)ww * kSegVec + (long long)kPer * tid;
+  const long long sv0 = g.vbeg + (long long)ch * kChunkVec + (long long)ww * kSegVec;
+  const bool tail = has_tail(A, sv0, sv0 + kSegVec);
+  float wv[kPer * VE];
+  double tsum = 0.0;
+  int last_pos = -1;
+  #pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const uint32_t off = (uint32_t)((rel + k) * 16);
+    const long long vi = g.vbeg + rel + k;
+    u4 vt = buf_load(rt, off), va = buf_load(ra, off), vb = buf_load(rb, off);
+    if (tail) {
+      fix_vec<DT>(A, g, A.t, vi, vt);
+      if (!bonus) {
+        fix_vec<DT>(A, g, A.a, vi, va);
+        fix_vec<DT>(A, g, A.b, vi, vb);
+      }
+    } else {
+      mask_vec<DT>(A, g, vi, vt);
+      mask_vec<DT>(A, g, vi, va);
+      mask_vec<DT>(A, g, vi, vb);
+    }
+    #pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      const float xt = Elem<DT>::get(vt, e);
+      const float x = bonus ? bonus_elem(xt, rk.c, rk.Rf)
+                            : resid_elem(xt, Elem<DT>::get(va, e), Elem<DT>::get(vb, e), rk);
+      wv[k * VE + e] = x;
+      tsum += (double)x;
+      if (x > 0.0f) last_pos = (int)((vi * VE + e) - g.e0);
+    }
+  }
+  double incl, excl;
+  block_scan(tsum, sm, incl, excl);
+  double run = before + excl;
+  int first_ok = 0x7FFFFFFF;
+  #pragma unroll
+  for (int k = 0; k < kPer; ++k)
+    #pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      const float x = wv[k * VE + e];
+      run += (double)x;
+      if (x > 0.0f && run > target && first_ok == 0x7FFFFFFF)
+        first_ok = (int)((g.vbeg + rel + k) * VE + e - g.e0);
+    }
+  int pick = block_min_i(first_ok, sm);
+  if (pick == 0x7FFFFFFF) {
+    // rounding left the target past the segment's own sum: its last nonzero
+    const int neg = block_min_i(last_pos >= 0 ? -last_pos : 0x7FFFFFFF, sm);
+    pick = (neg == 0x7FFFFFFF) ? -1 : -neg;
+  }
+  return pick;
+}
+
+// Argmax of the fused logits of a row by a full scan (whole workgroup); only
+// used when a residual is empty (p~ equal to q in fp32).
+template <int DT>
+DEV int row_argmax_f(const KArgs& A, const RowGeo& g, Smem& sm) {
+  float best = kFloorM;
+  int bi = 0x7FFFFFFF;
+  for (int x = wave_id() * 64 + lane_id(); x < A.V; x += kThreads) {
+    const long long idx = g.e0 + x;
+    const float f = fuse(Elem<DT>::load_one(A.t, idx), Elem<DT>::load_one(A.a, idx),
+                         Elem<DT>::load_one(A.b, idx), A.beta);
+    if (f > best) { best = f; bi = x; }
+  }
+  const float M = wave_max(best);
+  __syncthreads();
+  if (lane_id() == 0) sm.wj[wave_id()] = M;
+  __syncthreads();
+  float Mb = sm.wj[0];
+  #pragma unroll
+  for (int q = 1; q < kWaves; ++q) Mb = fmaxf(Mb, sm.wj[q]);
+  return block_min_i(best == Mb ? bi : 0x7FFFFFFF, sm);
+}
+
+template <int DT>
+DEV void pick_item(const KArgs& A, int req, Smem& sm) {
+  const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
+  const int K = A.K;
+  load_header(A, req, sm);
+  if (sm.hdr[H_STATE] != kStatePending) return;
+  // wave 0: D of the rows that have it, final decisions, the emitting row
+  float lpd = 0.0f;
+  double Dl = 0.0;
+  if (w == 0) {
+    const bool is_draft = lane < K;
+    uint32_t st = 0, task = 0, arg = 0;
+    double thr = 0.0;
+    float lpe = 0.0f;
+    if (lane <= K) {
+      const uint64_t* dr = dec_row(A, req, lane);
+      st = pay(wait_tag(dr + D_STATUS, A));
+      task = pay(wait_tag(dr + D_TASK, A));
+      thr = payd(wait_tag(dr + D_THR_LO, A), wait_tag(dr + D_THR_HI, A));
+      lpd = payf(wait_tag(dr + D_LPD, A));
+      arg = pay(wait_tag(dr + D_ARG, A));
+      lpe = payf(wait_tag(dr + D_LPEMIT, A));
+    }
+    if (task & kTaskJsd) {
+      double s = 0.0;
+      for (int m = 0; m < A.S; ++m) {
+        const uint64_t* p = p2_rec(A, req, lane, m) + P2_J;
+        s += payd(wait_tag(p, A), wait_tag(p + 1, A));
+      }
+      double D = 0.5 * kLn2 * s;   // the partials are in log2 units
+      Dl = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
+    }
+    const bool decided = st & kStDecided;
+    const bool acc = decided ? (st & kStAccept) != 0 : (Dl > thr);
+    const int jr = wave_min_i(is_draft && !acc ? lane : 0x7FFFFFFF);
+    const int j = jr == 0x7FFFFFFF ? K : jr;
+    const int argj = __builtin_amdgcn_readlane((int)arg, j);
+    const float lpej = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lpe), j));
+    if (lane == 0) { sm.flags[0] = j; sm.flags[1] = argj; sm.dd[0] = (double)lpej; }
+  }
+  __syncthreads();
+  const int j = sm.flags[0];
+  const float tau = sload_f32(A.tau, req);
+  int next = sm.flags[1];
+  float lpn = (float)sm.dd[0];
+  if (tau > 0.0f) {
+    load_row_block(A, req, j, sm);
+    const bool bonus = j == K;
+    const double u = (double)A.u[(size_t)req * (K + 1) + K];
+    int pick = cdf_pick<DT>(A, req, j, u, bonus, sm);
+    const RowGeo g = row_geo<DT>(A, req * (K + 1) + j);
+    if (pick < 0) pick = row_argmax_f<DT>(A, g, sm);
+    next = pick;
+    const long long idx = g.e0 + next;
+    float x = Elem<DT>::load_one(A.t, idx);
+    if (!bonus) x = fuse_masked(x, Elem<DT>::load_one(A.a, idx), Elem<DT>::load_one(A.b, idx), A.beta);
+    const double c = (double)__uint_as_float(sm.cst[D_C]);
+    const double l2 = u2d(sm.cst[D_L2E_LO], sm.cst[D_L2E_HI]);
+    lpn = (float)(((double)x * c - l2) * kLn2);
+  }
+  if (w == 0) write_outputs(A, req, j, next, lpn, lpd, Dl);
+}
+
+}  // namespace asym
+
+#endif  // ASYMSPEC_RESOLVE_H_

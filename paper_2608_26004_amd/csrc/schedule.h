@@ -1,0 +1,139 @@
+// Work-item schedule of the fused decision step.
+//
+// Plain C++ (no HIP types) so that the same code runs in the kernel, in the
+// host launcher and in a host-only test.
+//
+// The step is a single ordered list of work items, handed out in order by an
+// atomic counter.  Items are grouped in steps q = 0, 1, 2, ...; step q holds
+//   * the statistics items of request q       ((K+1) * S items: one per row
+//     and vocabulary chunk), when q < B,
+//   * the decide item of request q - L1       (1 item),
+//   * the pass-2 items of request q - L2      (S items, one per chunk),
+//   * the pick item of request q - L3         (1 item),
+// each present only when its request index lies in [0, B).  An item only ever
+// waits for items earlier in the list, so the lowest unfinished item can
+// always proceed.  The lags keep those waits rare: each spans a multiple of
+// the number of items in flight at once.
+//
+// Steps fall into at most 7 runs of equal composition (the boundaries are
+// 0, L1, L2, L3, B, B+L1, B+L2, B+L3); an item index is decoded by finding
+// its run.
+
+#ifndef ASYMSPEC_SCHEDULE_H_
+#define ASYMSPEC_SCHEDULE_H_
+
+#ifndef ASYM_HD
+#define ASYM_HD
+#endif
+
+namespace asym {
+
+enum ItemType { kItemNone = -1, kItemStats = 0, kItemDecide = 1, kItemPass2 = 2, kItemPick = 3 };
+enum PartBits { kPartStats = 1, kPartDecide = 2, kPartPass2 = 4, kPartPick = 8 };
+
+constexpr int kMaxRuns = 8;
+
+struct Sched {
+  int n_runs;
+  int total;              // number of items
+  int L1, L2, L3;
+  int q0[kMaxRuns];       // first step of the run
+  int i0[kMaxRuns];       // index of the run's first item
+  int blk[kMaxRuns];      // items per step in the run (> 0)
+  int parts[kMaxRuns];    // PartBits present in every step of the run
+};
+
+struct Item {
+  int type;   // ItemType
+  int req;    // request index
+  int sub;    // stats: row-in-request * S + chunk; pass 2: chunk; else 0
+};
+
+ASYM_HD inline int sched_parts(int q, int B, int L1, int L2, int L3) {
+  int p = 0;
+  if (q >= 0 && q < B) p |= kPartStats;
+  if (q - L1 >= 0 && q - L1 < B) p |= kPartDecide;
+  if (q - L2 >= 0 && q - L2 < B) p |= kPartPass2;
+  if (q - L3 >= 0 && q - L3 < B) p |= kPartPick;
+  return p;
+}
+
+ASYM_HD inline int sched_block(int parts, int K, int S) {
+  return ((parts & kPartStats) ? (K + 1) * S : 0) + ((parts & kPartDecide) ? 1 : 0) +
+         ((parts & kPartPass2) ? S : 0) + ((parts & kPartPick) ? 1 : 0);
+}
+
+// Lags in steps.  items_in_flight is the number of workgroups; each holds
+// its current item and the next one, and a resolve item that waits holds its
+// workgroup, so each lag spans lag_pct percent of items_in_flight statistics
+// items.  Returns false when the schedule would not fit in 31-bit indices.
+inline bool sched_build(int B, int K, int S, int items_in_flight, Sched& sc, int lag_pct = 400) {
+  if (B < 1 || K < 0 || S < 1 || items_in_flight < 1) return false;
+  // steps hold at least the (K+1) * S statistics items of their request
+  const long long per_step = (long long)(K + 1) * S;
+  const long long span = (long long)items_in_flight * lag_pct / 100;
+  const int window = (int)((span + per_step - 1) / per_step);
+  sc.L1 = window + 1;
+  sc.L2 = sc.L1 + window + 1;
+  sc.L3 = sc.L2 + window + 1;
+  int bp[8] = {0, sc.L1, sc.L2, sc.L3, B, B + sc.L1, B + sc.L2, B + sc.L3};
+  // sort the 8 boundaries (insertion sort) and drop duplicates
+  for (int i = 1; i < 8; ++i)
+    for (int j = i; j > 0 && bp[j - 1] > bp[j]; --j) {
+      const int t = bp[j]; bp[j] = bp[j - 1]; bp[j - 1] = t;
+    }
+  long long idx = 0;
+  sc.n_runs = 0;
+  for (int i = 0; i + 1 < 8; ++i) {
+    const int qa = bp[i], qb = bp[i + 1];
+    if (qb <= qa) continue;
+    const int parts = sched_parts(qa, B, sc.L1, sc.L2, sc.L3);
+    const int blk = sched_block(parts, K, S);
+    if (blk == 0) continue;
+    if (sc.n_runs >= kMaxRuns) return false;
+    sc.q0[sc.n_runs] = qa;
+    sc.i0[sc.n_runs] = (int)idx;
+    sc.blk[sc.n_runs] = blk;
+    sc.parts[sc.n_runs] = parts;
+    ++sc.n_runs;
+    idx += (long long)(qb - qa) * blk;
+    if (idx >= (1LL << 31) - 1) return false;
+  }
+  sc.total = (int)idx;
+  return true;
+}
+
+ASYM_HD inline Item sched_item(const Sched& sc, int K, int S, int idx) {
+  Item it{kItemNone, 0, 0};
+  if (idx < 0 || idx >= sc.total) return it;
+  int r = 0;
+  for (int k = 1; k < sc.n_runs; ++k)
+    if (idx >= sc.i0[k]) r = k;
+  const int off = idx - sc.i0[r];
+  const int blk = sc.blk[r];
+  const int qs = off / blk;
+  int o = off - qs * blk;
+  const int q = sc.q0[r] + qs;
+  const int parts = sc.parts[r];
+  const int ns = (K + 1) * S;
+  if (parts & kPartStats) {
+    if (o < ns) { it.type = kItemStats; it.req = q; it.sub = o; return it; }
+    o -= ns;
+  }
+  if (parts & kPartDecide) {
+    if (o < 1) { it.type = kItemDecide; it.req = q - sc.L1; it.sub = 0; return it; }
+    o -= 1;
+  }
+  if (parts & kPartPass2) {
+    if (o < S) { it.type = kItemPass2; it.req = q - sc.L2; it.sub = o; return it; }
+    o -= S;
+  }
+  it.type = kItemPick;
+  it.req = q - sc.L3;
+  it.sub = 0;
+  return it;
+}
+
+}  // namespace asym
+
+#endif  // ASYMSPEC_SCHEDULE_H_

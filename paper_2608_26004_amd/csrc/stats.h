@@ -1,0 +1,319 @@
+// Statistics item: one vocabulary chunk of one row, streamed once from HBM.
+//
+// Per chunk it produces the maximum and the sum of exp2(x * c - fl(M * c))
+// of every logit stream the row's decision needs (the normalisers of the
+// log-softmaxes in Eq. 3-4, at the row's temperature where the emission
+// distribution needs it), the first index of the chunk's maximum fused logit
+// f = t + beta (a - b) (Eq. 2; greedy drafts) or verifier logit (greedy bonus
+// row, Alg. 1), and whether a and b differ anywhere in the chunk (a row with
+// a == b everywhere has D = 0 exactly).
+//
+// Layout: chunk m of a row covers its vectors [m * kChunkVec, (m+1) *
+// kChunkVec); sub-tile s holds kTileVec of them, wave w a run of 64 * kNV and
+// lane l every 64th from there, so each load instruction of a wave reads 1 KiB
+// of contiguous memory.  Sub-tile s + 1 is loaded while sub-tile s is reduced.
+
+#ifndef ASYMSPEC_STATS_H_
+#define ASYMSPEC_STATS_H_
+
+#include "device.h"
+
+namespace asym {
+
+typedef uint64_t u2l __attribute__((ext_vector_type(2)));
+
+template <int KIND> struct KindTraits;
+template <> struct KindTraits<kGreedyDraft> {
+  static constexpr int NS = 3; static constexpr bool kArg = true; static constexpr int argslot = sF;
+  static constexpr bool kT = true, kF = true, kA = true, kB = true, kAT = false;
+};
+template <> struct KindTraits<kSampleDraft1> {
+  static constexpr int NS = 3; static constexpr bool kArg = false; static constexpr int argslot = sF;
+  static constexpr bool kT = false, kF = true, kA = true, kB = true, kAT = false;
+};
+template <> struct KindTraits<kSampleDraftT> {
+  static constexpr int NS = 3; static constexpr bool kArg = false; static constexpr int argslot = sF;
+  static constexpr bool kT = false, kF = true, kA = true, kB = true, kAT = true;
+};
+template <> struct KindTraits<kGreedyBonus> {
+  static constexpr int NS = 1; static constexpr bool kArg = true; static constexpr int argslot = sT;
+  static constexpr bool kT = true, kF = false, kA = false, kB = false, kAT = false;
+};
+template <> struct KindTraits<kSampleBonus> {
+  static constexpr int NS = 1; static constexpr bool kArg = false; static constexpr int argslot = sT;
+  static constexpr bool kT = true, kF = false, kA = false, kB = false, kAT = false;
+};
+
+// Offset, in vectors from the thread's first vector, of its j-th vector
+// (sub-tile j / kNV, step j % kNV).
+constexpr int vec_rel(int j) { return (j / kNV) * kTileVec + (j % kNV) * 64; }
+#ifndef ASYMSPEC_WIN
+#define ASYMSPEC_WIN 4
+#endif
+constexpr int kWin = ASYMSPEC_WIN;   // vectors per stream in flight per thread
+
+template <int DT, int NS>
+DEV void load_tile(const __amdgpu_buffer_rsrc_t (&r)[3], uint32_t off0, u4 (&buf)[3][kNV]) {
+  #pragma unroll
+  for (int k = 0; k < kNV; ++k) {
+    const uint32_t off = off0 + (uint32_t)(k * 64 * 16);
+    #pragma unroll
+    for (int s = 0; s < NS; ++s) buf[s][k] = buf_load(r[s], off);
+  }
+}
+
+// Per-slot accumulators of one thread.
+struct StatsAcc {
+  Acc T, A, B, F, AT;
+  uint64_t neq;   // lanes that saw a != b (wave-uniform mask)
+};
+
+// Wave partials, cross-wave combine and the tagged chunk record.
+template <int DT, int KIND>
+DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, const StatsAcc& q,
+                       Smem& sm) {
+  using TR = KindTraits<KIND>;
+  constexpr int VE = Elem<DT>::VE;
+  constexpr bool kDraft = TR::NS == 3;
+  const int lane = lane_id(), w = wave_id();
+  const float c = g.c;
+  // wave partials: max, sum rescaled to the wave max
+  #define ASYM_WAVE_SLOT(S_, Q_, C_, USED_)                                  \
+    {                                                                       \
+      float mw = kFloorM, sw = 0.0f;                                        \
+      if (USED_) {                                                          \
+        mw = wave_max(Q_.m);                                                \
+        sw = wave_sum(Q_.s * __builtin_amdgcn_exp2f(Q_.R - mw * (C_)));     \
+      }                                                                     \
+      if (lane == 0) { sm.wm[w][S_] = mw; sm.ws[w][S_] = sw; }              \
+    }
+  ASYM_WAVE_SLOT(sT, q.T, (kDraft ? kL2E : c), TR::kT)
+  ASYM_WAVE_SLOT(sA, q.A, kL2E, TR::kA)
+  ASYM_WAVE_SLOT(sB, q.B, kL2E, TR::kB)
+  ASYM_WAVE_SLOT(sF, q.F, c, TR::kF)
+  ASYM_WAVE_SLOT(sAT, q.AT, c, TR::kAT)
+  #undef ASYM_WAVE_SLOT
+  {
+    int cand = 0x7FFFFFFF;
+    if (TR::kArg) {
+      // the lanes holding the wave maximum re-read the vector where their
+      // running maximum first reached it and take its first such element
+      const Acc& qa = TR::argslot == sF ? q.F : q.T;
+      const float mw = wave_max(qa.m);
+      if (qa.m == mw && mw > kFloorM) {
+        const long long rv = rel0 + vec_rel(qa.pos);
+        const long long vi = g.vbeg + rv;
+        const uint32_t off = (uint32_t)(rv * 16);
+        u4 vt = buf_load(row_rsrc(A, A.t, g), off);
+        fix_vec<DT>(A, g, A.t, vi, vt);
+        u4 va = vt, vb = vt;
+        if (kDraft) {
+          va = buf_load(row_rsrc(A, A.a, g), off);
+          vb = buf_load(row_rsrc(A, A.b, g), off);
+          fix_vec<DT>(A, g, A.a, vi, va);
+          fix_vec<DT>(A, g, A.b, vi, vb);
+        }
+        int ei = VE;
+        #pragma unroll
+        for (int e = VE - 1; e >= 0; --e) {
+          const float xt = Elem<DT>::get(vt, e);
+          const float x = kDraft ? fuse(xt, Elem<DT>::get(va, e), Elem<DT>::get(vb, e), A.beta) : xt;
+          ei = (x == mw) ? e : ei;
+        }
+        if (ei < VE) cand = (int)(vi * VE + ei - g.e0);
+      }
+      cand = wave_min_i(cand);
+    }
+    const int wn = q.neq != 0 ? 1 : 0;
+    if (lane == 0) { sm.warg[w] = cand; sm.wneq[w] = wn; }
+  }
+  __syncthreads();
+  // wave 0: lane s < kSlots combines slot s over the waves; lane kSlots the
+  // argmax and the a-vs-b flag; then the lanes publish the record
+  if (w == 0) {
+    uint64_t* rec = A.rec1 + ((size_t)g.row * A.S + m) * kR1;
+    if (lane < kSlots) {
+      const float cs = (lane == sA || lane == sB || (lane == sT && kDraft)) ? kL2E : c;
+      float M = kFloorM;
+      #pragma unroll
+      for (int i = 0; i < kWaves; ++i) M = fmaxf(M, sm.wm[i][lane]);
+      const float R = M * cs;
+      float S = 0.0f;
+      #pragma unroll
+      for (int i = 0; i < kWaves; ++i) S += sm.ws[i][lane] * __builtin_amdgcn_exp2f(sm.wm[i][lane] * cs - R);
+      st_tag(rec + R1_M + lane, __float_as_uint(M), A.epoch);
+      st_tag(rec + R1_S + lane, __float_as_uint(S), A.epoch);
+    } else if (lane == kSlots) {
+      constexpr int asl = TR::argslot;
+      float Mall = kFloorM;
+      #pragma unroll
+      for (int i = 0; i < kWaves; ++i) Mall = fmaxf(Mall, sm.wm[i][asl]);
+      int arg = 0x7FFFFFFF, nq = 0;
+      #pragma unroll
+      for (int i = 0; i < kWaves; ++i) {
+        if (sm.wm[i][asl] == Mall) arg = min(arg, sm.warg[i]);
+        nq |= sm.wneq[i];
+      }
+      st_tag(rec + R1_ARG, (uint32_t)arg, A.epoch);
+      st_tag(rec + R1_NEQ, (uint32_t)nq, A.epoch);
+    }
+  }
+}
+
+// Ties the accumulator state to this point of the program: without it the
+// compiler sinks the arithmetic of later vectors to the end of the chunk and
+// keeps all their loaded data live at once.
+DEV void pin(Acc& q) { asm volatile("" : "+v"(q.m), "+v"(q.R), "+v"(q.s)); }
+
+// One vector of each stream into the accumulators.
+template <int DT, int KIND, bool kB1, bool kClamp>
+DEV void stats_vec(const KArgs& A, float c, const u4& vt, const u4& va, const u4& vb, int kk, StatsAcc& q) {
+  using TR = KindTraits<KIND>;
+  constexpr int VE = Elem<DT>::VE;
+  float xt[VE];
+  #pragma unroll
+  for (int e = 0; e < VE; ++e) xt[e] = Elem<DT>::get(vt, e);
+  if (TR::NS == 3) {
+    float xa[VE], xb[VE], xf[VE];
+    #pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      xa[e] = Elem<DT>::get(va, e);
+      xb[e] = Elem<DT>::get(vb, e);
+      xf[e] = kB1 ? fuse1(xt[e], xa[e], xb[e]) : fuse(xt[e], xa[e], xb[e], A.beta);
+    }
+    // the compare is folded into a wave mask at once and pinned there: left
+    // to itself the compiler re-materialises it at its only use, keeping
+    // every loaded vector of a and b live to the end of the chunk
+    const u2l pa = __builtin_bit_cast(u2l, va), pb = __builtin_bit_cast(u2l, vb);
+    uint64_t nm = __ballot((pa.x != pb.x) | (pa.y != pb.y));
+    asm volatile("" : "+s"(nm));
+    q.neq |= nm;
+    if (TR::kT) acc_vec<VE, false, false>(q.T, xt, kL2E, kk);
+    acc_vec<VE, kClamp, TR::kArg>(q.F, xf, c, kk);
+    acc_vec<VE, false, false>(q.A, xa, kL2E, kk);
+    acc_vec<VE, false, false>(q.B, xb, kL2E, kk);
+    if (TR::kAT) acc_vec<VE, false, false>(q.AT, xa, c, kk);
+    if (TR::kT) pin(q.T);
+    pin(q.F);
+    pin(q.A);
+    pin(q.B);
+    if (TR::kAT) pin(q.AT);
+  } else {
+    acc_vec<VE, false, TR::kArg>(q.T, xt, c, kk);
+    pin(q.T);
+  }
+}
+
+DEV void stats_init(StatsAcc& q, float c) {
+  acc_init(q.T, c); acc_init(q.A, kL2E); acc_init(q.B, kL2E); acc_init(q.F, c); acc_init(q.AT, c);
+  q.neq = 0;
+}
+
+// Generic path: one vector at a time, every vector repaired (row boundary,
+// array end), NaN-safe exponent for f.  Used for the chunk that holds a
+// ragged array end and to redo a chunk whose f sum came out NaN.
+template <int DT, int KIND, bool kB1>
+DEV void stats_slow(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
+  using TR = KindTraits<KIND>;
+  constexpr bool kDraft = TR::NS == 3;
+  const int lane = lane_id(), w = wave_id();
+  const __amdgpu_buffer_rsrc_t rt = row_rsrc(A, A.t, g);
+  const __amdgpu_buffer_rsrc_t ra = row_rsrc(A, kDraft ? A.a : A.t, g);
+  const __amdgpu_buffer_rsrc_t rb = row_rsrc(A, kDraft ? A.b : A.t, g);
+  const long long rel0 = (long long)m * kChunkVec + (long long)w * (64 * kNV) + lane;
+  StatsAcc q;
+  stats_init(q, g.c);
+  #pragma unroll 1
+  for (int kk = 0; kk < kNSub * kNV; ++kk) {
+    const long long rv = rel0 + (long long)(kk / kNV) * kTileVec + (kk % kNV) * 64;
+    const uint32_t off = (uint32_t)(rv * 16);
+    const long long vi = g.vbeg + rv;
+    u4 vt = buf_load(rt, off), va = vt, vb = vt;
+    fix_vec<DT>(A, g, A.t, vi, vt);
+    if (kDraft) {
+      va = buf_load(ra, off);
+      vb = buf_load(rb, off);
+      fix_vec<DT>(A, g, A.a, vi, va);
+      fix_vec<DT>(A, g, A.b, vi, vb);
+    }
+    stats_vec<DT, KIND, kB1, true>(A, g.c, vt, va, vb, kk, q);
+  }
+  publish_stats<DT, KIND>(A, g, m, rel0, q, sm);
+}
+
+// Fast path; kMask for the first and last chunk of a row (elements outside
+// the row are masked, without branches).  Returns false, without publishing,
+// when the chunk must be redone on the generic path.
+template <int DT, int KIND, bool kB1, bool kMask>
+DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
+  using TR = KindTraits<KIND>;
+  constexpr int VE = Elem<DT>::VE;
+  constexpr int NS = TR::NS;
+  constexpr bool kDraft = NS == 3;
+  const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
+  const float c = g.c;
+  const __amdgpu_buffer_rsrc_t r[3] = {row_rsrc(A, A.t, g), row_rsrc(A, kDraft ? A.a : A.t, g),
+                                       row_rsrc(A, kDraft ? A.b : A.t, g)};
+  // this thread's first vector, relative to the row's first vector
+  const int rel0 = m * kChunkVec + w * (64 * kNV) + lane;
+  const uint32_t off0 = (uint32_t)rel0 * 16u;
+  // the row starts lo_e elements into its first vector
+  const int lo_e = (int)(g.e0 - g.vbeg * VE);
+
+  StatsAcc q;
+  stats_init(q, c);
+  // rolling prefetch: slot j % kWin holds vector j; it is refilled with
+  // vector j + kWin as soon as vector j is reduced
+  constexpr int kVecs = kNSub * kNV;
+  u4 buf[3][kWin];
+  #pragma unroll
+  for (int j = 0; j < kWin; ++j)
+    #pragma unroll
+    for (int s = 0; s < NS; ++s) buf[s][j] = buf_load(r[s], off0 + (uint32_t)(vec_rel(j) * 16));
+  #pragma unroll
+  for (int j = 0; j < kVecs; ++j) {
+    const int sl = j % kWin;
+    if (kMask) {
+      // elements outside the row become -inf (selects, no branches)
+      const int e_lo = lo_e - (rel0 + vec_rel(j)) * VE;
+      const int ilo = min(max(e_lo, 0), VE), ihi = min(max(e_lo + A.V, 0), VE);
+      #pragma unroll
+      for (int s = 0; s < NS; ++s) Elem<DT>::mask_to_neginf(buf[s][sl], ilo, ihi);
+    }
+    // masked elements have a = b = -inf, so f is NaN there: the boundary
+    // chunks clamp the exponent of f
+    stats_vec<DT, KIND, kB1, kMask>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl], buf[NS == 3 ? 2 : 0][sl], j, q);
+    if (j + kWin < kVecs) {
+      #pragma unroll
+      for (int s = 0; s < NS; ++s) buf[s][sl] = buf_load(r[s], off0 + (uint32_t)(vec_rel(j + kWin) * 16));
+    }
+    // one vector's temporaries at a time
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // In an interior chunk a fused logit that is not a number (a = b = -inf:
+  // a token both views mask) makes some thread's f sum NaN; only then is the
+  // chunk redone on the NaN-safe path.  The test is workgroup-wide, so every
+  // thread takes the same path.
+  if (kDraft && !kMask && __syncthreads_or(q.F.s != q.F.s)) return false;
+  publish_stats<DT, KIND>(A, g, m, rel0, q, sm);
+  return true;
+}
+
+template <int DT, int KIND, bool kB1>
+DEV void stats_item(const KArgs& A, int row, int m, Smem& sm) {
+  constexpr int VE = Elem<DT>::VE;
+  const RowGeo g = row_geo<DT>(A, row);
+  const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
+  bool done = false;
+  if (!has_tail(A, c0, c1)) {
+    // a chunk whose vectors lie wholly inside the row needs no masking
+    const bool interior = c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V;
+    done = interior ? stats_fast<DT, KIND, kB1, false>(A, g, m, sm)
+                    : stats_fast<DT, KIND, kB1, true>(A, g, m, sm);
+  }
+  if (!done) stats_slow<DT, KIND, kB1>(A, g, m, sm);
+}
+
+}  // namespace asym
+
+#endif  // ASYMSPEC_STATS_H_

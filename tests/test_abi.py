@@ -39,6 +39,8 @@ def test_workspace_size():
     assert s > 0 and s % 256 == 0
     assert asp.workspace_size(0, 6, 100, asp.BF16) == 0
     assert asp.workspace_size(1, -1, 100, asp.BF16) == 0
+    assert asp.workspace_size(1, 64, 100, asp.BF16) == 0      # K + 1 rows must fit one wave
+    assert asp.workspace_size(1, 63, 100, asp.BF16) > 0
     assert asp.workspace_size(1, 1, 0, asp.BF16) == 0
     assert asp.workspace_size(1, 1, 10, 7) == 0
     assert asp.workspace_size(4, 2, 1000, asp.FP32) >= asp.workspace_size(1, 2, 1000, asp.FP32)
