@@ -55,9 +55,10 @@ def _oracle_worker(reqs):
     return len(reqs)
 
 
-def cpu_baseline(x, max_requests):
+def cpu_baseline(x, max_requests, min_seconds):
     """The oracle over the first `max_requests` requests of the workload, in a
-    fork pool over requests on the host cores; returns rows/s and cores."""
+    fork pool over requests on the host cores, repeated until `min_seconds`
+    of wall time have passed; returns rows/s and the process count."""
     global _CPU_INPUTS
     import multiprocessing as mp
     _CPU_INPUTS = x
@@ -65,14 +66,76 @@ def cpu_baseline(x, max_requests):
     cores = max(1, min(16, len(os.sched_getaffinity(0)), n))
     chunks = [list(range(i, n, cores)) for i in range(cores)]
     ctx = mp.get_context("fork")
-    t0 = time.perf_counter()
+    done = 0
+    passes = 0
     with ctx.Pool(cores) as pool:
-        done = sum(pool.map(_oracle_worker, chunks))
-    wall = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        while True:
+            done += sum(pool.map(_oracle_worker, chunks))
+            passes += 1
+            wall = time.perf_counter() - t0
+            if wall >= min_seconds:
+                break
     rows = done * (x.K + 1)
     return dict(value=rows / wall, unit="rows/s", cores=cores, kind="oracle",
-                sample=f"{done} of {x.B} requests ({rows} rows) of the same workload, "
-                       f"fp64 NumPy oracle, fork pool of {cores} processes, wall {wall:.2f} s")
+                sample=f"{passes} pass(es) over {n} of {x.B} requests ({rows} rows) of the same "
+                       f"workload, fp64 NumPy oracle, fork pool of {cores} processes, "
+                       f"wall {wall:.1f} s")
+
+
+# ----------------------------------------------------------- HBM traffic --
+def _counter_rows(d):
+    """(dispatch id, kernel name, counter value) per dispatch from the
+    rocprofv3 counter-collection CSV under directory d."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    out = {}
+    for fn in files:
+        with open(fn) as f:
+            for row in csv.DictReader(f):
+                key = (fn, int(row["Dispatch_Id"]))
+                val = float(row.get("Counter_Value", 0.0))
+                prev = out.get(key, (row["Kernel_Name"], 0.0))
+                out[key] = (prev[0], prev[1] + val)
+    return [(k[1], v[0], v[1]) for k, v in sorted(out.items())]
+
+
+def write_traffic(fetch_dir, write_dir, workload, copy_bytes):
+    """Per-launch HBM bytes of the fused-verify kernel from two rocprofv3
+    --pmc runs of `bench.py --calibrate-copy` (FETCH_SIZE, then WRITE_SIZE,
+    in KiB per dispatch), each scaled by bytes / KiB that the same counter
+    reads for the plain device copy of `copy_bytes` bytes issued after the
+    timed launches."""
+    res = {}
+    for label, d in (("fetch", fetch_dir), ("write", write_dir)):
+        rows = _counter_rows(d)
+        fv = [(i, v) for i, n, v in rows if "fuse_verify_kernel" in n]
+        if not fv:
+            raise SystemExit(f"{label}: no fused-verify dispatch in {d}")
+        last = max(i for i, _ in fv)
+        cp = [v for i, n, v in rows if i > last and "copy" in n.lower() and v > 1024.0]
+        if not cp:
+            raise SystemExit(f"{label}: no calibration copy after the timed launches in {d}")
+        kib_fv = sum(v for _, v in fv) / len(fv)
+        kib_cp = sum(cp) / len(cp)
+        factor = copy_bytes / (kib_cp * 1024.0)
+        res[label] = dict(kib_per_dispatch=kib_fv, copy_kib_per_dispatch=kib_cp,
+                          bytes_per_counted_byte=factor, bytes=kib_fv * 1024.0 * factor,
+                          dispatches=len(fv))
+    out = dict(source_digest=lib_digest(), workload=workload,
+               bytes_per_launch=res["fetch"]["bytes"] + res["write"]["bytes"],
+               fetch=res["fetch"], write=res["write"], copy_bytes=copy_bytes)
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out))
+
+
+COPY_BYTES = 1 << 30
 
 
 # ------------------------------------------------------------------- main --
@@ -85,6 +148,15 @@ def main():
     ap.add_argument("--gate", action="store_true", help="also return (D, gamma_eff) per row")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-requests", type=int, default=128)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="repeat the oracle sample until this much wall time has passed")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after timing, run a plain 1 GiB device copy 3 times (PMC scale reference)")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of "
+                         "`bench.py --calibrate-copy` into profiles/traffic_<workload>.json")
+    ap.add_argument("--gen-workers", type=int, default=None,
+                    help="processes for the input generator (1 under a profiler)")
     ap.add_argument("--copies", type=int, default=2,
                     help="distinct input copies rotated between steps (cold cache)")
     args = ap.parse_args()
@@ -94,14 +166,17 @@ def main():
         sys.exit(2)
 
     wl = synth.WORKLOADS[args.workload]
+    if args.write_traffic:
+        write_traffic(args.write_traffic[0], args.write_traffic[1], wl.name, COPY_BYTES)
+        return
     t_gen = time.perf_counter()
-    x = synth.workload_inputs(args.workload)
+    x = synth.workload_inputs(args.workload, workers=args.gen_workers)
     t_gen = time.perf_counter() - t_gen
     print(f"[bench] generated {wl.name} in {t_gen:.1f} s", file=sys.stderr, flush=True)
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(x, args.cpu_requests)
+        cpu = cpu_baseline(x, args.cpu_requests, args.cpu_seconds)
         print(f"[bench] cpu baseline {cpu['value']:.1f} rows/s on {cpu['cores']} cores",
               file=sys.stderr, flush=True)
 
@@ -154,6 +229,14 @@ def main():
     rows = B * (K + 1)
     nbytes = x.nbytes_read()
     achieved = nbytes / (kern_ms * 1e-3) / 1e9
+
+    if args.calibrate_copy:
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     acc = outs[0].cpu().numpy()
     traffic = None
