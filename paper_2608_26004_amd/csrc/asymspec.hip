@@ -1,6 +1,6 @@
 // AsymSpec fused decision step for MI355X (gfx950, CDNA4, wave64).
 //
-// One persistent cooperative launch does the whole step of Alg. 1 for every
+// One persistent launch does the whole step of Alg. 1 for every
 // request: the vocabulary-wide statistics of the verifier logits t and the
 // drafter logits a (full view) and b (compressed view), the delta-fused logits
 // f = t + beta (a - b) (Sec. 3.2, Eq. 1-2), the Jensen-Shannon divergence D and
@@ -41,15 +41,17 @@
 
 namespace asym {
 
-// Work queues: kQueues counters, each in its own 128-byte line; workgroup g
-// serves queue g % nq, whose items are the global indices q, q + nq, ...
-// in increasing order, so every queue hands out its items in list order and
-// a queue's lowest unfinished item can always run.  A counter holds (epoch,
-// count); the first workgroup of a launch to touch it raises it to
-// (epoch, 0) with one atomic max (epochs grow within a process), and items
-// are then taken with fetch-add.
+// Work queues: kQueues counters, each in its own 128-byte line, and an
+// arrival counter.  A workgroup serves queue (arrival order) % nq, whose
+// items are the global indices q, q + nq, ... in increasing order.  Every
+// queue is thus served by a running workgroup and hands out its items in
+// list order, so the lowest unfinished item can always run, whether or not
+// the whole grid is resident.  A counter holds (epoch, count); the first
+// workgroup of a launch to touch it raises it to (epoch, 0) with one atomic
+// max (epochs grow within a process), and values are then taken with
+// fetch-add.
 constexpr int kQueues = 8;
-constexpr int kQueueStride = 16;   // 64-bit words between counters
+constexpr int kQueueStride = 16;   // 64-bit words between counters (arrival counter last)
 
 DEV void queue_init(const KArgs& A, uint64_t* ctr) {
   const uint64_t want = (uint64_t)A.epoch << 32;
@@ -68,10 +70,10 @@ DEV void queue_init(const KArgs& A, uint64_t* ctr) {
     if (!pl.again(A)) break;
   }
 }
-DEV uint32_t grab(uint64_t* ctr, int nq, int q) {
-  const uint32_t n = (uint32_t)__hip_atomic_fetch_add(ctr, (uint64_t)1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return n * (uint32_t)nq + (uint32_t)q;
+DEV uint32_t take(uint64_t* ctr) {
+  return (uint32_t)__hip_atomic_fetch_add(ctr, (uint64_t)1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+DEV uint32_t grab(uint64_t* ctr, int nq, int q) { return take(ctr) * (uint32_t)nq + (uint32_t)q; }
 
 template <int DT, bool kB1>
 DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
@@ -100,13 +102,18 @@ void fuse_verify_kernel(KArgs A) {
   __shared__ Smem sm;
   const int tid = threadIdx.x;
   const int nq = min((int)gridDim.x, kQueues);
-  const int q = (int)blockIdx.x % nq;
-  uint64_t* ctr = A.qctr + (size_t)q * kQueueStride;
   if (tid == 0) {
-    queue_init(A, ctr);
-    sm.next[0] = (int)grab(ctr, nq, q);
+    uint64_t* arrive = A.qctr + (size_t)kQueues * kQueueStride;
+    queue_init(A, arrive);
+    const int q = (int)(take(arrive) % (uint32_t)nq);
+    uint64_t* c = A.qctr + (size_t)q * kQueueStride;
+    queue_init(A, c);
+    sm.next[0] = (int)grab(c, nq, q);
+    sm.queue = q;
   }
   __syncthreads();
+  const int q = sm.queue;
+  uint64_t* ctr = A.qctr + (size_t)q * kQueueStride;
   uint32_t cur = (uint32_t)sm.next[0];
   int par = 1;
   while (cur < (uint32_t)A.sc.total) {
@@ -163,7 +170,7 @@ static bool make_layout(int B, int K, int V, int dtype, Layout& L) {
   L.off_rec1 = off; off = align_up(off + L.rows * L.S * kR1 * 8, 256);
   L.off_dec = off;  off = align_up(off + (size_t)B * (kDecHdr + (size_t)(K + 1) * kDecRow) * 8, 256);
   L.off_rec2 = off; off = align_up(off + L.rows * L.S * kR2 * 8, 256);
-  L.off_q = off;    off = align_up(off + (size_t)kQueues * kQueueStride * 8, 256);
+  L.off_q = off;    off = align_up(off + (size_t)(kQueues + 1) * kQueueStride * 8, 256);
   L.off_err = off;  off = align_up(off + 8, 256);
   L.total = off;
   return true;
@@ -195,7 +202,6 @@ static const DevInfo* device_info() {
   hipDeviceProp_t pr;
   if (hipGetDeviceProperties(&pr, dev) != hipSuccess) return nullptr;
   if (std::strncmp(pr.gcnArchName, "gfx950", 6) != 0) return nullptr;
-  if (!pr.cooperativeLaunch) return nullptr;
   di.n_cu = pr.multiProcessorCount;
   for (int dt = 0; dt < 2; ++dt) {
     int nb = 1 << 30;
@@ -301,9 +307,10 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   if (!sched_build(B, K, L.S, gmax, A.sc)) return ASYMSPEC_E_ARG;
   const int grid = std::min(gmax, A.sc.total);
 
+  // An ordinary launch: the queues need no co-residency (see queue_init).
   void* args[] = {&A};
-  const hipError_t e = hipLaunchCooperativeKernel(kernel_ptr(dtype, params->beta == 1.0f), dim3(grid),
-                                                  dim3(kThreads), args, 0, (hipStream_t)stream);
+  const hipError_t e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f), dim3(grid),
+                                       dim3(kThreads), args, 0, (hipStream_t)stream);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return ASYMSPEC_E_DEVICE;

@@ -480,6 +480,7 @@ DEV Gather sgather(const KArgs& A, const RowGeo& g) {
 // --------------------------------------------------------- shared memory
 struct Smem {
   int next[2];                     // work-queue hand-off (double buffered)
+  int queue;                       // the queue this workgroup serves
   // statistics item: per-wave partials
   float wm[kWaves][kSlots];
   float ws[kWaves][kSlots];
