@@ -10,7 +10,7 @@ Prints one JSON line: rows/s (B*(K+1) verified positions per second) as the
 value, the achieved HBM bandwidth of the kernel against MI355X's 8 TB/s, and
 the CPU oracle timed on the host as a reported baseline.
 
-  python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--workload 3]
+  python bench.py [--gpus 1] [--steps 200] [--warmup 300] [--workload 3]
 """
 
 import argparse
@@ -142,8 +142,9 @@ COPY_BYTES = 1 << 30
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    # the clocks settle after a few hundred back-to-back calls (about 50 ms)
+    ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--gate", action="store_true", help="also return (D, gamma_eff) per row")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")

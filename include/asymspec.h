@@ -78,7 +78,7 @@ typedef struct asymspec_params {
 /* Bytes of device workspace asymspec_fuse_verify needs for this shape
  * (0 for invalid arguments).  The workspace needs no initialisation and may be
  * reused across calls of any shape: every record the kernel exchanges between
- * workgroups, and its work-queue counter, is tagged with a per-call epoch.
+ * workgroups is tagged with a per-call epoch.
  * Calls that may run at the same time need distinct workspaces. */
 size_t asymspec_workspace_size(int B, int K, int V, int dtype);
 

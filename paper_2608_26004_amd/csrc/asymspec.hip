@@ -1,23 +1,23 @@
 // AsymSpec fused decision step for MI355X (gfx950, CDNA4, wave64).
 //
-// One persistent launch does the whole step of Alg. 1 for every
-// request: the vocabulary-wide statistics of the verifier logits t and the
-// drafter logits a (full view) and b (compressed view), the delta-fused logits
+// One launch does the whole step of Alg. 1 for every request: the
+// vocabulary-wide statistics of the verifier logits t and the drafter logits
+// a (full view) and b (compressed view), the delta-fused logits
 // f = t + beta (a - b) (Sec. 3.2, Eq. 1-2), the Jensen-Shannon divergence D and
 // the CDA gate gamma * exp(-D) (Sec. 3.3, Eq. 3), the acceptance test (Eq. 4,
 // or its speculative-sampling form for temperature > 0), and the emission at
 // the first rejection or the bonus token.
 //
-// The launch is a work queue (schedule.h): workgroups take items in order
-// from an atomic counter.  Statistics items (stats.h) stream every logit
+// The launch is an ordered list of work items (schedule.h), one workgroup per
+// item, so the hardware dispatcher hands them out in list order and balances
+// them over the compute units.  Statistics items (stats.h) stream every logit
 // once from HBM and never wait; per request, a decide, S pass-2 and a pick
 // item (resolve.h) follow a few requests behind and re-read only the rows
-// whose outcome needs a second pass, while those rows are still in the
-// memory-side cache.
+// whose outcome needs a second pass.
 //
 // Cross-workgroup records are arrays of 64-bit slots whose high word is the
 // launch epoch and low word a payload, written and read with relaxed
-// agent-scope atomics (no cache flushes).  An aligned 64-bit access is
+// system-scope atomics (no cache flushes).  An aligned 64-bit access is
 // single-copy atomic, so a reader that sees the epoch in a slot sees its
 // payload; writers never wait, readers poll until every slot they need is
 // in.  The workspace therefore needs no initialisation.
@@ -41,40 +41,6 @@
 
 namespace asym {
 
-// Work queues: kQueues counters, each in its own 128-byte line, and an
-// arrival counter.  A workgroup serves queue (arrival order) % nq, whose
-// items are the global indices q, q + nq, ... in increasing order.  Every
-// queue is thus served by a running workgroup and hands out its items in
-// list order, so the lowest unfinished item can always run, whether or not
-// the whole grid is resident.  A counter holds (epoch, count); the first
-// workgroup of a launch to touch it raises it to (epoch, 0) with one atomic
-// max (epochs grow within a process), and values are then taken with
-// fetch-add.
-constexpr int kQueues = 8;
-constexpr int kQueueStride = 16;   // 64-bit words between counters (arrival counter last)
-
-DEV void queue_init(const KArgs& A, uint64_t* ctr) {
-  const uint64_t want = (uint64_t)A.epoch << 32;
-  const uint64_t old = __hip_atomic_fetch_max(ctr, want, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if ((uint32_t)(old >> 32) <= A.epoch) return;
-  // a counter left by a later epoch (another library instance on this
-  // workspace): replace it by compare-and-swap
-  uint64_t v = old;
-  Poll pl;
-  while (!tag_ok(v, A.epoch)) {
-    uint64_t expect = v;
-    if (__hip_atomic_compare_exchange_strong(ctr, &expect, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_AGENT))
-      break;
-    v = expect;
-    if (!pl.again(A)) break;
-  }
-}
-DEV uint32_t take(uint64_t* ctr) {
-  return (uint32_t)__hip_atomic_fetch_add(ctr, (uint64_t)1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-DEV uint32_t grab(uint64_t* ctr, int nq, int q) { return take(ctr) * (uint32_t)nq + (uint32_t)q; }
-
 template <int DT, bool kB1>
 DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
   const int i = sub / A.S, m = sub - (sub / A.S) * A.S;
@@ -96,47 +62,23 @@ DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
 #define ASYMSPEC_WAVES 4
 #endif
 
+// One workgroup per item.  An item waits only for items earlier in the list
+// (lower workgroup index), and each XCD starts its share of the workgroups in
+// index order, so the lowest waiting workgroup always waits on items that are
+// running or queued behind workgroups that never wait: the list drains
+// whether or not every workgroup fits on the chip at once.  The waits are
+// bounded besides (Poll), and a timeout is counted in the workspace.
 template <int DT, bool kB1>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ASYMSPEC_WAVES)))
 void fuse_verify_kernel(KArgs A) {
   __shared__ Smem sm;
-  const int tid = threadIdx.x;
-  const int nq = min((int)gridDim.x, kQueues);
-  if (tid == 0) {
-    uint64_t* arrive = A.qctr + (size_t)kQueues * kQueueStride;
-    queue_init(A, arrive);
-    const int q = (int)(take(arrive) % (uint32_t)nq);
-    uint64_t* c = A.qctr + (size_t)q * kQueueStride;
-    queue_init(A, c);
-    sm.next[0] = (int)grab(c, nq, q);
-    sm.queue = q;
-  }
-  __syncthreads();
-  const int q = sm.queue;
-  uint64_t* ctr = A.qctr + (size_t)q * kQueueStride;
-  uint32_t cur = (uint32_t)sm.next[0];
-  int par = 1;
-  while (cur < (uint32_t)A.sc.total) {
-    uint32_t nx = 0;
-    if (tid == 0) nx = grab(ctr, nq, q);   // in flight while this item runs
-    // The arguments are re-read in every iteration through an opaque copy of
-    // the kernarg-segment pointer (scalar loads), so that no item's address
-    // arithmetic is hoisted out of the loop and kept live across the others.
-    auto kp = (const __attribute__((address_space(4))) KArgs*)__builtin_amdgcn_kernarg_segment_ptr();
-    asm volatile("" : "+s"(kp));
-    const KArgs& B = *(const KArgs*)kp;
-    const Item it = sched_item(B.sc, B.K, B.S, (int)cur);
-    switch (it.type) {
-      case kItemStats: stats_dispatch<DT, kB1>(B, it.req, it.sub, sm); break;
-      case kItemDecide: decide_item<DT>(B, it.req, sm); break;
-      case kItemPass2: pass2_item<DT>(B, it.req, it.sub, sm); break;
-      case kItemPick: pick_item<DT>(B, it.req, sm); break;
-      default: break;
-    }
-    if (tid == 0) sm.next[par] = (int)nx;
-    __syncthreads();
-    cur = (uint32_t)sm.next[par];
-    par ^= 1;
+  const Item it = sched_item(A.sc, A.K, A.S, (int)blockIdx.x);
+  switch (it.type) {
+    case kItemStats: stats_dispatch<DT, kB1>(A, it.req, it.sub, sm); break;
+    case kItemDecide: decide_item<DT>(A, it.req, sm); break;
+    case kItemPass2: pass2_item<DT>(A, it.req, it.sub, sm); break;
+    case kItemPick: pick_item<DT>(A, it.req, sm); break;
+    default: break;
   }
 }
 
@@ -149,7 +91,7 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
 struct Layout {
   int S, VE;
   size_t rows;
-  size_t off_rec1, off_dec, off_rec2, off_q, off_err, total;
+  size_t off_rec1, off_dec, off_rec2, off_err, total;
 };
 
 static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -170,7 +112,6 @@ static bool make_layout(int B, int K, int V, int dtype, Layout& L) {
   L.off_rec1 = off; off = align_up(off + L.rows * L.S * kR1 * 8, 256);
   L.off_dec = off;  off = align_up(off + (size_t)B * (kDecHdr + (size_t)(K + 1) * kDecRow) * 8, 256);
   L.off_rec2 = off; off = align_up(off + L.rows * L.S * kR2 * 8, 256);
-  L.off_q = off;    off = align_up(off + (size_t)(kQueues + 1) * kQueueStride * 8, 256);
   L.off_err = off;  off = align_up(off + 8, 256);
   L.total = off;
   return true;
@@ -223,8 +164,8 @@ static uint32_t next_epoch() {
   static std::once_flag once;
   std::call_once(once, [] {
     const uint64_t t = (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count();
-    // a varying start well below 2^31, so that epochs keep growing (the
-    // work-queue counters rely on it) for 2^31 launches
+    // a varying start, so that a workspace reused by another process or
+    // library instance is unlikely to hold slots tagged with a live epoch
     ctr.store((uint32_t)((t ^ (t >> 32) ^ ((uint64_t)getpid() << 16)) & 0x3FFFFFFFu) | 1u);
   });
   uint32_t e;
@@ -295,7 +236,6 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   A.rec1 = (uint64_t*)(ws + L.off_rec1);
   A.dec = (uint64_t*)(ws + L.off_dec);
   A.rec2 = (uint64_t*)(ws + L.off_rec2);
-  A.qctr = (uint64_t*)(ws + L.off_q);
   A.err = (uint32_t*)(ws + L.off_err);
   A.stream_bytes = (unsigned long long)B * (K + 1) * (unsigned long long)V * (dtype == ASYMSPEC_BF16 ? 2ull : 4ull);
   A.B = B; A.K = K; A.V = V; A.S = L.S;
@@ -303,11 +243,10 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   A.want_gate = gate_out != nullptr;
   A.ln_gamma = std::log((double)params->gamma);
   A.epoch = next_epoch();
-  const int gmax = di->max_blocks[dtype];
-  if (!sched_build(B, K, L.S, gmax, A.sc)) return ASYMSPEC_E_ARG;
-  const int grid = std::min(gmax, A.sc.total);
+  // lags scale with the number of workgroups the chip holds at once
+  if (!sched_build(B, K, L.S, di->max_blocks[dtype], A.sc)) return ASYMSPEC_E_ARG;
+  const int grid = A.sc.total;
 
-  // An ordinary launch: the queues need no co-residency (see queue_init).
   void* args[] = {&A};
   const hipError_t e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f), dim3(grid),
                                        dim3(kThreads), args, 0, (hipStream_t)stream);

@@ -298,9 +298,9 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bo
     #pragma unroll
     for (int k = 0; k < kG; ++k) {
       const uint32_t off = (uint32_t)((rel0 + (long long)(k0 + k) * 64) * 16);
-      vt[k] = nt ? buf_load(rt, off) : u4{0, 0, 0, 0};
-      va[k] = nab ? buf_load(ra, off) : u4{0, 0, 0, 0};
-      vb[k] = nab ? buf_load(rb, off) : u4{0, 0, 0, 0};
+      vt[k] = nt ? buf_load_nt(rt, off) : u4{0, 0, 0, 0};
+      va[k] = nab ? buf_load_nt(ra, off) : u4{0, 0, 0, 0};
+      vb[k] = nab ? buf_load_nt(rb, off) : u4{0, 0, 0, 0};
     }
     #pragma unroll
     for (int k = 0; k < kG; ++k) {

@@ -3,8 +3,9 @@
 // Plain C++ (no HIP types) so that the same code runs in the kernel, in the
 // host launcher and in a host-only test.
 //
-// The step is a single ordered list of work items, handed out in order by an
-// atomic counter.  Items are grouped in steps q = 0, 1, 2, ...; step q holds
+// The step is a single ordered list of work items, one workgroup each, which
+// the hardware starts in index order.  Items are grouped in steps q = 0, 1,
+// 2, ...; step q holds
 //   * the statistics items of request q       ((K+1) * S items: one per row
 //     and vocabulary chunk), when q < B,
 //   * the decide item of request q - L1       (1 item),
@@ -63,10 +64,11 @@ ASYM_HD inline int sched_block(int parts, int K, int S) {
          ((parts & kPartPass2) ? S : 0) + ((parts & kPartPick) ? 1 : 0);
 }
 
-// Lags in steps.  items_in_flight is the number of workgroups; each holds
-// its current item and the next one, and a resolve item that waits holds its
-// workgroup, so each lag spans lag_pct percent of items_in_flight statistics
-// items.  Returns false when the schedule would not fit in 31-bit indices.
+// Lags in steps.  items_in_flight is the number of workgroups the chip holds
+// at once; the items of one request finish about that many items after the
+// first of them starts, and a resolve item that waits holds its workgroup, so
+// each lag spans lag_pct percent of items_in_flight statistics items.
+// Returns false when the schedule would not fit in 31-bit indices.
 inline bool sched_build(int B, int K, int S, int items_in_flight, Sched& sc, int lag_pct = 400) {
   if (B < 1 || K < 0 || S < 1 || items_in_flight < 1) return false;
   // steps hold at least the (K+1) * S statistics items of their request

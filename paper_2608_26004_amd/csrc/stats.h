@@ -58,7 +58,7 @@ DEV void load_tile(const __amdgpu_buffer_rsrc_t (&r)[3], uint32_t off0, u4 (&buf
   for (int k = 0; k < kNV; ++k) {
     const uint32_t off = off0 + (uint32_t)(k * 64 * 16);
     #pragma unroll
-    for (int s = 0; s < NS; ++s) buf[s][k] = buf_load(r[s], off);
+    for (int s = 0; s < NS; ++s) buf[s][k] = buf_load_nt(r[s], off);
   }
 }
 
@@ -269,7 +269,7 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   #pragma unroll
   for (int j = 0; j < kWin; ++j)
     #pragma unroll
-    for (int s = 0; s < NS; ++s) buf[s][j] = buf_load(r[s], off0 + (uint32_t)(vec_rel(j) * 16));
+    for (int s = 0; s < NS; ++s) buf[s][j] = buf_load_nt(r[s], off0 + (uint32_t)(vec_rel(j) * 16));
   #pragma unroll
   for (int j = 0; j < kVecs; ++j) {
     const int sl = j % kWin;
@@ -285,7 +285,7 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
     stats_vec<DT, KIND, kB1, kMask>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl], buf[NS == 3 ? 2 : 0][sl], j, q);
     if (j + kWin < kVecs) {
       #pragma unroll
-      for (int s = 0; s < NS; ++s) buf[s][sl] = buf_load(r[s], off0 + (uint32_t)(vec_rel(j + kWin) * 16));
+      for (int s = 0; s < NS; ++s) buf[s][sl] = buf_load_nt(r[s], off0 + (uint32_t)(vec_rel(j + kWin) * 16));
     }
     // one vector's temporaries at a time
     __builtin_amdgcn_sched_barrier(0);
