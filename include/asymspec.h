@@ -103,7 +103,9 @@ int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stre
  *                       emission draw.  Unused for greedy requests, but required.
  *   temperature         tau [B] float; tau <= 0 selects greedy decoding for
  *                       that request (the paper's setting), tau > 0 sampling.
- *   B >= 1, 0 <= K <= 63, V >= 1, B*(K+1)*V < 2^40
+ *   B >= 1, 0 <= K <= 63, V >= 1, B*(K+1)*V < 2^40, and V at most
+ *                       4194297 (bf16) or 2097149 (fp32): a row spans at most
+ *                       256 chunks of 32 KiB
  *   params              see asymspec_params (host pointer)
  *   accept_len          [B] int32 out: number of accepted drafts, in [0, K]
  *   next_token          [B] int32 out: the token emitted after them

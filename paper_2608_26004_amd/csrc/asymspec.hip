@@ -105,7 +105,8 @@ static bool make_layout(int B, int K, int V, int dtype, Layout& L) {
   // a row spans at most this many 16-byte vectors (it may start mid-vector)
   const long long nvec_max = ((long long)V + 2LL * L.VE - 2) / L.VE;
   const long long S = (nvec_max + kChunkVec - 1) / kChunkVec;
-  if (S > (1 << 20)) return false;
+  // a request's decision combines each row's chunks in one workgroup pass
+  if (S > kThreads) return false;
   L.S = (int)S;
   L.rows = (size_t)B * (K + 1);
   size_t off = 0;

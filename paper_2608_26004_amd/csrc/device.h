@@ -59,9 +59,12 @@ enum Slot { sT = 0, sA = 1, sB = 2, sF = 3, sAT = 4, kSlots = 5 };
 enum { R1_M = 0, R1_S = kSlots, R1_ARG = 2 * kSlots, R1_NEQ = 2 * kSlots + 1, R1_USED = 2 * kSlots + 2,
        kR1 = 16 };
 
-// Decision record of one request: a header and one block per row.
+// Decision record of one request: a header and one block per row, published
+// by the decide item; pass-2 and pick items load it into LDS (Smem::req,
+// Smem::rows).
 enum { H_STATE = 0, H_J = 1, H_TASK_LO = 2, H_TASK_HI = 3, H_USED = 4, kDecHdr = 8 };
 enum { kStateFinal = 1, kStatePending = 2 };
+enum { R_J = 0, R_TASK_LO = 1, R_TASK_HI = 2, R_FIN = 3, kReqWords = 4 };
 enum {
   D_TASK = 0,   // pass-2 work on the row: kTaskJsd | kTaskRes | kTaskBonus
   D_C,          // exponent scale of the row's emission distribution (log2 e / tau, or log2 e)
@@ -159,6 +162,28 @@ struct Poll {
       return false;
     }
     return true;
+  }
+};
+
+// Workgroup-wide polling step: done() is true once every thread's ok holds;
+// otherwise it sleeps with the same backoff as Poll and returns false, or
+// gives up (true, and counts an error) when thread 0 finds the wait timed
+// out.  Every thread gets the same answer.
+struct BlockPoll {
+  uint64_t t0;
+  int n;
+  DEV BlockPoll() : t0(__builtin_amdgcn_s_memrealtime()), n(0) {}
+  DEV bool done(bool ok, const KArgs& A) {
+    if (__syncthreads_and(ok)) return true;
+    const int reps = 1 << (n < 5 ? n : 5);
+    for (int i = 0; i < reps; ++i) __builtin_amdgcn_s_sleep(2);
+    ++n;
+    const bool late = threadIdx.x == 0 && __builtin_amdgcn_s_memrealtime() - t0 > kPollTicks;
+    if (__syncthreads_or(late)) {
+      if (threadIdx.x == 0) err_count(A.err);
+      return true;
+    }
+    return false;
   }
 };
 
@@ -491,15 +516,15 @@ struct Smem {
   float ws[kWaves][kSlots];
   int warg[kWaves];
   int wneq[kWaves];
-  // decide item: per-row values for the wave-0 pass
-  uint32_t rstat[kMaxK + 1];
-  uint32_t rarg[kMaxK + 1];
-  float rlpe[kMaxK + 1];
-  float rlpd[kMaxK + 1];
-  uint32_t rowv[kWaves][kDecRow];  // one row's decision block, per wave
-  // pass 2 / pick: constants of the current row, partials, scans
-  uint32_t cst[kDecRow];
-  uint32_t hdr[H_USED];
+  // decision of a request: per-row blocks, request words, and the
+  // per-(row, chunk) values the decide item combines into them
+  uint32_t rows[kMaxK + 1][kDecRow];
+  uint32_t req[kReqWords];
+  float dm[kThreads][kSlots];
+  double dt[kThreads][kSlots];
+  int darg[kThreads];
+  int dneq[kThreads];
+  // pass 2 / pick: partials, scans
   float wj[kWaves];
   float wseg[kWaves];
   int flags[8];

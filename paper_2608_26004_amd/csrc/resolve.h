@@ -33,90 +33,21 @@ DEV uint64_t* p2_rec(const KArgs& A, int req, int i, int m) {
 }
 
 // ------------------------------------------------------------------ decide
-// One wave combines the S chunk records of row g; lane 0 classifies the row
-// and fills sm.rowv[w] with its decision block.  All 64 lanes must call it.
+// Classification of one row from its combined statistics: maxima M and
+// reference exponents R = fl(M * c) per slot, sums Sp rescaled to R (fp64),
+// the first index of the argmax slot's maximum, and whether a and b differ.
+// Fills the row's decision block v (kDecRow words).
 template <int DT>
-DEV void decide_row(const KArgs& A, const RowGeo& g, Smem& sm) {
-  const int lane = lane_id(), w = wave_id();
+DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const float (&M)[kSlots],
+                      const float (&R)[kSlots], const double (&Sp)[kSlots], int arg, bool neq,
+                      uint32_t* v) {
   const int kind = g.kind;
   const bool draft = kind_draft(kind);
   const bool samp = kind_samp(kind);
-  float cs[kSlots];
-  cs[sT] = draft ? kL2E : g.c;
-  cs[sA] = kL2E;
-  cs[sB] = kL2E;
-  cs[sF] = g.c;
-  cs[sAT] = g.c;
-  const uint64_t* base = A.rec1 + (size_t)g.row * A.S * kR1;
-  const uint32_t ep = A.epoch;
-  // lane ch holds record ch (ch < 64); records past 64 are re-read below
-  uint64_t r[R1_USED];
-  const bool have = lane < A.S;
-  {
-    Poll pl;
-    while (true) {
-      bool ok = true;
-      if (have) {
-        #pragma unroll
-        for (int j = 0; j < R1_USED; ++j) {
-          r[j] = ld_tag(base + (size_t)lane * kR1 + j);
-          ok = ok && tag_ok(r[j], ep);
-        }
-      }
-      for (int ch = lane + 64; ch < A.S; ch += 64) {
-        #pragma unroll
-        for (int j = 0; j < R1_USED; ++j) ok = ok && tag_ok(ld_tag(base + (size_t)ch * kR1 + j), ep);
-      }
-      if (__all(ok) || !pl.again(A)) break;
-    }
-  }
-  float M[kSlots];
-  #pragma unroll
-  for (int s = 0; s < kSlots; ++s) M[s] = have ? payf(r[R1_M + s]) : kFloorM;
-  for (int ch = lane + 64; ch < A.S; ch += 64) {
-    #pragma unroll
-    for (int s = 0; s < kSlots; ++s) M[s] = fmaxf(M[s], payf(ld_tag(base + (size_t)ch * kR1 + R1_M + s)));
-  }
-  #pragma unroll
-  for (int s = 0; s < kSlots; ++s) M[s] = wave_max_all(M[s]);
-  float R[kSlots];
-  double Sp[kSlots];
-  // the argmax slot (f for drafts, t for the bonus row); selects, not
-  // runtime indices, keep the arrays in registers
-  const float Marg = draft ? M[sF] : M[sT];
-  int arg = 0x7FFFFFFF, nq = 0;
-  #pragma unroll
-  for (int s = 0; s < kSlots; ++s) {
-    R[s] = M[s] * cs[s];
-    Sp[s] = have ? (double)payf(r[R1_S + s]) * exp2((double)(payf(r[R1_M + s]) * cs[s]) - (double)R[s]) : 0.0;
-  }
-  if (have) {
-    const float mine = draft ? payf(r[R1_M + sF]) : payf(r[R1_M + sT]);
-    if (mine == Marg) arg = (int)pay(r[R1_ARG]);
-    nq = (int)pay(r[R1_NEQ]);
-  }
-  for (int ch = lane + 64; ch < A.S; ch += 64) {
-    const uint64_t* rc = base + (size_t)ch * kR1;
-    #pragma unroll
-    for (int s = 0; s < kSlots; ++s) {
-      const float mc = payf(ld_tag(rc + R1_M + s));
-      Sp[s] += (double)payf(ld_tag(rc + R1_S + s)) * exp2((double)(mc * cs[s]) - (double)R[s]);
-    }
-    if (payf(ld_tag(rc + (draft ? R1_M + sF : R1_M + sT))) == Marg) arg = min(arg, (int)pay(ld_tag(rc + R1_ARG)));
-    nq |= (int)pay(ld_tag(rc + R1_NEQ));
-  }
-  #pragma unroll
-  for (int s = 0; s < kSlots; ++s) Sp[s] = wave_sum_d(Sp[s]);
-  arg = wave_min_i(arg);
-  const bool neq = __any(nq != 0);
-  const Gather gq = sgather<DT>(A, g);
-  if (lane != 0) return;
-
   double L2[kSlots];
   #pragma unroll
   for (int s = 0; s < kSlots; ++s) L2[s] = (double)R[s] + log2_dbl(Sp[s]);
   const bool cda = A.gate_mode == ASYMSPEC_GATE_CDA;
-  uint32_t* v = sm.rowv[w];
   #pragma unroll
   for (int i = 0; i < kDecRow; ++i) v[i] = 0u;
   int decided = 1, accept = 0;
@@ -187,6 +118,121 @@ DEV void decide_row(const KArgs& A, const RowGeo& g, Smem& sm) {
                 (neq ? kStNeq : 0);
 }
 
+// The decision of request req (Alg. 1, Eq. 2-4) from its statistics
+// records, into sm.rows (one decision block per row) and sm.req (first sure
+// rejection, pass-2 tasks, whether the request is final without pass 2).
+// Thread (i, ch) of a group of rows takes record ch of row i, so all records
+// arrive in one round trip; the row's maxima, sums, argmax and a-vs-b flag
+// are combined through LDS in chunk order and the row's first thread
+// classifies it.  Whole workgroup; S must not exceed kThreads.
+template <int DT>
+DEV void decide_request(const KArgs& A, int req, Smem& sm) {
+  const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
+  const int K = A.K, S = A.S, nrow = K + 1;
+  const int rpg = kThreads / S;                 // rows per group
+  const int li = tid / S, ch = tid - li * S;
+  for (int r0 = 0; r0 < nrow; r0 += rpg) {
+    const int nr = min(rpg, nrow - r0);
+    const bool have = li < nr;
+    const int i = r0 + (have ? li : 0);
+    const RowGeo g = row_geo<DT>(A, req * nrow + i);
+    const bool draft = kind_draft(g.kind);
+    float cs[kSlots];
+    cs[sT] = draft ? kL2E : g.c;
+    cs[sA] = kL2E;
+    cs[sB] = kL2E;
+    cs[sF] = g.c;
+    cs[sAT] = g.c;
+    // the row's first thread gathers the draft token's logits meanwhile
+    Gather gq{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
+    if (have && ch == 0) gq = sgather<DT>(A, g);
+    uint64_t r[R1_USED];
+    const uint64_t* base = A.rec1 + ((size_t)g.row * S + ch) * kR1;
+    {
+      BlockPoll bp;
+      while (true) {
+        bool ok = true;
+        #pragma unroll
+        for (int j = 0; j < R1_USED; ++j) {
+          r[j] = have ? ld_tag(base + j) : ((uint64_t)A.epoch << 32);
+          ok = ok && tag_ok(r[j], A.epoch);
+        }
+        if (bp.done(ok, A)) break;
+      }
+    }
+    // row maxima: every thread of the row reads the row's records from LDS
+    if (have) {
+      #pragma unroll
+      for (int s = 0; s < kSlots; ++s) sm.dm[tid][s] = payf(r[R1_M + s]);
+    }
+    __syncthreads();
+    float M[kSlots], Rr[kSlots];
+    #pragma unroll
+    for (int s = 0; s < kSlots; ++s) M[s] = kFloorM;
+    if (have) {
+      const int t0 = li * S;
+      for (int c = 0; c < S; ++c) {
+        #pragma unroll
+        for (int s = 0; s < kSlots; ++s) M[s] = fmaxf(M[s], sm.dm[t0 + c][s]);
+      }
+    }
+    // this chunk's terms of the row sums, rescaled to the row's reference
+    #pragma unroll
+    for (int s = 0; s < kSlots; ++s) Rr[s] = M[s] * cs[s];
+    if (have) {
+      const float Marg = draft ? M[sF] : M[sT];
+      #pragma unroll
+      for (int s = 0; s < kSlots; ++s)
+        sm.dt[tid][s] = (double)payf(r[R1_S + s]) * exp2((double)(payf(r[R1_M + s]) * cs[s]) - (double)Rr[s]);
+      const float mine = draft ? payf(r[R1_M + sF]) : payf(r[R1_M + sT]);
+      sm.darg[tid] = mine == Marg ? (int)pay(r[R1_ARG]) : 0x7FFFFFFF;
+      sm.dneq[tid] = (int)pay(r[R1_NEQ]);
+    }
+    __syncthreads();
+    if (have && ch == 0) {
+      double Sp[kSlots];
+      #pragma unroll
+      for (int s = 0; s < kSlots; ++s) Sp[s] = 0.0;
+      int arg = 0x7FFFFFFF, nq = 0;
+      for (int c = 0; c < S; ++c) {
+        #pragma unroll
+        for (int s = 0; s < kSlots; ++s) Sp[s] += sm.dt[tid + c][s];
+        arg = min(arg, sm.darg[tid + c]);
+        nq |= sm.dneq[tid + c];
+      }
+      classify_row<DT>(A, g, gq, M, Rr, Sp, arg, nq != 0, sm.rows[i]);
+    }
+    __syncthreads();
+  }
+  // request level (wave 0, lane i = row i): the first sure rejection j*, and
+  // the rows pass 2 must look at
+  if (w == 0) {
+    const float tau = sload_f32(A.tau, req);
+    const bool samp = tau > 0.0f;
+    const bool row_ok = lane <= K;
+    const uint32_t st = row_ok ? sm.rows[lane][D_STATUS] : 0u;
+    const bool is_draft = lane < K;
+    const bool decided = st & kStDecided, accept = st & kStAccept, neq = st & kStNeq;
+    const int jr = wave_min_i(is_draft && decided && !accept ? lane : 0x7FFFFFFF);
+    const int jstar = jr == 0x7FFFFFFF ? K : jr;
+    const bool open = is_draft && lane < jstar && !decided;
+    uint32_t task = 0;
+    if (is_draft && (open || (A.want_gate && neq))) task |= kTaskJsd;
+    if (samp && is_draft && (open || lane == jstar)) task |= kTaskRes;
+    if (samp && lane == K && jstar == K) task |= kTaskBonus;
+    const unsigned long long tmask = __ballot(task != 0);
+    const bool fin = !samp && !__any((task & kTaskJsd) != 0);
+    if (row_ok) sm.rows[lane][D_TASK] = task;
+    if (lane == 0) {
+      sm.req[R_J] = (uint32_t)jstar;
+      sm.req[R_TASK_LO] = (uint32_t)tmask;
+      sm.req[R_TASK_HI] = (uint32_t)(tmask >> 32);
+      sm.req[R_FIN] = fin ? 1u : 0u;
+    }
+  }
+  __syncthreads();
+}
+
 // Every output of request `req`, written by wave 0: lane i < K holds draft
 // i's fused log-probability and D_i.
 DEV void write_outputs(const KArgs& A, int req, int j, int next, float lp_next, float lpd_lane,
@@ -212,74 +258,83 @@ DEV void write_outputs(const KArgs& A, int req, int j, int next, float lp_next, 
 
 template <int DT>
 DEV void decide_item(const KArgs& A, int req, Smem& sm) {
-  const int lane = lane_id(), w = wave_id();
-  const int K = A.K;
-  const int row0 = req * (K + 1);
-  for (int i = w; i <= K; i += kWaves) {
-    const RowGeo g = row_geo<DT>(A, row0 + i);
-    decide_row<DT>(A, g, sm);
-    __builtin_amdgcn_wave_barrier();
-    const uint32_t val = lane < kDecRow ? sm.rowv[w][lane] : 0u;
-    uint64_t* drow = dec_row(A, req, i);
-    if (lane < D_USED && lane != D_TASK) st_tag(drow + lane, val, A.epoch);
+  const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
+  const int K = A.K, nrow = K + 1;
+  decide_request<DT>(A, req, sm);
+  // publish: every word of every row block, then the header
+  for (int k = tid; k < nrow * D_USED; k += kThreads) {
+    const int i = k / D_USED, j = k - i * D_USED;
+    st_tag(dec_row(A, req, i) + j, sm.rows[i][j], A.epoch);
+  }
+  const bool fin = sm.req[R_FIN] != 0u;
+  if (w == 0) {
+    uint64_t* hdr = dec_hdr(A, req);
     if (lane == 0) {
-      sm.rstat[i] = sm.rowv[w][D_STATUS];
-      sm.rarg[i] = sm.rowv[w][D_ARG];
-      sm.rlpe[i] = __uint_as_float(sm.rowv[w][D_LPEMIT]);
-      sm.rlpd[i] = __uint_as_float(sm.rowv[w][D_LPD]);
+      st_tag(hdr + H_J, sm.req[R_J], A.epoch);
+      st_tag(hdr + H_TASK_LO, sm.req[R_TASK_LO], A.epoch);
+      st_tag(hdr + H_TASK_HI, sm.req[R_TASK_HI], A.epoch);
+      st_tag(hdr + H_STATE, fin ? kStateFinal : kStatePending, A.epoch);
     }
-    __builtin_amdgcn_wave_barrier();
+    if (fin) {
+      // greedy with no open draft: accept_len = j*, emit the fused argmax of
+      // row j* (Eq. 2) or the verifier argmax of the bonus row (Alg. 1)
+      const int jstar = (int)sm.req[R_J];
+      const int next = (int)sm.rows[jstar][D_ARG];
+      const float lpn = __uint_as_float(sm.rows[jstar][D_LPEMIT]);
+      const float lpd = lane < K ? __uint_as_float(sm.rows[lane][D_LPD]) : 0.0f;
+      write_outputs(A, req, jstar, next, lpn, lpd, 0.0);
+    }
+  }
+}
+
+// The published decision of request req into sm.req and sm.rows: the
+// header and every row block are requested at once and polled together.
+// Returns the request's state (kStateFinal or kStatePending).  Whole
+// workgroup.
+DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
+  const int tid = wave_id() * 64 + lane_id();
+  const int nrow = A.K + 1;
+  const int nw = H_USED + nrow * D_USED;
+  constexpr int kPer = ((kMaxK + 1) * D_USED + H_USED + kThreads - 1) / kThreads;
+  uint64_t v[kPer];
+  BlockPoll bp;
+  while (true) {
+    bool ok = true;
+    #pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int k = tid + q * kThreads;
+      if (k < nw) {
+        const uint64_t* p = k < H_USED ? dec_hdr(A, req) + k
+                                       : dec_row(A, req, (k - H_USED) / D_USED) + (k - H_USED) % D_USED;
+        v[q] = ld_tag(p);
+        ok = ok && tag_ok(v[q], A.epoch);
+      }
+    }
+    if (bp.done(ok, A)) break;
+  }
+  #pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int k = tid + q * kThreads;
+    if (k < nw) {
+      if (k >= H_USED) {
+        const int i = (k - H_USED) / D_USED;
+        sm.rows[i][(k - H_USED) % D_USED] = pay(v[q]);
+      } else if (k == H_STATE) {
+        sm.req[R_FIN] = pay(v[q]) == kStateFinal ? 1u : 0u;
+      } else if (k == H_J) {
+        sm.req[R_J] = pay(v[q]);
+      } else if (k == H_TASK_LO) {
+        sm.req[R_TASK_LO] = pay(v[q]);
+      } else {
+        sm.req[R_TASK_HI] = pay(v[q]);
+      }
+    }
   }
   __syncthreads();
-  if (w != 0) return;
-  // wave 0: lane i looks at row i
-  const float tau = sload_f32(A.tau, req);
-  const bool samp = tau > 0.0f;
-  const bool row_ok = lane <= K;
-  const uint32_t st = row_ok ? sm.rstat[lane] : 0u;
-  const bool is_draft = lane < K;
-  const bool decided = st & kStDecided, accept = st & kStAccept, neq = st & kStNeq;
-  const int jr = wave_min_i(is_draft && decided && !accept ? lane : 0x7FFFFFFF);
-  const int jstar = jr == 0x7FFFFFFF ? K : jr;
-  const bool open = is_draft && lane < jstar && !decided;
-  uint32_t task = 0;
-  if (is_draft && (open || (A.want_gate && neq))) task |= kTaskJsd;
-  if (samp && is_draft && (open || lane == jstar)) task |= kTaskRes;
-  if (samp && lane == K && jstar == K) task |= kTaskBonus;
-  const unsigned long long tmask = __ballot(task != 0);
-  const bool fin = !samp && !__any((task & kTaskJsd) != 0);
-  if (row_ok) st_tag(dec_row(A, req, lane) + D_TASK, task, A.epoch);
-  uint64_t* hdr = dec_hdr(A, req);
-  if (lane == 0) {
-    st_tag(hdr + H_J, (uint32_t)jstar, A.epoch);
-    st_tag(hdr + H_TASK_LO, (uint32_t)tmask, A.epoch);
-    st_tag(hdr + H_TASK_HI, (uint32_t)(tmask >> 32), A.epoch);
-    st_tag(hdr + H_STATE, fin ? kStateFinal : kStatePending, A.epoch);
-  }
-  if (fin) {
-    // greedy with no open draft: accept_len = j*, emit the fused argmax of
-    // row j* (Eq. 2) or the verifier argmax of the bonus row (Alg. 1)
-    const int next = (int)sm.rarg[jstar];
-    const float lpn = sm.rlpe[jstar];
-    write_outputs(A, req, jstar, next, lpn, is_draft ? sm.rlpd[lane] : 0.0f, 0.0);
-  }
+  return sm.req[R_FIN] != 0u ? (uint32_t)kStateFinal : (uint32_t)kStatePending;
 }
 
 // ------------------------------------------------------------------ pass 2
-// Header of request req into sm.hdr (wave 0 polls; whole workgroup returns
-// after a barrier).
-DEV void load_header(const KArgs& A, int req, Smem& sm) {
-  const int lane = lane_id(), w = wave_id();
-  if (w == 0 && lane < H_USED) sm.hdr[lane] = pay(wait_tag(dec_hdr(A, req) + lane, A));
-  __syncthreads();
-}
-// Decision block of row i of request req into sm.cst.
-DEV void load_row_block(const KArgs& A, int req, int i, Smem& sm) {
-  const int lane = lane_id(), w = wave_id();
-  if (w == 0 && lane < D_USED) sm.cst[lane] = pay(wait_tag(dec_row(A, req, i) + lane, A));
-  __syncthreads();
-}
-
 // Pass-2 sums of one thread over its kSegPerLane vectors of a chunk.
 // kMode 0: interior chunk (no masking); 1: masked, branch-free; 2: generic
 // (one vector at a time, array-end repair).
@@ -337,23 +392,22 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bo
 template <int DT>
 DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
-  const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
-  load_header(A, req, sm);
-  if (sm.hdr[H_STATE] != kStatePending) return;
-  unsigned long long tmask = (unsigned long long)sm.hdr[H_TASK_LO] | ((unsigned long long)sm.hdr[H_TASK_HI] << 32);
+  const int lane = lane_id(), w = wave_id();
+  if (load_decision(A, req, sm) != kStatePending) return;
+  unsigned long long tmask = (unsigned long long)sm.req[R_TASK_LO] | ((unsigned long long)sm.req[R_TASK_HI] << 32);
   while (tmask != 0) {
     const int i = __builtin_ctzll(tmask);
     tmask &= tmask - 1;
-    load_row_block(A, req, i, sm);
-    const uint32_t task = sm.cst[D_TASK];
+    const uint32_t* cst = sm.rows[i];
+    const uint32_t task = cst[D_TASK];
     const RowGeo g = row_geo<DT>(A, req * (A.K + 1) + i);
     const bool dj = task & kTaskJsd, dr = task & kTaskRes, db = task & kTaskBonus;
-    const ResidConst rk{A.beta, __uint_as_float(sm.cst[D_C]), __uint_as_float(sm.cst[D_RF]),
-                        __uint_as_float(sm.cst[D_ISF]), __uint_as_float(sm.cst[D_RQ]),
-                        __uint_as_float(sm.cst[D_ISQ])};
-    const JsdConst jk{__uint_as_float(sm.cst[D_RA]), __uint_as_float(sm.cst[D_RB]),
-                      __uint_as_float(sm.cst[D_KAHI]), __uint_as_float(sm.cst[D_KALO]),
-                      __uint_as_float(sm.cst[D_KBHI]), __uint_as_float(sm.cst[D_KBLO])};
+    const ResidConst rk{A.beta, __uint_as_float(cst[D_C]), __uint_as_float(cst[D_RF]),
+                        __uint_as_float(cst[D_ISF]), __uint_as_float(cst[D_RQ]),
+                        __uint_as_float(cst[D_ISQ])};
+    const JsdConst jk{__uint_as_float(cst[D_RA]), __uint_as_float(cst[D_RB]),
+                      __uint_as_float(cst[D_KAHI]), __uint_as_float(cst[D_KALO]),
+                      __uint_as_float(cst[D_KBHI]), __uint_as_float(cst[D_KBLO])};
     const long long rel0 = (long long)m * kChunkVec + (long long)w * kSegVec + lane;
     const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
     float accj = 0.0f, seg = 0.0f;
@@ -387,7 +441,7 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
 // Inverse-CDF draw over row i of request req: the first element x whose
 // cumulative weight exceeds u * total, with the weights of pass 2 (residual
 // for drafts, bonus weights for the bonus row) recomputed by the same element
-// functions.  Row constants are in sm.cst.  Returns -1 when no element
+// functions.  Row constants are in sm.rows[i].  Returns -1 when no element
 // carries weight.  Whole workgroup.
 template <int DT>
 DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm) {
@@ -445,9 +499,10 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
   const double before = sm.dd[6];
   // 2. scan inside the segment: thread tid takes vectors kPer * tid ...
   const int ch = sel / kWaves, ww = sel % kWaves;
-  const ResidConst rk{A.beta, __uint_as_float(sm.cst[D_C]), __uint_as_float(sm.cst[D_RF]),
-                      __uint_as_float(sm.cst[D_ISF]), __uint_as_float(sm.cst[D_RQ]),
-                      __uint_as_float(sm.cst[D_ISQ])};
+  const uint32_t* cst = sm.rows[i];
+  const ResidConst rk{A.beta, __uint_as_float(cst[D_C]), __uint_as_float(cst[D_RF]),
+                      __uint_as_float(cst[D_ISF]), __uint_as_float(cst[D_RQ]),
+                      __uint_as_float(cst[D_ISQ])};
   const __amdgpu_buffer_rsrc_t rt = row_rsrc(A, A.t, g);
   const __amdgpu_buffer_rsrc_t ra = row_rsrc(A, bonus ? A.t : A.a, g);
   const __amdgpu_buffer_rsrc_t rb = row_rsrc(A, bonus ? A.t : A.b, g);
@@ -529,10 +584,9 @@ DEV int row_argmax_f(const KArgs& A, const RowGeo& g, Smem& sm) {
 
 template <int DT>
 DEV void pick_item(const KArgs& A, int req, Smem& sm) {
-  const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
+  const int lane = lane_id(), w = wave_id();
   const int K = A.K;
-  load_header(A, req, sm);
-  if (sm.hdr[H_STATE] != kStatePending) return;
+  if (load_decision(A, req, sm) != kStatePending) return;   // written by decide
   // wave 0: D of the rows that have it, final decisions, the emitting row
   float lpd = 0.0f;
   double Dl = 0.0;
@@ -542,13 +596,13 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
     double thr = 0.0;
     float lpe = 0.0f;
     if (lane <= K) {
-      const uint64_t* dr = dec_row(A, req, lane);
-      st = pay(wait_tag(dr + D_STATUS, A));
-      task = pay(wait_tag(dr + D_TASK, A));
-      thr = payd(wait_tag(dr + D_THR_LO, A), wait_tag(dr + D_THR_HI, A));
-      lpd = payf(wait_tag(dr + D_LPD, A));
-      arg = pay(wait_tag(dr + D_ARG, A));
-      lpe = payf(wait_tag(dr + D_LPEMIT, A));
+      const uint32_t* v = sm.rows[lane];
+      st = v[D_STATUS];
+      task = v[D_TASK];
+      thr = u2d(v[D_THR_LO], v[D_THR_HI]);
+      lpd = __uint_as_float(v[D_LPD]);
+      arg = v[D_ARG];
+      lpe = __uint_as_float(v[D_LPEMIT]);
     }
     if (task & kTaskJsd) {
       double s = 0.0;
@@ -573,7 +627,6 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
   int next = sm.flags[1];
   float lpn = (float)sm.dd[0];
   if (tau > 0.0f) {
-    load_row_block(A, req, j, sm);
     const bool bonus = j == K;
     const double u = (double)A.u[(size_t)req * (K + 1) + K];
     int pick = cdf_pick<DT>(A, req, j, u, bonus, sm);
@@ -583,8 +636,8 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
     const long long idx = g.e0 + next;
     float x = Elem<DT>::load_one(A.t, idx);
     if (!bonus) x = fuse_masked(x, Elem<DT>::load_one(A.a, idx), Elem<DT>::load_one(A.b, idx), A.beta);
-    const double c = (double)__uint_as_float(sm.cst[D_C]);
-    const double l2 = u2d(sm.cst[D_L2E_LO], sm.cst[D_L2E_HI]);
+    const double c = (double)__uint_as_float(sm.rows[j][D_C]);
+    const double l2 = u2d(sm.rows[j][D_L2E_LO], sm.rows[j][D_L2E_HI]);
     lpn = (float)(((double)x * c - l2) * kLn2);
   }
   if (w == 0) write_outputs(A, req, j, next, lpn, lpd, Dl);

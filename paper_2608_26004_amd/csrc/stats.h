@@ -250,7 +250,7 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
   constexpr int NS = TR::NS;
   constexpr bool kDraft = NS == 3;
-  const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
+  const int lane = lane_id(), w = wave_id();
   const float c = g.c;
   const __amdgpu_buffer_rsrc_t r[3] = {row_rsrc(A, A.t, g), row_rsrc(A, kDraft ? A.a : A.t, g),
                                        row_rsrc(A, kDraft ? A.b : A.t, g)};

@@ -44,6 +44,12 @@ def test_workspace_size():
     assert asp.workspace_size(1, 1, 0, asp.BF16) == 0
     assert asp.workspace_size(1, 1, 10, 7) == 0
     assert asp.workspace_size(4, 2, 1000, asp.FP32) >= asp.workspace_size(1, 2, 1000, asp.FP32)
+    # a row spans at most 256 chunks of 2048 16-byte vectors (it may start
+    # mid-vector): V <= 4194297 in bf16, 2097149 in fp32
+    assert asp.workspace_size(1, 1, 4194297, asp.BF16) > 0
+    assert asp.workspace_size(1, 1, 4194298, asp.BF16) == 0
+    assert asp.workspace_size(1, 1, 2097149, asp.FP32) > 0
+    assert asp.workspace_size(1, 1, 2097150, asp.FP32) == 0
 
 
 def _call(**over):
