@@ -187,6 +187,28 @@ struct BlockPoll {
   }
 };
 
+// Whole workgroup: wait (bounded) until slot p carries the launch epoch,
+// with one load per poll.
+DEV void wait_one(const uint64_t* p, const KArgs& A) {
+  BlockPoll bp;
+  while (!bp.done(threadIdx.x != 0 || tag_ok(ld_tag(p), A.epoch), A)) {
+  }
+}
+
+// Whole workgroup: load() requests a set of tagged slots and returns whether
+// this thread's share all carry the launch epoch.  When the first attempt
+// misses, the workgroup polls only the slot `sentinel` (written about last)
+// until it is in, so that a waiting workgroup adds little traffic, and then
+// loads until every share is in (bounded).
+template <class F>
+DEV void load_tagged(const KArgs& A, const uint64_t* sentinel, F&& load) {
+  if (__syncthreads_and(load())) return;
+  wait_one(sentinel, A);
+  BlockPoll bp;
+  while (!bp.done(load(), A)) {
+  }
+}
+
 // Poll a tagged slot until it carries the launch epoch (bounded).
 DEV uint64_t wait_tag(const uint64_t* p, const KArgs& A) {
   uint64_t v = ld_tag(p);

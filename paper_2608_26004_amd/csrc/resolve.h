@@ -32,6 +32,16 @@ DEV uint64_t* p2_rec(const KArgs& A, int req, int i, int m) {
   return A.rec2 + (((size_t)req * (A.K + 1) + i) * A.S + m) * kR2;
 }
 
+// Element-term constants of a row from its decision block.
+DEV ResidConst resid_const(const KArgs& A, const uint32_t* cst) {
+  return ResidConst{A.beta, __uint_as_float(cst[D_C]), __uint_as_float(cst[D_RF]),
+                    __uint_as_float(cst[D_ISF]), __uint_as_float(cst[D_RQ]), __uint_as_float(cst[D_ISQ])};
+}
+DEV JsdConst jsd_const(const uint32_t* cst) {
+  return JsdConst{__uint_as_float(cst[D_RA]), __uint_as_float(cst[D_RB]), __uint_as_float(cst[D_KAHI]),
+                  __uint_as_float(cst[D_KALO]), __uint_as_float(cst[D_KBHI]), __uint_as_float(cst[D_KBLO])};
+}
+
 // ------------------------------------------------------------------ decide
 // Classification of one row from its combined statistics: maxima M and
 // reference exponents R = fl(M * c) per slot, sums Sp rescaled to R (fp64),
@@ -131,6 +141,9 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
   const int K = A.K, S = A.S, nrow = K + 1;
   const int rpg = kThreads / S;                 // rows per group
   const int li = tid / S, ch = tid - li * S;
+  // the request's last statistics item in list order is about the last to
+  // finish: a waiting workgroup polls its record only
+  const uint64_t* sentinel = A.rec1 + (((size_t)req * nrow + K) * S + (S - 1)) * kR1 + R1_NEQ;
   for (int r0 = 0; r0 < nrow; r0 += rpg) {
     const int nr = min(rpg, nrow - r0);
     const bool have = li < nr;
@@ -148,18 +161,15 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
     if (have && ch == 0) gq = sgather<DT>(A, g);
     uint64_t r[R1_USED];
     const uint64_t* base = A.rec1 + ((size_t)g.row * S + ch) * kR1;
-    {
-      BlockPoll bp;
-      while (true) {
-        bool ok = true;
-        #pragma unroll
-        for (int j = 0; j < R1_USED; ++j) {
-          r[j] = have ? ld_tag(base + j) : ((uint64_t)A.epoch << 32);
-          ok = ok && tag_ok(r[j], A.epoch);
-        }
-        if (bp.done(ok, A)) break;
+    load_tagged(A, sentinel, [&]() {
+      bool ok = true;
+      #pragma unroll
+      for (int j = 0; j < R1_USED; ++j) {
+        r[j] = have ? ld_tag(base + j) : ((uint64_t)A.epoch << 32);
+        ok = ok && tag_ok(r[j], A.epoch);
       }
-    }
+      return ok;
+    });
     // row maxima: every thread of the row reads the row's records from LDS
     if (have) {
       #pragma unroll
@@ -267,6 +277,7 @@ DEV void decide_item(const KArgs& A, int req, Smem& sm) {
     st_tag(dec_row(A, req, i) + j, sm.rows[i][j], A.epoch);
   }
   const bool fin = sm.req[R_FIN] != 0u;
+  __syncthreads();   // the header goes out after every row word
   if (w == 0) {
     uint64_t* hdr = dec_hdr(A, req);
     if (lane == 0) {
@@ -297,8 +308,8 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
   const int nw = H_USED + nrow * D_USED;
   constexpr int kPer = ((kMaxK + 1) * D_USED + H_USED + kThreads - 1) / kThreads;
   uint64_t v[kPer];
-  BlockPoll bp;
-  while (true) {
+  // the header goes out after the rows: a waiting workgroup polls it only
+  load_tagged(A, dec_hdr(A, req) + H_STATE, [&]() {
     bool ok = true;
     #pragma unroll
     for (int q = 0; q < kPer; ++q) {
@@ -310,8 +321,8 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
         ok = ok && tag_ok(v[q], A.epoch);
       }
     }
-    if (bp.done(ok, A)) break;
-  }
+    return ok;
+  });
   #pragma unroll
   for (int q = 0; q < kPer; ++q) {
     const int k = tid + q * kThreads;
@@ -402,12 +413,8 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
     const uint32_t task = cst[D_TASK];
     const RowGeo g = row_geo<DT>(A, req * (A.K + 1) + i);
     const bool dj = task & kTaskJsd, dr = task & kTaskRes, db = task & kTaskBonus;
-    const ResidConst rk{A.beta, __uint_as_float(cst[D_C]), __uint_as_float(cst[D_RF]),
-                        __uint_as_float(cst[D_ISF]), __uint_as_float(cst[D_RQ]),
-                        __uint_as_float(cst[D_ISQ])};
-    const JsdConst jk{__uint_as_float(cst[D_RA]), __uint_as_float(cst[D_RB]),
-                      __uint_as_float(cst[D_KAHI]), __uint_as_float(cst[D_KALO]),
-                      __uint_as_float(cst[D_KBHI]), __uint_as_float(cst[D_KBLO])};
+    const ResidConst rk = resid_const(A, cst);
+    const JsdConst jk = jsd_const(cst);
     const long long rel0 = (long long)m * kChunkVec + (long long)w * kSegVec + lane;
     const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
     float accj = 0.0f, seg = 0.0f;
@@ -442,7 +449,9 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
 // cumulative weight exceeds u * total, with the weights of pass 2 (residual
 // for drafts, bonus weights for the bonus row) recomputed by the same element
 // functions.  Row constants are in sm.rows[i].  Returns -1 when no element
-// carries weight.  Whole workgroup.
+// carries weight; otherwise the element's index, and, when the scan itself
+// found it, sm.flags[2] = 1 and its logit (f for drafts, t for the bonus
+// row) in sm.dd[3].  Whole workgroup.
 template <int DT>
 DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
@@ -450,45 +459,72 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
   const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
   const RowGeo g = row_geo<DT>(A, req * (A.K + 1) + i);
   const int nseg = A.S * kWaves;
-  // total weight (wave 0 waits for every segment sum)
-  if (w == 0) {
-    double tot = 0.0;
-    for (int sg = lane; sg < nseg; sg += 64) {
-      const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
-      const uint64_t lo = wait_tag(p, A), hi = wait_tag(p + 1, A);
-      tot += payd(lo, hi);
-    }
-    tot = wave_sum_d(tot);
-    if (lane == 0) sm.dd[4] = tot;
-  }
-  __syncthreads();
-  const double total = sm.dd[4];
-  if (!(total > 0.0)) return -1;
-  const double target = u * total;
-  // 1. the segment holding the target: scan of segment sums in index order
-  double carry = 0.0;
+  if (tid == 0) sm.flags[2] = 0;
+  double target;
   int sel = 0x7FFFFFFF, last_nz = -1;
-  for (int s0 = 0; s0 < nseg && sel == 0x7FFFFFFF; s0 += kThreads) {
-    const int sg = s0 + tid;
+  if (nseg <= kThreads) {
+    // 1. one pass: thread sg holds segment sum sg; the scan gives the total
+    // and the segment holding the target
+    const int sg = tid;
     double v = 0.0;
     if (sg < nseg) {
       const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
-      v = payd(ld_tag(p), ld_tag(p + 1));
+      v = payd(wait_tag(p, A), wait_tag(p + 1, A));
     }
     double incl, excl;
     block_scan(v, sm, incl, excl);
-    incl += carry;
-    excl += carry;
+    if (tid == kThreads - 1) sm.dd[4] = incl;
+    __syncthreads();
+    const double total = sm.dd[4];
+    if (!(total > 0.0)) return -1;
+    target = u * total;
     const int cand = block_min_i((v > 0.0 && incl > target) ? sg : 0x7FFFFFFF, sm);
     const int lnz = block_min_i(v > 0.0 ? -sg : 0x7FFFFFFF, sm);
     if (lnz != 0x7FFFFFFF) last_nz = -lnz;
-    __syncthreads();
     if (sg == cand) sm.dd[6] = excl;
     if (sg == last_nz) sm.dd[7] = excl;
-    if (tid == kThreads - 1) sm.dd[5] = incl;
     __syncthreads();
-    carry = sm.dd[5];
     sel = cand;
+  } else {
+    // total weight (wave 0 waits for every segment sum)
+    if (w == 0) {
+      double tot = 0.0;
+      for (int sg = lane; sg < nseg; sg += 64) {
+        const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
+        const uint64_t lo = wait_tag(p, A), hi = wait_tag(p + 1, A);
+        tot += payd(lo, hi);
+      }
+      tot = wave_sum_d(tot);
+      if (lane == 0) sm.dd[4] = tot;
+    }
+    __syncthreads();
+    const double total = sm.dd[4];
+    if (!(total > 0.0)) return -1;
+    target = u * total;
+    // 1. the segment holding the target: scan of segment sums in index order
+    double carry = 0.0;
+    for (int s0 = 0; s0 < nseg && sel == 0x7FFFFFFF; s0 += kThreads) {
+      const int sg = s0 + tid;
+      double v = 0.0;
+      if (sg < nseg) {
+        const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
+        v = payd(ld_tag(p), ld_tag(p + 1));
+      }
+      double incl, excl;
+      block_scan(v, sm, incl, excl);
+      incl += carry;
+      excl += carry;
+      const int cand = block_min_i((v > 0.0 && incl > target) ? sg : 0x7FFFFFFF, sm);
+      const int lnz = block_min_i(v > 0.0 ? -sg : 0x7FFFFFFF, sm);
+      if (lnz != 0x7FFFFFFF) last_nz = -lnz;
+      __syncthreads();
+      if (sg == cand) sm.dd[6] = excl;
+      if (sg == last_nz) sm.dd[7] = excl;
+      if (tid == kThreads - 1) sm.dd[5] = incl;
+      __syncthreads();
+      carry = sm.dd[5];
+      sel = cand;
+    }
   }
   if (sel == 0x7FFFFFFF) {
     if (last_nz < 0) return -1;
@@ -500,40 +536,40 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
   // 2. scan inside the segment: thread tid takes vectors kPer * tid ...
   const int ch = sel / kWaves, ww = sel % kWaves;
   const uint32_t* cst = sm.rows[i];
-  const ResidConst rk{A.beta, __uint_as_float(cst[D_C]), __uint_as_float(cst[D_RF]),
-                      __uint_as_float(cst[D_ISF]), __uint_as_float(cst[D_RQ]),
-                      __uint_as_float(cst[D_ISQ])};
+  const ResidConst rk = resid_const(A, cst);
   const __amdgpu_buffer_rsrc_t rt = row_rsrc(A, A.t, g);
   const __amdgpu_buffer_rsrc_t ra = row_rsrc(A, bonus ? A.t : A.a, g);
-  const __amdgpu_buffer_rsrc_t rb = row_rsrc(A, bonus ? A.t : A.b, g);
+  // a row whose a and b are equal bitwise reads a for b (same weights)
+  const bool nb = !bonus && (cst[D_STATUS] & kStNeq) != 0u;
+  const __amdgpu_buffer_rsrc_t rb = row_rsrc(A, nb ? A.b : A.t, g);
   const long long rel = (long long)ch * kChunkVec + (long long)ww * kSegVec + (long long)kPer * tid;
   const long long sv0 = g.vbeg + (long long)ch * kChunkVec + (long long)ww * kSegVec;
   const bool tail = has_tail(A, sv0, sv0 + kSegVec);
-  float wv[kPer * VE];
+  u4 vt[kPer], va[kPer], vb[kPer];
   double tsum = 0.0;
   int last_pos = -1;
   #pragma unroll
   for (int k = 0; k < kPer; ++k) {
     const uint32_t off = (uint32_t)((rel + k) * 16);
     const long long vi = g.vbeg + rel + k;
-    u4 vt = buf_load(rt, off), va = buf_load(ra, off), vb = buf_load(rb, off);
+    vt[k] = buf_load(rt, off);
+    va[k] = bonus ? vt[k] : buf_load(ra, off);
+    vb[k] = nb ? buf_load(rb, off) : u4{0, 0, 0, 0};
     if (tail) {
-      fix_vec<DT>(A, g, A.t, vi, vt);
-      if (!bonus) {
-        fix_vec<DT>(A, g, A.a, vi, va);
-        fix_vec<DT>(A, g, A.b, vi, vb);
-      }
+      fix_vec<DT>(A, g, A.t, vi, vt[k]);
+      if (!bonus) fix_vec<DT>(A, g, A.a, vi, va[k]);
+      if (nb) fix_vec<DT>(A, g, A.b, vi, vb[k]);
     } else {
-      mask_vec<DT>(A, g, vi, vt);
-      mask_vec<DT>(A, g, vi, va);
-      mask_vec<DT>(A, g, vi, vb);
+      mask_vec<DT>(A, g, vi, vt[k]);
+      mask_vec<DT>(A, g, vi, va[k]);
+      mask_vec<DT>(A, g, vi, vb[k]);
     }
+    if (!nb) vb[k] = va[k];
     #pragma unroll
     for (int e = 0; e < VE; ++e) {
-      const float xt = Elem<DT>::get(vt, e);
+      const float xt = Elem<DT>::get(vt[k], e);
       const float x = bonus ? bonus_elem(xt, rk.c, rk.Rf)
-                            : resid_elem(xt, Elem<DT>::get(va, e), Elem<DT>::get(vb, e), rk);
-      wv[k * VE + e] = x;
+                            : resid_elem(xt, Elem<DT>::get(va[k], e), Elem<DT>::get(vb[k], e), rk);
       tsum += (double)x;
       if (x > 0.0f) last_pos = (int)((vi * VE + e) - g.e0);
     }
@@ -542,20 +578,31 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
   block_scan(tsum, sm, incl, excl);
   double run = before + excl;
   int first_ok = 0x7FFFFFFF;
+  float fx = 0.0f;
   #pragma unroll
   for (int k = 0; k < kPer; ++k)
     #pragma unroll
     for (int e = 0; e < VE; ++e) {
-      const float x = wv[k * VE + e];
+      const float xt = Elem<DT>::get(vt[k], e);
+      const float xa = Elem<DT>::get(va[k], e), xb = Elem<DT>::get(vb[k], e);
+      const float x = bonus ? bonus_elem(xt, rk.c, rk.Rf) : resid_elem(xt, xa, xb, rk);
       run += (double)x;
-      if (x > 0.0f && run > target && first_ok == 0x7FFFFFFF)
+      if (x > 0.0f && run > target && first_ok == 0x7FFFFFFF) {
         first_ok = (int)((g.vbeg + rel + k) * VE + e - g.e0);
+        fx = bonus ? xt : fuse_masked(xt, xa, xb, A.beta);
+      }
     }
   int pick = block_min_i(first_ok, sm);
   if (pick == 0x7FFFFFFF) {
     // rounding left the target past the segment's own sum: its last nonzero
     const int neg = block_min_i(last_pos >= 0 ? -last_pos : 0x7FFFFFFF, sm);
     pick = (neg == 0x7FFFFFFF) ? -1 : -neg;
+  } else {
+    if (first_ok == pick) {
+      sm.flags[2] = 1;
+      sm.dd[3] = (double)fx;
+    }
+    __syncthreads();
   }
   return pick;
 }
@@ -631,11 +678,17 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
     const double u = (double)A.u[(size_t)req * (K + 1) + K];
     int pick = cdf_pick<DT>(A, req, j, u, bonus, sm);
     const RowGeo g = row_geo<DT>(A, req * (K + 1) + j);
+    const bool have_x = pick >= 0 && sm.flags[2] != 0;
     if (pick < 0) pick = row_argmax_f<DT>(A, g, sm);
     next = pick;
-    const long long idx = g.e0 + next;
-    float x = Elem<DT>::load_one(A.t, idx);
-    if (!bonus) x = fuse_masked(x, Elem<DT>::load_one(A.a, idx), Elem<DT>::load_one(A.b, idx), A.beta);
+    float x;
+    if (have_x) {
+      x = (float)sm.dd[3];
+    } else {
+      const long long idx = g.e0 + next;
+      x = Elem<DT>::load_one(A.t, idx);
+      if (!bonus) x = fuse_masked(x, Elem<DT>::load_one(A.a, idx), Elem<DT>::load_one(A.b, idx), A.beta);
+    }
     const double c = (double)__uint_as_float(sm.rows[j][D_C]);
     const double l2 = u2d(sm.rows[j][D_L2E_LO], sm.rows[j][D_L2E_HI]);
     lpn = (float)(((double)x * c - l2) * kLn2);
