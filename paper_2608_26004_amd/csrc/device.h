@@ -62,9 +62,9 @@ enum { R1_M = 0, R1_S = kSlots, R1_ARG = 2 * kSlots, R1_NEQ = 2 * kSlots + 1, R1
 // Decision record of one request: a header and one block per row, published
 // by the decide item; pass-2 and pick items load it into LDS (Smem::req,
 // Smem::rows).
-enum { H_STATE = 0, H_J = 1, H_TASK_LO = 2, H_TASK_HI = 3, H_USED = 4, kDecHdr = 8 };
+enum { H_STATE = 0, H_J = 1, H_TASK_LO = 2, H_TASK_HI = 3, H_SAMP = 4, H_USED = 5, kDecHdr = 8 };
 enum { kStateFinal = 1, kStatePending = 2 };
-enum { R_J = 0, R_TASK_LO = 1, R_TASK_HI = 2, R_FIN = 3, kReqWords = 4 };
+enum { R_J = 0, R_TASK_LO = 1, R_TASK_HI = 2, R_FIN = 3, R_SAMP = 4, kReqWords = 5 };
 enum {
   D_TASK = 0,   // pass-2 work on the row: kTaskJsd | kTaskRes | kTaskBonus
   D_C,          // exponent scale of the row's emission distribution (log2 e / tau, or log2 e)
@@ -207,6 +207,18 @@ DEV void load_tagged(const KArgs& A, const uint64_t* sentinel, F&& load) {
   BlockPoll bp;
   while (!bp.done(load(), A)) {
   }
+}
+
+// The fp64 value in the tagged slot pair at p (low word first); both loads
+// go out together, and the pair is polled until both carry the epoch.
+DEV double wait_pair(const uint64_t* p, const KArgs& A) {
+  uint64_t lo = ld_tag(p), hi = ld_tag(p + 1);
+  Poll pl;
+  while (!(tag_ok(lo, A.epoch) && tag_ok(hi, A.epoch)) && pl.again(A)) {
+    lo = ld_tag(p);
+    hi = ld_tag(p + 1);
+  }
+  return payd(lo, hi);
 }
 
 // Poll a tagged slot until it carries the launch epoch (bounded).
@@ -424,6 +436,25 @@ DEV float sload_f32(const void* base, long long idx) {
   return __uint_as_float(((cptr32)base)[idx]);
 }
 
+// The geometry of a row without its temperature (kind and c unset): for
+// the items that only address the row, so that no load of tau stands
+// before their first memory access.
+template <int DT>
+DEV RowGeo row_span(const KArgs& A, int row) {
+  constexpr int VE = Elem<DT>::VE;
+  RowGeo g;
+  g.row = row;
+  g.req = row / (A.K + 1);
+  g.pos = row - g.req * (A.K + 1);
+  g.tau = 0.0f;
+  g.kind = -1;
+  g.c = 0.0f;
+  g.e0 = (long long)row * A.V;
+  g.vbeg = g.e0 / VE;
+  g.vend = (g.e0 + A.V + VE - 1) / VE;
+  return g;
+}
+
 template <int DT>
 DEV RowGeo row_geo(const KArgs& A, int row) {
   constexpr int VE = Elem<DT>::VE;
@@ -515,10 +546,12 @@ DEV float sload_elem(const void* base, long long idx) {
   return __uint_as_float(((cptr32)base)[idx]);
 }
 
+// The draft token's logits and the caller's proposal probability and
+// uniform for draft row g (g.pos < K); a bonus row gets neutral values.
 template <int DT>
 DEV Gather sgather(const KArgs& A, const RowGeo& g) {
   Gather q{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
-  if (kind_draft(g.kind)) {
+  if (g.pos < A.K) {
     int dtok = (int)((cptr32)(const void*)A.d)[g.req * A.K + g.pos];
     dtok = dtok < 0 ? 0 : (dtok >= A.V ? A.V - 1 : dtok);
     const long long idx = g.e0 + dtok;

@@ -148,6 +148,15 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
     const int nr = min(rpg, nrow - r0);
     const bool have = li < nr;
     const int i = r0 + (have ? li : 0);
+    // first requests: the records, the draft token and its logits (row
+    // leaders), then the temperature; none waits for another but the
+    // logits for the token
+    const uint64_t* base = A.rec1 + ((size_t)(req * nrow + i) * S + ch) * kR1;
+    uint64_t r[R1_USED];
+    #pragma unroll
+    for (int j = 0; j < R1_USED; ++j) r[j] = have ? ld_tag(base + j) : ((uint64_t)A.epoch << 32);
+    Gather gq{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
+    if (have && ch == 0) gq = sgather<DT>(A, row_span<DT>(A, req * nrow + i));
     const RowGeo g = row_geo<DT>(A, req * nrow + i);
     const bool draft = kind_draft(g.kind);
     float cs[kSlots];
@@ -156,12 +165,15 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
     cs[sB] = kL2E;
     cs[sF] = g.c;
     cs[sAT] = g.c;
-    // the row's first thread gathers the draft token's logits meanwhile
-    Gather gq{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
-    if (have && ch == 0) gq = sgather<DT>(A, g);
-    uint64_t r[R1_USED];
-    const uint64_t* base = A.rec1 + ((size_t)g.row * S + ch) * kR1;
+    bool first = true;
     load_tagged(A, sentinel, [&]() {
+      if (first) {
+        first = false;
+        bool ok = true;
+        #pragma unroll
+        for (int j = 0; j < R1_USED; ++j) ok = ok && tag_ok(r[j], A.epoch);
+        return ok;
+      }
       bool ok = true;
       #pragma unroll
       for (int j = 0; j < R1_USED; ++j) {
@@ -238,6 +250,7 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
       sm.req[R_TASK_LO] = (uint32_t)tmask;
       sm.req[R_TASK_HI] = (uint32_t)(tmask >> 32);
       sm.req[R_FIN] = fin ? 1u : 0u;
+      sm.req[R_SAMP] = samp ? 1u : 0u;
     }
   }
   __syncthreads();
@@ -284,6 +297,7 @@ DEV void decide_item(const KArgs& A, int req, Smem& sm) {
       st_tag(hdr + H_J, sm.req[R_J], A.epoch);
       st_tag(hdr + H_TASK_LO, sm.req[R_TASK_LO], A.epoch);
       st_tag(hdr + H_TASK_HI, sm.req[R_TASK_HI], A.epoch);
+      st_tag(hdr + H_SAMP, sm.req[R_SAMP], A.epoch);
       st_tag(hdr + H_STATE, fin ? kStateFinal : kStatePending, A.epoch);
     }
     if (fin) {
@@ -336,8 +350,10 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
         sm.req[R_J] = pay(v[q]);
       } else if (k == H_TASK_LO) {
         sm.req[R_TASK_LO] = pay(v[q]);
-      } else {
+      } else if (k == H_TASK_HI) {
         sm.req[R_TASK_HI] = pay(v[q]);
+      } else {
+        sm.req[R_SAMP] = pay(v[q]);
       }
     }
   }
@@ -411,7 +427,7 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
     tmask &= tmask - 1;
     const uint32_t* cst = sm.rows[i];
     const uint32_t task = cst[D_TASK];
-    const RowGeo g = row_geo<DT>(A, req * (A.K + 1) + i);
+    const RowGeo g = row_span<DT>(A, req * (A.K + 1) + i);
     const bool dj = task & kTaskJsd, dr = task & kTaskRes, db = task & kTaskBonus;
     const ResidConst rk = resid_const(A, cst);
     const JsdConst jk = jsd_const(cst);
@@ -457,7 +473,7 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
   constexpr int VE = Elem<DT>::VE;
   constexpr int kPer = kSegVec / kThreads;   // vectors per thread in a segment
   const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
-  const RowGeo g = row_geo<DT>(A, req * (A.K + 1) + i);
+  const RowGeo g = row_span<DT>(A, req * (A.K + 1) + i);
   const int nseg = A.S * kWaves;
   if (tid == 0) sm.flags[2] = 0;
   double target;
@@ -469,7 +485,7 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
     double v = 0.0;
     if (sg < nseg) {
       const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
-      v = payd(wait_tag(p, A), wait_tag(p + 1, A));
+      v = wait_pair(p, A);
     }
     double incl, excl;
     block_scan(v, sm, incl, excl);
@@ -491,8 +507,7 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
       double tot = 0.0;
       for (int sg = lane; sg < nseg; sg += 64) {
         const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
-        const uint64_t lo = wait_tag(p, A), hi = wait_tag(p + 1, A);
-        tot += payd(lo, hi);
+        tot += wait_pair(p, A);
       }
       tot = wave_sum_d(tot);
       if (lane == 0) sm.dd[4] = tot;
@@ -634,6 +649,9 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
   const int lane = lane_id(), w = wave_id();
   const int K = A.K;
   if (load_decision(A, req, sm) != kStatePending) return;   // written by decide
+  const bool samp = sm.req[R_SAMP] != 0u;
+  // requested now, used after the segment sums arrive
+  const float uK = samp ? A.u[(size_t)req * (K + 1) + K] : 0.0f;
   // wave 0: D of the rows that have it, final decisions, the emitting row
   float lpd = 0.0f;
   double Dl = 0.0;
@@ -651,14 +669,14 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
       arg = v[D_ARG];
       lpe = __uint_as_float(v[D_LPEMIT]);
     }
-    if (task & kTaskJsd) {
-      double s = 0.0;
-      for (int m = 0; m < A.S; ++m) {
-        const uint64_t* p = p2_rec(A, req, lane, m) + P2_J;
-        s += payd(wait_tag(p, A), wait_tag(p + 1, A));
-      }
-      double D = 0.5 * kLn2 * s;   // the partials are in log2 units
-      Dl = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
+    // D of each row that has a JSD task: lane c takes chunk c's partial
+    for (unsigned long long jm = __ballot((task & kTaskJsd) != 0u); jm != 0; jm &= jm - 1) {
+      const int i = __builtin_ctzll(jm);
+      double part = 0.0;
+      for (int c = lane; c < A.S; c += 64) part += wait_pair(p2_rec(A, req, i, c) + P2_J, A);
+      part = wave_sum_d(part);
+      const double D = 0.5 * kLn2 * part;   // the partials are in log2 units
+      if (lane == i) Dl = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
     }
     const bool decided = st & kStDecided;
     const bool acc = decided ? (st & kStAccept) != 0 : (Dl > thr);
@@ -670,14 +688,13 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
   }
   __syncthreads();
   const int j = sm.flags[0];
-  const float tau = sload_f32(A.tau, req);
   int next = sm.flags[1];
   float lpn = (float)sm.dd[0];
-  if (tau > 0.0f) {
+  if (samp) {
     const bool bonus = j == K;
-    const double u = (double)A.u[(size_t)req * (K + 1) + K];
+    const double u = (double)uK;
     int pick = cdf_pick<DT>(A, req, j, u, bonus, sm);
-    const RowGeo g = row_geo<DT>(A, req * (K + 1) + j);
+    const RowGeo g = row_span<DT>(A, req * (K + 1) + j);
     const bool have_x = pick >= 0 && sm.flags[2] != 0;
     if (pick < 0) pick = row_argmax_f<DT>(A, g, sm);
     next = pick;
