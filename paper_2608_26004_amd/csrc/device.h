@@ -145,16 +145,20 @@ DEV void err_count(const uint32_t* e) {
   __hip_atomic_fetch_add(const_cast<uint32_t*>(e), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 // Bounded polling with exponential backoff: the n-th retry sleeps
-// 128 * 2^min(n, 5) cycles, so a wave that waits long issues few loads and
-// leaves the memory system to the streaming work; a wait gives up (and counts
-// an error) after kPollTicks of the 100 MHz real-time clock.
+// 128 * 2^min(n, kPollMaxShift) cycles, so a wave that waits long issues few
+// loads and leaves the memory system to the streaming work; a wait gives up
+// (and counts an error) after kPollTicks of the 100 MHz real-time clock.
+#ifndef ASYMSPEC_POLL_SHIFT
+#define ASYMSPEC_POLL_SHIFT 3
+#endif
+constexpr int kPollMaxShift = ASYMSPEC_POLL_SHIFT;
 struct Poll {
   uint64_t t0;
   int n;
   DEV Poll() : t0(__builtin_amdgcn_s_memrealtime()), n(0) {}
   // Sleeps before the next poll; false once the wait has timed out.
   DEV bool again(const KArgs& A) {
-    const int reps = 1 << (n < 5 ? n : 5);
+    const int reps = 1 << (n < kPollMaxShift ? n : kPollMaxShift);
     for (int i = 0; i < reps; ++i) __builtin_amdgcn_s_sleep(2);
     ++n;
     if (__builtin_amdgcn_s_memrealtime() - t0 > kPollTicks) {
@@ -175,7 +179,7 @@ struct BlockPoll {
   DEV BlockPoll() : t0(__builtin_amdgcn_s_memrealtime()), n(0) {}
   DEV bool done(bool ok, const KArgs& A) {
     if (__syncthreads_and(ok)) return true;
-    const int reps = 1 << (n < 5 ? n : 5);
+    const int reps = 1 << (n < kPollMaxShift ? n : kPollMaxShift);
     for (int i = 0; i < reps; ++i) __builtin_amdgcn_s_sleep(2);
     ++n;
     const bool late = threadIdx.x == 0 && __builtin_amdgcn_s_memrealtime() - t0 > kPollTicks;

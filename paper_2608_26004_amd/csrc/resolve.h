@@ -322,8 +322,7 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
   const int nw = H_USED + nrow * D_USED;
   constexpr int kPer = ((kMaxK + 1) * D_USED + H_USED + kThreads - 1) / kThreads;
   uint64_t v[kPer];
-  // the header goes out after the rows: a waiting workgroup polls it only
-  load_tagged(A, dec_hdr(A, req) + H_STATE, [&]() {
+  auto load = [&]() {
     bool ok = true;
     #pragma unroll
     for (int q = 0; q < kPer; ++q) {
@@ -336,7 +335,9 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
       }
     }
     return ok;
-  });
+  };
+  // the header goes out after the rows: a waiting workgroup polls it only
+  load_tagged(A, dec_hdr(A, req) + H_STATE, load);
   #pragma unroll
   for (int q = 0; q < kPer; ++q) {
     const int k = tid + q * kThreads;
