@@ -43,6 +43,19 @@ Conventions fixed here (each is listed with its reason in the design doc):
   contribute 0; the result is clamped to [0, ln 2].
 * Each request's drafts/uniforms come in as inputs; this module draws no
   random numbers.
+
+Variants the paper compares against (Sec. 5 mechanism ablation; App. B
+"Models and hyperparameters" and the JSD-vs-KL table of App. C), selected by
+``gate_mode`` and ``delta_mode``:
+
+* gate FIXED   gamma_eff = gamma (standard speculative acceptance);
+* gate KL      D_i = KL(softmax(a_i) || softmax(b_i)), natural log, not
+               bounded (P = 0 terms are 0; P > 0 where Q = 0 gives +inf);
+* gate LAMBDA  D_i = lambda * Delta_i(d_i), Delta = log softmax(a_i) -
+               log softmax(b_i) taken at the draft token (the paper writes
+               Delta as a vector; the gate needs its value at d_i);
+* delta A      raw-augmented fusion, delta_i = a_i          (f = t + beta a);
+* delta TB     SCD-style fusion, delta_i = t_i - b_i        (f = t + beta (t - b)).
 """
 
 from __future__ import annotations
@@ -56,6 +69,12 @@ LN2 = math.log(2.0)
 
 GATE_CDA = 0      # gamma_eff = gamma * exp(-D)         (Sec. 3.3, Eq. 3)
 GATE_FIXED = 1    # gamma_eff = gamma  (fixed-gamma baseline of App. B)
+GATE_KL = 2       # gamma * exp(-KL(P || Q))            (App. C, JSD vs. KL)
+GATE_LAMBDA = 3   # gamma * exp(-lambda * Delta(d))     (App. B, tuned-lambda foil)
+
+DELTA_AB = 0      # delta = a - b   (Eq. 1, the paper's same-model source)
+DELTA_A = 1       # delta = a       (raw-augmented, Sec. 5 ablation)
+DELTA_TB = 2      # delta = t - b   (SCD-style, Sec. 5 ablation)
 
 
 # --------------------------------------------------------------------------
@@ -82,16 +101,24 @@ def to_f32(x: np.ndarray) -> np.ndarray:
 # Sec. 3.2, Eq. 1-2: the fused logits.
 # --------------------------------------------------------------------------
 def fused_logits_f32(t32: np.ndarray, a32: np.ndarray, b32: np.ndarray,
-                     beta: float) -> np.ndarray:
-    """f = t + beta * (a - b), in fp32, in that order (Eq. 1 gives
+                     beta: float, delta_mode: int = DELTA_AB) -> np.ndarray:
+    """f = t + beta * delta, in fp32, in that order (Eq. 1 gives
     delta = a - b in logit space; Eq. 2 adds beta * delta to the verifier
-    logits).  NaN (only from -inf - (-inf)) is returned as -inf: a token both
-    drafter views mask stays masked."""
+    logits; the ablation's alternatives take delta = a or delta = t - b).
+    NaN (only from -inf - (-inf), or inf * 0) is returned as -inf: the token
+    is masked."""
     t32 = np.asarray(t32, np.float32)
     a32 = np.asarray(a32, np.float32)
     b32 = np.asarray(b32, np.float32)
     with np.errstate(invalid="ignore", over="ignore"):
-        delta = np.subtract(a32, b32, dtype=np.float32)
+        if delta_mode == DELTA_AB:
+            delta = np.subtract(a32, b32, dtype=np.float32)
+        elif delta_mode == DELTA_A:
+            delta = a32
+        elif delta_mode == DELTA_TB:
+            delta = np.subtract(t32, b32, dtype=np.float32)
+        else:
+            raise ValueError(delta_mode)
         scaled = np.multiply(np.float32(beta), delta, dtype=np.float32)
         f = np.add(t32, scaled, dtype=np.float32)
     return np.where(np.isnan(f), np.float32(-np.inf), f).astype(np.float32)
@@ -143,11 +170,46 @@ def jsd(a: np.ndarray, b: np.ndarray) -> float:
     return min(max(d, 0.0), LN2)
 
 
+def kl(a: np.ndarray, b: np.ndarray) -> float:
+    """KL(softmax(a) || softmax(b)) = sum_x P log(P/Q), natural log, not
+    bounded.  Terms with P = 0 are 0; a token with P > 0 and Q = 0 makes it
+    +inf."""
+    P = softmax(a)
+    Q = softmax(b)
+    nz = P > 0
+    if np.any(Q[nz] == 0):
+        return math.inf
+    return float(np.sum(P[nz] * np.log(P[nz] / Q[nz])))
+
+
+def log_ratio_at(a: np.ndarray, b: np.ndarray, d: int) -> float:
+    """Delta(d) = log softmax(a)[d] - log softmax(b)[d] (the tuned-lambda
+    gate's per-position drafter log-probability difference, at the draft
+    token)."""
+    la = float(log_softmax(a)[d])
+    lb = float(log_softmax(b)[d])
+    if la == -math.inf and lb == -math.inf:
+        return math.nan
+    return la - lb
+
+
 def gamma_eff(D: float, gamma: float, gate_mode: int = GATE_CDA) -> float:
-    """Eq. 3: gamma_eff = gamma * exp(-D) (CDA), or gamma (fixed-gamma gate)."""
+    """Eq. 3: gamma_eff = gamma * exp(-D) (CDA, and the KL and lambda
+    variants with their own D), or gamma (fixed-gamma gate)."""
     if gate_mode == GATE_FIXED:
         return float(gamma)
     return float(gamma) * math.exp(-float(D))
+
+
+def divergence(a: np.ndarray, b: np.ndarray, d: int, gate_mode: int,
+               lam: float) -> float:
+    """The D of gamma_eff = gamma * exp(-D) for each gate (JSD for the CDA
+    and fixed gates, where the fixed gate reports it without using it)."""
+    if gate_mode == GATE_KL:
+        return kl(a, b)
+    if gate_mode == GATE_LAMBDA:
+        return float(lam) * log_ratio_at(a, b, d)
+    return jsd(a, b)
 
 
 # --------------------------------------------------------------------------
@@ -208,7 +270,8 @@ def verify_request(t: np.ndarray, a: np.ndarray, b: np.ndarray,
                    draft_tokens: np.ndarray, draft_probs: np.ndarray | None,
                    uniforms: np.ndarray, temperature: float,
                    beta: float = 1.0, gamma: float = 0.5,
-                   gate_mode: int = GATE_CDA) -> RequestResult:
+                   gate_mode: int = GATE_CDA, delta_mode: int = DELTA_AB,
+                   lam: float = 0.1) -> RequestResult:
     """One request of Alg. 1's decision step.
 
     t, a, b: stored logits [K+1][V] (uint16 bf16 bits or fp32).  Row K is the
@@ -229,16 +292,21 @@ def verify_request(t: np.ndarray, a: np.ndarray, b: np.ndarray,
     f_rows = []
     for i in range(K):
         d = int(draft_tokens[i])
-        f = fused_logits_f32(t32[i], a32[i], b32[i], beta)       # Eq. 1-2
+        f = fused_logits_f32(t32[i], a32[i], b32[i], beta, delta_mode)  # Eq. 1-2
         f_rows.append(f)
-        D = jsd(a32[i], b32[i])                                  # Eq. 3
+        D = divergence(a32[i], b32[i], d, gate_mode, lam)        # Eq. 3
         ge = gamma_eff(D, gamma, gate_mode)                      # Eq. 3
         r = RowResult(D=D, gamma_eff=ge)
+        # ln gamma_eff = ln gamma - D, kept in log form (D may be +inf)
+        lge = math.log(gamma) if gate_mode == GATE_FIXED else math.log(gamma) - D
         if greedy:
             # Eq. 4 in log form: log p_t(d) - log p_b(d) - log gamma_eff > 0
             lpt = log_softmax(t32[i])[d]
             lpb = log_softmax(b32[i])[d]
-            margin = lpt - lpb - math.log(ge)
+            with np.errstate(invalid="ignore"):
+                margin = float(lpt - lpb - lge)
+            if math.isnan(margin):
+                margin = -math.inf
             r.margin = margin
             r.accept = bool(margin > 0.0)
             r.decision_gap = abs(math.expm1(margin)) if np.isfinite(margin) else math.inf
@@ -255,7 +323,8 @@ def verify_request(t: np.ndarray, a: np.ndarray, b: np.ndarray,
             elif lp_d == -math.inf:
                 ratio = 0.0
             else:
-                ratio = min(1.0, math.exp(lp_d - lq_d - math.log(ge)))
+                x = lp_d - lq_d - lge
+                ratio = 0.0 if math.isnan(x) else min(1.0, math.exp(min(x, 0.0)))
             r.ratio = ratio
             r.accept = bool(u[i] < ratio)
             r.decision_gap = abs(ratio - float(u[i]))
@@ -311,7 +380,8 @@ def verify_request(t: np.ndarray, a: np.ndarray, b: np.ndarray,
 
 def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
                 beta: float = 1.0, gamma: float = 0.5,
-                gate_mode: int = GATE_CDA, requests=None):
+                gate_mode: int = GATE_CDA, requests=None,
+                delta_mode: int = DELTA_AB, lam: float = 0.1):
     """Batch form over requests: t, a, b [B][K+1][V]; draft_tokens [B][K];
     draft_probs [B][K] or None; uniforms [B][K+1]; temperature [B].
     ``requests`` restricts the work to a subset of request indices.
@@ -330,7 +400,8 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
         r = verify_request(t[bi], a[bi], b[bi], draft_tokens[bi],
                            None if draft_probs is None else draft_probs[bi],
                            uniforms[bi], float(temperature[bi]),
-                           beta=beta, gamma=gamma, gate_mode=gate_mode)
+                           beta=beta, gamma=gamma, gate_mode=gate_mode,
+                           delta_mode=delta_mode, lam=lam)
         acc[k] = r.accept_len
         nxt[k] = r.next_token
         flp[k] = r.fused_logprobs

@@ -346,3 +346,122 @@ def test_draft_probs_given_or_computed_agree():
         if not (r1[k].near_tie(1e-5) or r2[k].near_tie(1e-5)):
             assert acc1[k] == acc2[k] and nxt1[k] == nxt2[k]
     np.testing.assert_allclose(flp1[:, :3], flp2[:, :3], atol=1e-12)
+
+
+# ------------------------------------------- gate and fusion variants --
+# App. B (fixed and tuned-lambda gates), App. C (KL in place of the JSD),
+# Sec. 5 mechanism ablation (delta = a and delta = t - b).
+
+def test_kl_matches_scipy_rel_entr():
+    """KL(softmax(a) || softmax(b)) in natural log, against scipy."""
+    rng = np.random.default_rng(31)
+    for V in (2, 17, 1000):
+        a, b = rand_rows(V, 2, rng=rng)
+        P = sps.softmax(a.astype(np.float64))
+        Q = sps.softmax(b.astype(np.float64))
+        assert abs(O.kl(a, b) - float(np.sum(sps.rel_entr(P, Q)))) < 1e-10
+
+
+def test_kl_closed_form_and_special_cases():
+    """The V = 2 value of tests/golden; zero for equal distributions
+    (softmax is shift invariant); masked P terms drop out; a token with
+    P > 0 and Q = 0 makes it infinite (the gate is unbounded)."""
+    g = json.load(open(os.path.join(GOLDEN, "worked_example_gates_v2.json")))
+    a = np.log(np.array([0.5, 0.5]))
+    b = np.log(np.array([0.75, 0.25]))
+    assert abs(O.kl(a, b) - eval(g["kl_closed_form"], {"ln": math.log})) < 1e-12
+    x = rand_rows(50, 1)[0].astype(np.float64)
+    assert abs(O.kl(x, x + 3.0)) < 1e-12
+    am = x.copy(); am[7] = -np.inf
+    assert math.isfinite(O.kl(am, x))
+    assert O.kl(x, am) == math.inf
+
+
+def test_kl_pinsker_and_small_divergence_ratio():
+    """Pinsker: KL >= 2 TV^2; near equal distributions KL ~ 4 JSD (both are
+    chi^2 / 2 and chi^2 / 8 to second order)."""
+    rng = np.random.default_rng(32)
+    for _ in range(20):
+        a, b = rand_rows(64, 2, rng=rng)
+        P = sps.softmax(a.astype(np.float64)); Q = sps.softmax(b.astype(np.float64))
+        assert O.kl(a, b) >= 2.0 * (0.5 * np.abs(P - Q).sum()) ** 2 - 1e-12
+    a = rand_rows(500, 1, rng=rng)[0].astype(np.float64)
+    b = a + 1e-3 * rng.standard_normal(500)
+    r = O.kl(a, b) / O.jsd(a, b)
+    assert 3.95 < r < 4.05
+
+
+def test_log_ratio_at_draft_token():
+    """Delta(d) = log softmax(a)[d] - log softmax(b)[d], against scipy."""
+    rng = np.random.default_rng(33)
+    a, b = rand_rows(40, 2, rng=rng)
+    for d in (0, 13, 39):
+        ref = float(sps.log_softmax(a.astype(np.float64))[d] - sps.log_softmax(b.astype(np.float64))[d])
+        assert abs(O.log_ratio_at(a, b, d) - ref) < 1e-12
+
+
+def test_worked_example_kl_and_lambda_gates():
+    """App. B/C gates on the two-token example of tests/golden: the KL gate
+    accepts like CDA, the lambda gate (Delta < 0 raises gamma_eff above
+    gamma) rejects like the fixed gate."""
+    g = json.load(open(os.path.join(GOLDEN, "worked_example_v2.json")))
+    gg = json.load(open(os.path.join(GOLDEN, "worked_example_gates_v2.json")))
+    t = np.stack([_row(r) for r in g["t"]])
+    a = np.stack([_row(r) for r in g["a"]])
+    b = np.stack([_row(r) for r in g["b"]])
+    d = np.array(g["draft_tokens"], np.int32)
+    u = np.zeros(2, np.float32)
+    env = {"ln": math.log, "sqrt": math.sqrt}
+    r = O.verify_request(t, a, b, d, None, u, 0.0, beta=1.0, gamma=0.5, gate_mode=O.GATE_KL)
+    assert (r.accept_len, r.next_token) == (gg["kl"]["accept_len"], gg["kl"]["next_token"])
+    assert abs(r.rows[0].gamma_eff - eval(gg["kl"]["gamma_eff"], env)) < 1e-6
+    lam = gg["lambda"]["lam"]
+    r = O.verify_request(t, a, b, d, None, u, 0.0, beta=1.0, gamma=0.5,
+                         gate_mode=O.GATE_LAMBDA, lam=lam)
+    assert (r.accept_len, r.next_token) == (gg["lambda"]["accept_len"], gg["lambda"]["next_token"])
+    assert abs(r.rows[0].D - eval(gg["lambda"]["D"], env)) < 1e-6
+    assert abs(r.rows[0].gamma_eff - eval(gg["lambda"]["gamma_eff"], env)) < 1e-6
+
+
+def test_lambda_zero_is_the_fixed_gate():
+    """gamma exp(-0 * Delta) = gamma: decisions match the fixed gate."""
+    rng = np.random.default_rng(34)
+    for tau in (0.0, 1.0):
+        t, a, b = (rand_rows(64, 4, rng=rng) for _ in range(3))
+        d = rng.integers(0, 64, 3).astype(np.int32)
+        u = rng.random(4).astype(np.float32)
+        r0 = O.verify_request(t, a, b, d, None, u, tau, gate_mode=O.GATE_LAMBDA, lam=0.0)
+        r1 = O.verify_request(t, a, b, d, None, u, tau, gate_mode=O.GATE_FIXED)
+        assert (r0.accept_len, r0.next_token) == (r1.accept_len, r1.next_token)
+
+
+def _lognorm(x):
+    return x - sps.logsumexp(x)
+
+
+def test_delta_modes_as_products_of_experts():
+    """Sec. 5 ablation sources, by shift invariance of softmax: the fused
+    distribution is p_t p_a^beta / p_b^beta (ours), p_t p_a^beta
+    (raw-augmented) and p_t^(1+beta) / p_b^beta (SCD-style), up to the fp32
+    rounding of f."""
+    rng = np.random.default_rng(35)
+    t, a, b = rand_rows(300, 3, rng=rng)
+    lt, la, lb = (sps.log_softmax(x.astype(np.float64)) for x in (t, a, b))
+    beta = 0.7
+    cases = {O.DELTA_AB: lt + beta * (la - lb), O.DELTA_A: lt + beta * la,
+             O.DELTA_TB: (1 + beta) * lt - beta * lb}
+    for mode, ref in cases.items():
+        f = O.fused_logits_f32(t, a, b, beta, mode)
+        assert np.max(np.abs(O.log_softmax(f) - _lognorm(ref))) < 1e-5
+
+
+def test_delta_modes_degenerate_cases():
+    """beta = 0 leaves t in every mode; the raw-augmented source with a = 0
+    and the SCD-style source with b = t also leave t (bitwise, fp32)."""
+    rng = np.random.default_rng(36)
+    t, a, b = rand_rows(64, 3, rng=rng)
+    for mode in (O.DELTA_AB, O.DELTA_A, O.DELTA_TB):
+        assert np.array_equal(O.fused_logits_f32(t, a, b, 0.0, mode).view(np.uint32), t.view(np.uint32))
+    z = np.zeros_like(a)
+    assert np.array_equal(O.fused_logits_f32(t, z, b, 1.0, O.DELTA_A).view(np.uint32), t.view(np.uint32))
+    assert np.array_equal(O.fused_logits_f32(t, a, t, 1.0, O.DELTA_TB).view(np.uint32), t.view(np.uint32))
