@@ -63,16 +63,30 @@ extern "C" {
 #define ASYMSPEC_FP32 1           /* IEEE binary32, 4 bytes per logit         */
 
 /* ---- acceptance gates -------------------------------------------------- */
-#define ASYMSPEC_GATE_CDA   0     /* gamma_eff = gamma * exp(-JSD)   (Eq. 3)          */
-#define ASYMSPEC_GATE_FIXED 1     /* gamma_eff = gamma, the fixed-gamma gate the paper
+#define ASYMSPEC_GATE_CDA    0    /* gamma_eff = gamma * exp(-JSD)   (Eq. 3)          */
+#define ASYMSPEC_GATE_FIXED  1    /* gamma_eff = gamma, the fixed-gamma gate the paper
                                      compares against (App. B, "Models and
                                      hyperparameters") */
+#define ASYMSPEC_GATE_KL     2    /* gamma_eff = gamma * exp(-KL(P || Q)), P and Q the
+                                     drafter views' softmaxes: the KL instantiation of
+                                     D in the JSD-vs-KL table (App. C); not bounded */
+#define ASYMSPEC_GATE_LAMBDA 3    /* gamma_eff = gamma * exp(-lambda * Delta(d)),
+                                     Delta = log softmax(a) - log softmax(b) at the
+                                     draft token: the tuned-lambda gate (App. B) */
+
+/* ---- sources of the context-gain signal delta (Eq. 1-2) ---------------- */
+#define ASYMSPEC_DELTA_AB 0       /* delta = a - b (Eq. 1, the paper's method)        */
+#define ASYMSPEC_DELTA_A  1       /* delta = a, raw-augmented (Sec. 5 ablation)       */
+#define ASYMSPEC_DELTA_TB 2       /* delta = t - b, SCD-style (Sec. 5 ablation)       */
 
 typedef struct asymspec_params {
-  float beta;        /* fusion weight of Eq. 2; finite, >= 0 (paper default 1.0) */
-  float gamma;       /* base threshold of Eq. 3-4; in (0, 1] (paper default 0.5)  */
-  int32_t gate_mode; /* ASYMSPEC_GATE_CDA or ASYMSPEC_GATE_FIXED                  */
-  uint32_t flags;    /* reserved, must be 0                                       */
+  float beta;         /* fusion weight of Eq. 2; finite, >= 0 (paper default 1.0) */
+  float gamma;        /* base threshold of Eq. 3-4; in (0, 1] (paper default 0.5)  */
+  int32_t gate_mode;  /* ASYMSPEC_GATE_*                                           */
+  uint32_t flags;     /* reserved, must be 0                                       */
+  int32_t delta_mode; /* ASYMSPEC_DELTA_* (ASYMSPEC_DELTA_AB for the paper)        */
+  float lambda;       /* scale of ASYMSPEC_GATE_LAMBDA, finite (paper default 0.1);
+                         ignored by the other gates                                */
 } asymspec_params;
 
 /* Bytes of device workspace asymspec_fuse_verify needs for this shape
@@ -115,7 +129,10 @@ int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stre
  *                       log-probability of next_token under the distribution
  *                       that emitted it (the fused row at the first rejection,
  *                       or the verifier's bonus row)
- *   gate_out            [B][K][2] float out (D_i, gamma_eff_i), or NULL
+ *   gate_out            [B][K][2] float out (D_i, gamma_eff_i), or NULL; D_i
+ *                       is the JSD (CDA and fixed gates), the KL (KL gate) or
+ *                       lambda * Delta_i(d_i) (lambda gate), and gamma_eff_i =
+ *                       gamma (fixed gate) or gamma * exp(-D_i)
  *   workspace           device scratch of >= asymspec_workspace_size bytes,
  *                       256-byte aligned, contents opaque between calls
  *   stream              hipStream_t or NULL

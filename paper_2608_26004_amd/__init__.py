@@ -12,12 +12,18 @@ import ctypes
 import os
 
 __all__ = ["fuse_verify", "workspace_size", "Workspace", "load_library", "status_string",
-           "BF16", "FP32", "GATE_CDA", "GATE_FIXED", "AsymSpecError"]
+           "BF16", "FP32", "GATE_CDA", "GATE_FIXED", "GATE_KL", "GATE_LAMBDA",
+           "DELTA_AB", "DELTA_A", "DELTA_TB", "AsymSpecError"]
 
 BF16 = 0
 FP32 = 1
 GATE_CDA = 0
 GATE_FIXED = 1
+GATE_KL = 2
+GATE_LAMBDA = 3
+DELTA_AB = 0
+DELTA_A = 1
+DELTA_TB = 2
 
 OK = 0
 E_ARG = -1
@@ -38,7 +44,8 @@ class AsymSpecError(RuntimeError):
 
 class _Params(ctypes.Structure):
     _fields_ = [("beta", ctypes.c_float), ("gamma", ctypes.c_float),
-                ("gate_mode", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+                ("gate_mode", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("delta_mode", ctypes.c_int32), ("lam", ctypes.c_float)]
 
 
 def load_library(path: str | None = None):
@@ -105,12 +112,15 @@ _default_ws = {}
 
 def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
                 beta: float = 1.0, gamma: float = 0.5, gate_mode: int = GATE_CDA,
-                return_gate: bool = False, workspace: Workspace | None = None, out=None):
+                return_gate: bool = False, workspace: Workspace | None = None, out=None,
+                delta_mode: int = DELTA_AB, lam: float = 0.1):
     """One AsymSpec decision step on the current HIP stream.
 
     t, a, b: [B, K+1, V] torch.bfloat16 or torch.float32 on the GPU
     draft_tokens: [B, K] int32; draft_probs: [B, K] float32 or None;
     uniforms: [B, K+1] float32; temperature: [B] float32 (<= 0: greedy).
+    gate_mode: GATE_CDA (the paper), GATE_FIXED, GATE_KL or GATE_LAMBDA (with
+    scale lam); delta_mode: DELTA_AB (the paper), DELTA_A or DELTA_TB.
     Returns (accept_len [B] int32, next_token [B] int32,
              fused_logprobs [B, K+1] float32[, gate [B, K, 2] float32])."""
     import torch
@@ -153,7 +163,7 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     if workspace is None:
         workspace = _default_ws.setdefault(dev, Workspace(dev))
     wsbuf = workspace.get(ws_bytes, dev)
-    params = _Params(float(beta), float(gamma), int(gate_mode), 0)
+    params = _Params(float(beta), float(gamma), int(gate_mode), 0, int(delta_mode), float(lam))
     st = lib.asymspec_fuse_verify(_ptr(t), _ptr(a), _ptr(b), dt, _ptr(draft_tokens),
                                   _ptr(draft_probs), _ptr(uniforms), _ptr(temperature),
                                   B, K, V, ctypes.byref(params), _ptr(acc), _ptr(nxt),

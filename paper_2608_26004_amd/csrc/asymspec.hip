@@ -41,20 +41,20 @@
 
 namespace asym {
 
-template <int DT, bool kB1>
+template <int DT, bool kB1, int DM>
 DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
   const int i = sub / A.S, m = sub - (sub / A.S) * A.S;
   const int row = req * (A.K + 1) + i;
   const float tau = sload_f32(A.tau, req);
   if (i == A.K) {
-    if (tau > 0.0f) stats_item<DT, kSampleBonus, kB1>(A, row, m, sm);
-    else stats_item<DT, kGreedyBonus, kB1>(A, row, m, sm);
+    if (tau > 0.0f) stats_item<DT, kSampleBonus, kB1, DM>(A, row, m, sm);
+    else stats_item<DT, kGreedyBonus, kB1, DM>(A, row, m, sm);
   } else if (!(tau > 0.0f)) {
-    stats_item<DT, kGreedyDraft, kB1>(A, row, m, sm);
+    stats_item<DT, kGreedyDraft, kB1, DM>(A, row, m, sm);
   } else if (tau == 1.0f) {
-    stats_item<DT, kSampleDraft1, kB1>(A, row, m, sm);
+    stats_item<DT, kSampleDraft1, kB1, DM>(A, row, m, sm);
   } else {
-    stats_item<DT, kSampleDraftT, kB1>(A, row, m, sm);
+    stats_item<DT, kSampleDraftT, kB1, DM>(A, row, m, sm);
   }
 }
 
@@ -68,16 +68,16 @@ DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
 // running or queued behind workgroups that never wait: the list drains
 // whether or not every workgroup fits on the chip at once.  The waits are
 // bounded besides (Poll), and a timeout is counted in the workspace.
-template <int DT, bool kB1>
+template <int DT, bool kB1, int DM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ASYMSPEC_WAVES)))
 void fuse_verify_kernel(KArgs A) {
   __shared__ Smem sm;
   const Item it = sched_item(A.sc, A.K, A.S, (int)blockIdx.x);
   switch (it.type) {
-    case kItemStats: stats_dispatch<DT, kB1>(A, it.req, it.sub, sm); break;
+    case kItemStats: stats_dispatch<DT, kB1, DM>(A, it.req, it.sub, sm); break;
     case kItemDecide: decide_item<DT>(A, it.req, sm); break;
-    case kItemPass2: pass2_item<DT>(A, it.req, it.sub, sm); break;
-    case kItemPick: pick_item<DT>(A, it.req, sm); break;
+    case kItemPass2: pass2_item<DT, DM>(A, it.req, it.sub, sm); break;
+    case kItemPick: pick_item<DT, DM>(A, it.req, sm); break;
     default: break;
   }
 }
@@ -127,12 +127,24 @@ struct DevInfo {
 static DevInfo g_dev[64];
 static std::mutex g_dev_mu;
 
-static const void* kernel_ptr(int dtype, bool beta1) {
-  if (dtype == ASYMSPEC_BF16)
-    return beta1 ? (const void*)fuse_verify_kernel<ASYMSPEC_BF16, true>
-                 : (const void*)fuse_verify_kernel<ASYMSPEC_BF16, false>;
-  return beta1 ? (const void*)fuse_verify_kernel<ASYMSPEC_FP32, true>
-               : (const void*)fuse_verify_kernel<ASYMSPEC_FP32, false>;
+static_assert(kDeltaAB == ASYMSPEC_DELTA_AB && kDeltaA == ASYMSPEC_DELTA_A && kDeltaTB == ASYMSPEC_DELTA_TB,
+              "delta sources");
+
+// One kernel per storage type, beta == 1 or not, and source of delta.
+template <int DT>
+static const void* kernel_ptr_dt(bool beta1, int dm) {
+  if (beta1) {
+    if (dm == kDeltaA) return (const void*)fuse_verify_kernel<DT, true, kDeltaA>;
+    if (dm == kDeltaTB) return (const void*)fuse_verify_kernel<DT, true, kDeltaTB>;
+    return (const void*)fuse_verify_kernel<DT, true, kDeltaAB>;
+  }
+  if (dm == kDeltaA) return (const void*)fuse_verify_kernel<DT, false, kDeltaA>;
+  if (dm == kDeltaTB) return (const void*)fuse_verify_kernel<DT, false, kDeltaTB>;
+  return (const void*)fuse_verify_kernel<DT, false, kDeltaAB>;
+}
+static const void* kernel_ptr(int dtype, bool beta1, int dm) {
+  return dtype == ASYMSPEC_BF16 ? kernel_ptr_dt<ASYMSPEC_BF16>(beta1, dm)
+                                : kernel_ptr_dt<ASYMSPEC_FP32>(beta1, dm);
 }
 
 static const DevInfo* device_info() {
@@ -147,12 +159,14 @@ static const DevInfo* device_info() {
   di.n_cu = pr.multiProcessorCount;
   for (int dt = 0; dt < 2; ++dt) {
     int nb = 1 << 30;
-    for (int b1 = 0; b1 < 2; ++b1) {
-      int x = 0;
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&x, kernel_ptr(dt, b1 != 0), kThreads, 0) != hipSuccess)
-        return nullptr;
-      nb = std::min(nb, x);
-    }
+    for (int b1 = 0; b1 < 2; ++b1)
+      for (int dm = 0; dm < 3; ++dm) {
+        int x = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&x, kernel_ptr(dt, b1 != 0, dm), kThreads, 0) !=
+            hipSuccess)
+          return nullptr;
+        nb = std::min(nb, x);
+      }
     if (nb < 1) return nullptr;
     di.max_blocks[dt] = nb * di.n_cu;
   }
@@ -214,7 +228,9 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   if (K > 0 && (a == nullptr || b == nullptr || draft_tokens == nullptr)) return ASYMSPEC_E_ARG;
   if (!std::isfinite(params->beta) || params->beta < 0.0f) return ASYMSPEC_E_ARG;
   if (!(params->gamma > 0.0f && params->gamma <= 1.0f)) return ASYMSPEC_E_ARG;
-  if (params->gate_mode != ASYMSPEC_GATE_CDA && params->gate_mode != ASYMSPEC_GATE_FIXED) return ASYMSPEC_E_ARG;
+  if (params->gate_mode < ASYMSPEC_GATE_CDA || params->gate_mode > ASYMSPEC_GATE_LAMBDA) return ASYMSPEC_E_ARG;
+  if (params->delta_mode < ASYMSPEC_DELTA_AB || params->delta_mode > ASYMSPEC_DELTA_TB) return ASYMSPEC_E_ARG;
+  if (params->gate_mode == ASYMSPEC_GATE_LAMBDA && !std::isfinite(params->lambda)) return ASYMSPEC_E_ARG;
   if (params->flags != 0u) return ASYMSPEC_E_ARG;
   if (!aligned(t, 16) || (K > 0 && (!aligned(a, 16) || !aligned(b, 16)))) return ASYMSPEC_E_ALIGN;
   if (!aligned(uniforms, 4) || !aligned(temperature, 4) || !aligned(accept_len, 4) ||
@@ -242,6 +258,8 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   A.B = B; A.K = K; A.V = V; A.S = L.S;
   A.beta = params->beta; A.gamma = params->gamma; A.gate_mode = params->gate_mode;
   A.want_gate = gate_out != nullptr;
+  A.delta_mode = params->delta_mode;
+  A.lam = params->gate_mode == ASYMSPEC_GATE_LAMBDA ? params->lambda : 0.0f;
   A.ln_gamma = std::log((double)params->gamma);
   A.epoch = next_epoch();
   // lags scale with the number of workgroups the chip holds at once
@@ -249,7 +267,7 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   const int grid = A.sc.total;
 
   void* args[] = {&A};
-  const hipError_t e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f), dim3(grid),
+  const hipError_t e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f, params->delta_mode), dim3(grid),
                                        dim3(kThreads), args, 0, (hipStream_t)stream);
   if (e != hipSuccess) {
     (void)hipGetLastError();

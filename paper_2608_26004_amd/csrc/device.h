@@ -79,6 +79,7 @@ enum {
   D_L2E_LO, D_L2E_HI,   // log2 normaliser (fp64) of the emission distribution
   D_ARG,        // greedy: argmax of f (drafts) or t (bonus)
   D_LPEMIT,     // greedy: log-probability of that argmax
+  D_GD_LO, D_GD_HI,     // lambda gate: D = lambda * Delta(d) (fp64)
   D_USED,
   kDecRow = 24
 };
@@ -98,6 +99,8 @@ struct KArgs {
   unsigned long long stream_bytes;   // bytes of each logit array
   int B, K, V, S;
   float beta, gamma; int gate_mode; int want_gate;
+  int delta_mode;     // source of delta in f = t + beta * delta
+  float lam;          // scale of the lambda gate
   double ln_gamma;
   uint32_t epoch;
   Sched sc;
@@ -293,13 +296,32 @@ template <> struct Elem<ASYMSPEC_FP32> {
 // Fused logit of Eq. 2 in fp32: t + beta * (a - b), in that order, no
 // contraction.  A NaN (a = b = -inf) stays NaN here; consumers treat it as a
 // masked token (maxima ignore it, exponent arguments are clamped).
-DEV float fuse(float t, float a, float b, float beta) {
-  return __fadd_rn(t, __fmul_rn(beta, __fsub_rn(a, b)));
+// Sources of the context-gain signal: delta = a - b (Eq. 1), or the
+// mechanism ablation's delta = a (raw-augmented) and delta = t - b
+// (SCD-style).  The values match the public ASYMSPEC_DELTA_* constants.
+enum { kDeltaAB = 0, kDeltaA = 1, kDeltaTB = 2 };
+template <int DM>
+DEV float delta_of(float t, float a, float b) {
+  if (DM == kDeltaA) return a;
+  if (DM == kDeltaTB) return __fsub_rn(t, b);
+  return __fsub_rn(a, b);
 }
-// beta = 1: fl(1 * x) = x, so this is bit-identical to fuse(t, a, b, 1).
-DEV float fuse1(float t, float a, float b) { return __fadd_rn(t, __fsub_rn(a, b)); }
-DEV float fuse_masked(float t, float a, float b, float beta) {
-  const float f = fuse(t, a, b, beta);
+// f = fl(t + fl(beta * delta)), in this order and without contraction.
+template <int DM>
+DEV float fuse(float t, float a, float b, float beta) {
+  return __fadd_rn(t, __fmul_rn(beta, delta_of<DM>(t, a, b)));
+}
+// beta = 1: fl(1 * x) = x, so this is bit-identical to fuse<DM>(t, a, b, 1).
+template <int DM>
+DEV float fuse1(float t, float a, float b) { return __fadd_rn(t, delta_of<DM>(t, a, b)); }
+// The same with the source chosen at run time (the resolve items): the
+// identical operations, so bit-identical to fuse<DM>.
+DEV float fuse_rt(float t, float a, float b, float beta, int dm) {
+  const float d = dm == kDeltaA ? a : (dm == kDeltaTB ? __fsub_rn(t, b) : __fsub_rn(a, b));
+  return __fadd_rn(t, __fmul_rn(beta, d));
+}
+DEV float fuse_masked(float t, float a, float b, float beta, int dm) {
+  const float f = fuse_rt(t, a, b, beta, dm);
   return (f != f) ? -INFINITY : f;
 }
 
@@ -397,8 +419,9 @@ DEV void acc_vec(Acc& q, const float (&x)[VE], float c, int k) {
 struct ResidConst { float beta, c, Rf, isf, Rq, isq; };
 // max(0, p~(x) - q(x)) with p~ = softmax(f / tau), q = softmax(a / tau).  A
 // NaN fused logit (a masked token) gives p = NaN and max(NaN, 0) = 0.
+template <int DM>
 DEV float resid_elem(float t, float a, float b, const ResidConst& k) {
-  const float f = fuse(t, a, b, k.beta);
+  const float f = fuse<DM>(t, a, b, k.beta);
   const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(f, k.c, -k.Rf)) * k.isf;
   const float q = __builtin_amdgcn_exp2f(__builtin_fmaf(a, k.c, -k.Rq)) * k.isq;
   return fmaxf(p - q, 0.0f);
@@ -417,6 +440,14 @@ DEV float jsd_elem(float a, float b, const JsdConst& k) {
   const float Q = __builtin_amdgcn_exp2f(lq);
   const float g = 1.0f - __builtin_amdgcn_logf(fmaxf(P + Q, 1e-37f));
   return __builtin_fmaf(P, lp + g, Q * (lq + g));
+}
+// KL term P log2(P/Q) of KL(softmax(a) || softmax(b)) (the gate of App. C),
+// 0 where P = 0.
+DEV float kl_elem(float a, float b, const JsdConst& k) {
+  const float lp = (fmaxf(__builtin_fmaf(a, kL2E, -k.Ra), kFloorM) - k.kahi) - k.kalo;
+  const float lq = (fmaxf(__builtin_fmaf(b, kL2E, -k.Rb), kFloorM) - k.kbhi) - k.kblo;
+  const float P = __builtin_amdgcn_exp2f(lp);
+  return P > 0.0f ? P * (lp - lq) : 0.0f;
 }
 
 // log2 of a positive double to ~1e-7 absolute: exact exponent split plus the

@@ -57,7 +57,7 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const f
   double L2[kSlots];
   #pragma unroll
   for (int s = 0; s < kSlots; ++s) L2[s] = (double)R[s] + log2_dbl(Sp[s]);
-  const bool cda = A.gate_mode == ASYMSPEC_GATE_CDA;
+  const int gm = A.gate_mode;
   #pragma unroll
   for (int i = 0; i < kDecRow; ++i) v[i] = 0u;
   int decided = 1, accept = 0;
@@ -72,7 +72,17 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const f
     v[D_KALO] = __float_as_uint((float)(ka - (double)kahi));
     v[D_KBHI] = __float_as_uint(kbhi);
     v[D_KBLO] = __float_as_uint((float)(kb - (double)kbhi));
-    const float fd = fuse_masked(gq.t, gq.a, gq.b, A.beta);
+    const float fd = fuse_masked(gq.t, gq.a, gq.b, A.beta, A.delta_mode);
+    // lambda gate (App. B): D = lambda * Delta(d), Delta the drafter views'
+    // log-probability difference at the draft token; decided here
+    double Dl = 0.0;
+    if (gm == ASYMSPEC_GATE_LAMBDA) {
+      const double lpa = ((double)gq.a * (double)kL2E - L2[sA]) * kLn2;
+      const double lpb1 = ((double)gq.b * (double)kL2E - L2[sB]) * kLn2;
+      Dl = (double)A.lam * (lpa - lpb1);
+      v[D_GD_LO] = dlo(Dl);
+      v[D_GD_HI] = dhi(Dl);
+    }
     if (!samp) {
       // Eq. 4 in log form: ln p_t(d) - ln p_b(d) - ln gamma + D > 0
       const double lpt = ((double)gq.t * (double)kL2E - L2[sT]) * kLn2;
@@ -83,9 +93,12 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const f
       v[D_LPD] = __float_as_uint((float)lpd);
       v[D_LPEMIT] = __float_as_uint((float)(((double)M[sF] * (double)kL2E - L2[sF]) * kLn2));
       v[D_ARG] = (uint32_t)arg;
-      if (!cda || !neq) accept = m0 > 0.0;
+      // D >= 0 for the divergence gates (and D = 0 when a == b bitwise),
+      // D <= ln 2 for the JSD; outside those bounds the row stays open
+      if (gm == ASYMSPEC_GATE_LAMBDA) accept = m0 + Dl > 0.0;
+      else if (gm == ASYMSPEC_GATE_FIXED || !neq) accept = m0 > 0.0;
       else if (m0 > 0.0) accept = 1;
-      else if (m0 + kLn2 <= 0.0) accept = 0;
+      else if (gm == ASYMSPEC_GATE_CDA && m0 + kLn2 <= 0.0) accept = 0;
       else { decided = 0; thr = -m0; }
     } else {
       // accept iff u < min(1, p~(d) / (gamma_eff q(d))), i.e. ln u < x + D
@@ -103,10 +116,20 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const f
       else if (lq == -INFINITY) x = INFINITY;
       else x = lpd - lq - A.ln_gamma;
       const double lnu = gq.u > 0.0f ? ln_f(gq.u) : -INFINITY;
-      if (!cda || !neq) accept = lnu < x;
-      else if (lnu < x) accept = 1;
-      else if (lnu >= x + kLn2) accept = 0;
-      else { decided = 0; thr = lnu - x; }
+      if (gm == ASYMSPEC_GATE_LAMBDA) {
+        if (lpd == -INFINITY) accept = 0;          // p~(d) = 0 rejects
+        else if (lq == -INFINITY) accept = 1;      // q(d) = 0 accepts
+        else accept = lnu < x + Dl;
+      } else if (gm == ASYMSPEC_GATE_FIXED || !neq) {
+        accept = lnu < x;
+      } else if (lnu < x) {
+        accept = 1;
+      } else if (gm == ASYMSPEC_GATE_CDA && lnu >= x + kLn2) {
+        accept = 0;
+      } else {
+        decided = 0;
+        thr = lnu - x;
+      }
       v[D_RF] = __float_as_uint(R[sF]);
       v[D_ISF] = __float_as_uint((float)(1.0 / Sp[sF]));
       v[D_RQ] = __float_as_uint(Rq);
@@ -239,7 +262,10 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
     const int jstar = jr == 0x7FFFFFFF ? K : jr;
     const bool open = is_draft && lane < jstar && !decided;
     uint32_t task = 0;
-    if (is_draft && (open || (A.want_gate && neq))) task |= kTaskJsd;
+    // pass 2 computes D (JSD, or KL for that gate) for the open rows and,
+    // when the gate output is wanted, for every row whose views differ; the
+    // lambda gate's D is known here
+    if (is_draft && A.gate_mode != ASYMSPEC_GATE_LAMBDA && (open || (A.want_gate && neq))) task |= kTaskJsd;
     if (samp && is_draft && (open || lane == jstar)) task |= kTaskRes;
     if (samp && lane == K && jstar == K) task |= kTaskBonus;
     const unsigned long long tmask = __ballot(task != 0);
@@ -265,9 +291,9 @@ DEV void write_outputs(const KArgs& A, int req, int j, int next, float lp_next, 
   if (lane < K) {
     A.flp_out[(size_t)req * (K + 1) + lane] = lpd_lane;
     if (A.gate_out != nullptr) {
-      const bool cda = A.gate_mode == ASYMSPEC_GATE_CDA;
-      const float ge = cda ? A.gamma * __builtin_amdgcn_exp2f((float)(-d_lane * 1.4426950408889634))
-                           : A.gamma;
+      // gamma_eff = gamma (fixed gate) or gamma exp(-D) (Eq. 3 and the
+      // KL and lambda variants)
+      const float ge = A.gate_mode == ASYMSPEC_GATE_FIXED ? A.gamma : (float)((double)A.gamma * exp(-d_lane));
       A.gate_out[((size_t)req * K + lane) * 2 + 0] = (float)d_lane;
       A.gate_out[((size_t)req * K + lane) * 2 + 1] = ge;
     }
@@ -307,7 +333,12 @@ DEV void decide_item(const KArgs& A, int req, Smem& sm) {
       const int next = (int)sm.rows[jstar][D_ARG];
       const float lpn = __uint_as_float(sm.rows[jstar][D_LPEMIT]);
       const float lpd = lane < K ? __uint_as_float(sm.rows[lane][D_LPD]) : 0.0f;
-      write_outputs(A, req, jstar, next, lpn, lpd, 0.0);
+      // D of the rows: 0 (no view difference, or no D wanted) or the
+      // lambda gate's, known here
+      const double dl = (lane < K && A.gate_mode == ASYMSPEC_GATE_LAMBDA)
+                            ? u2d(sm.rows[lane][D_GD_LO], sm.rows[lane][D_GD_HI])
+                            : 0.0;
+      write_outputs(A, req, jstar, next, lpn, lpd, dl);
     }
   }
 }
@@ -366,7 +397,8 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
 // Pass-2 sums of one thread over its kSegPerLane vectors of a chunk.
 // kMode 0: interior chunk (no masking); 1: masked, branch-free; 2: generic
 // (one vector at a time, array-end repair).
-template <int DT, int kMode>
+// kKL: the divergence term is KL's (the KL gate) rather than the JSD's.
+template <int DT, int kMode, int DM, bool kKL>
 DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bool dr, bool db,
                     const ResidConst& rk, const JsdConst& jk, float& accj, float& seg) {
   constexpr int VE = Elem<DT>::VE;
@@ -404,8 +436,8 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bo
       for (int e = 0; e < VE; ++e) {
         const float xa = Elem<DT>::get(va[k], e), xb = Elem<DT>::get(vb[k], e);
         const float xt = Elem<DT>::get(vt[k], e);
-        vj[e] = dj ? jsd_elem(xa, xb, jk) : 0.0f;
-        vr[e] = dr ? resid_elem(xt, xa, xb, rk) : (db ? bonus_elem(xt, rk.c, rk.Rf) : 0.0f);
+        vj[e] = dj ? (kKL ? kl_elem(xa, xb, jk) : jsd_elem(xa, xb, jk)) : 0.0f;
+        vr[e] = dr ? resid_elem<DM>(xt, xa, xb, rk) : (db ? bonus_elem(xt, rk.c, rk.Rf) : 0.0f);
       }
       #pragma unroll
       for (int st = 1; st < VE; st <<= 1)
@@ -417,7 +449,20 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bo
   }
 }
 
-template <int DT>
+template <int DT, int DM, bool kKL>
+DEV void pass2_sums_any(const KArgs& A, const RowGeo& g, long long rel0, long long c0, long long c1,
+                        bool dj, bool dr, bool db, const ResidConst& rk, const JsdConst& jk, float& accj,
+                        float& seg) {
+  constexpr int VE = Elem<DT>::VE;
+  if (has_tail(A, c0, c1))
+    pass2_sums<DT, 2, DM, kKL>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+  else if (c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
+    pass2_sums<DT, 0, DM, kKL>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+  else
+    pass2_sums<DT, 1, DM, kKL>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+}
+
+template <int DT, int DM>
 DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
   const int lane = lane_id(), w = wave_id();
@@ -436,12 +481,11 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
     const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
     float accj = 0.0f, seg = 0.0f;
     if (task != 0) {
-      if (has_tail(A, c0, c1))
-        pass2_sums<DT, 2>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
-      else if (c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
-        pass2_sums<DT, 0>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+      // JSD rows of the KL gate take the KL term (a rare, separate instance)
+      if (dj && A.gate_mode == ASYMSPEC_GATE_KL)
+        pass2_sums_any<DT, DM, true>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
       else
-        pass2_sums<DT, 1>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+        pass2_sums_any<DT, DM, false>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
     }
     const float wj = wave_sum(accj);
     const float wseg = wave_sum(seg);
@@ -469,7 +513,7 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
 // carries weight; otherwise the element's index, and, when the scan itself
 // found it, sm.flags[2] = 1 and its logit (f for drafts, t for the bonus
 // row) in sm.dd[3].  Whole workgroup.
-template <int DT>
+template <int DT, int DM>
 DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
   constexpr int kPer = kSegVec / kThreads;   // vectors per thread in a segment
@@ -585,7 +629,7 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
     for (int e = 0; e < VE; ++e) {
       const float xt = Elem<DT>::get(vt[k], e);
       const float x = bonus ? bonus_elem(xt, rk.c, rk.Rf)
-                            : resid_elem(xt, Elem<DT>::get(va[k], e), Elem<DT>::get(vb[k], e), rk);
+                            : resid_elem<DM>(xt, Elem<DT>::get(va[k], e), Elem<DT>::get(vb[k], e), rk);
       tsum += (double)x;
       if (x > 0.0f) last_pos = (int)((vi * VE + e) - g.e0);
     }
@@ -601,11 +645,11 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
     for (int e = 0; e < VE; ++e) {
       const float xt = Elem<DT>::get(vt[k], e);
       const float xa = Elem<DT>::get(va[k], e), xb = Elem<DT>::get(vb[k], e);
-      const float x = bonus ? bonus_elem(xt, rk.c, rk.Rf) : resid_elem(xt, xa, xb, rk);
+      const float x = bonus ? bonus_elem(xt, rk.c, rk.Rf) : resid_elem<DM>(xt, xa, xb, rk);
       run += (double)x;
       if (x > 0.0f && run > target && first_ok == 0x7FFFFFFF) {
         first_ok = (int)((g.vbeg + rel + k) * VE + e - g.e0);
-        fx = bonus ? xt : fuse_masked(xt, xa, xb, A.beta);
+        fx = bonus ? xt : fuse_masked(xt, xa, xb, A.beta, A.delta_mode);
       }
     }
   int pick = block_min_i(first_ok, sm);
@@ -631,8 +675,8 @@ DEV int row_argmax_f(const KArgs& A, const RowGeo& g, Smem& sm) {
   int bi = 0x7FFFFFFF;
   for (int x = wave_id() * 64 + lane_id(); x < A.V; x += kThreads) {
     const long long idx = g.e0 + x;
-    const float f = fuse(Elem<DT>::load_one(A.t, idx), Elem<DT>::load_one(A.a, idx),
-                         Elem<DT>::load_one(A.b, idx), A.beta);
+    const float f = fuse_rt(Elem<DT>::load_one(A.t, idx), Elem<DT>::load_one(A.a, idx),
+                            Elem<DT>::load_one(A.b, idx), A.beta, A.delta_mode);
     if (f > best) { best = f; bi = x; }
   }
   const float M = wave_max(best);
@@ -645,7 +689,7 @@ DEV int row_argmax_f(const KArgs& A, const RowGeo& g, Smem& sm) {
   return block_min_i(best == Mb ? bi : 0x7FFFFFFF, sm);
 }
 
-template <int DT>
+template <int DT, int DM>
 DEV void pick_item(const KArgs& A, int req, Smem& sm) {
   const int lane = lane_id(), w = wave_id();
   const int K = A.K;
@@ -676,9 +720,17 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
       double part = 0.0;
       for (int c = lane; c < A.S; c += 64) part += wait_pair(p2_rec(A, req, i, c) + P2_J, A);
       part = wave_sum_d(part);
-      const double D = 0.5 * kLn2 * part;   // the partials are in log2 units
-      if (lane == i) Dl = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
+      // the partials are in log2 units; JSD = half their sum, within
+      // [0, ln 2]; KL = their sum, >= 0
+      if (A.gate_mode == ASYMSPEC_GATE_KL) {
+        const double D = kLn2 * part;
+        if (lane == i) Dl = D < 0.0 ? 0.0 : D;
+      } else {
+        const double D = 0.5 * kLn2 * part;
+        if (lane == i) Dl = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
+      }
     }
+    if (A.gate_mode == ASYMSPEC_GATE_LAMBDA && lane < K) Dl = u2d(sm.rows[lane][D_GD_LO], sm.rows[lane][D_GD_HI]);
     const bool decided = st & kStDecided;
     const bool acc = decided ? (st & kStAccept) != 0 : (Dl > thr);
     const int jr = wave_min_i(is_draft && !acc ? lane : 0x7FFFFFFF);
@@ -694,7 +746,7 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
   if (samp) {
     const bool bonus = j == K;
     const double u = (double)uK;
-    int pick = cdf_pick<DT>(A, req, j, u, bonus, sm);
+    int pick = cdf_pick<DT, DM>(A, req, j, u, bonus, sm);
     const RowGeo g = row_span<DT>(A, req * (K + 1) + j);
     const bool have_x = pick >= 0 && sm.flags[2] != 0;
     if (pick < 0) pick = row_argmax_f<DT>(A, g, sm);
@@ -705,7 +757,7 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
     } else {
       const long long idx = g.e0 + next;
       x = Elem<DT>::load_one(A.t, idx);
-      if (!bonus) x = fuse_masked(x, Elem<DT>::load_one(A.a, idx), Elem<DT>::load_one(A.b, idx), A.beta);
+      if (!bonus) x = fuse_masked(x, Elem<DT>::load_one(A.a, idx), Elem<DT>::load_one(A.b, idx), A.beta, A.delta_mode);
     }
     const double c = (double)__uint_as_float(sm.rows[j][D_C]);
     const double l2 = u2d(sm.rows[j][D_L2E_LO], sm.rows[j][D_L2E_HI]);

@@ -69,7 +69,7 @@ struct StatsAcc {
 };
 
 // Wave partials, cross-wave combine and the tagged chunk record.
-template <int DT, int KIND>
+template <int DT, int KIND, int DM>
 DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, const StatsAcc& q,
                        Smem& sm) {
   using TR = KindTraits<KIND>;
@@ -117,7 +117,7 @@ DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, c
         #pragma unroll
         for (int e = VE - 1; e >= 0; --e) {
           const float xt = Elem<DT>::get(vt, e);
-          const float x = kDraft ? fuse(xt, Elem<DT>::get(va, e), Elem<DT>::get(vb, e), A.beta) : xt;
+          const float x = kDraft ? fuse<DM>(xt, Elem<DT>::get(va, e), Elem<DT>::get(vb, e), A.beta) : xt;
           ei = (x == mw) ? e : ei;
         }
         if (ei < VE) cand = (int)(vi * VE + ei - g.e0);
@@ -166,7 +166,7 @@ DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, c
 DEV void pin(Acc& q) { asm volatile("" : "+v"(q.m), "+v"(q.R), "+v"(q.s)); }
 
 // One vector of each stream into the accumulators.
-template <int DT, int KIND, bool kB1, bool kClamp>
+template <int DT, int KIND, bool kB1, int DM, bool kClamp>
 DEV void stats_vec(const KArgs& A, float c, const u4& vt, const u4& va, const u4& vb, int kk, StatsAcc& q) {
   using TR = KindTraits<KIND>;
   constexpr int VE = Elem<DT>::VE;
@@ -179,7 +179,7 @@ DEV void stats_vec(const KArgs& A, float c, const u4& vt, const u4& va, const u4
     for (int e = 0; e < VE; ++e) {
       xa[e] = Elem<DT>::get(va, e);
       xb[e] = Elem<DT>::get(vb, e);
-      xf[e] = kB1 ? fuse1(xt[e], xa[e], xb[e]) : fuse(xt[e], xa[e], xb[e], A.beta);
+      xf[e] = kB1 ? fuse1<DM>(xt[e], xa[e], xb[e]) : fuse<DM>(xt[e], xa[e], xb[e], A.beta);
     }
     // the compare is folded into a wave mask at once and pinned there: left
     // to itself the compiler re-materialises it at its only use, keeping
@@ -212,7 +212,7 @@ DEV void stats_init(StatsAcc& q, float c) {
 // Generic path: one vector at a time, every vector repaired (row boundary,
 // array end), NaN-safe exponent for f.  Used for the chunk that holds a
 // ragged array end and to redo a chunk whose f sum came out NaN.
-template <int DT, int KIND, bool kB1>
+template <int DT, int KIND, bool kB1, int DM>
 DEV void stats_slow(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   using TR = KindTraits<KIND>;
   constexpr bool kDraft = TR::NS == 3;
@@ -236,15 +236,15 @@ DEV void stats_slow(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
       fix_vec<DT>(A, g, A.a, vi, va);
       fix_vec<DT>(A, g, A.b, vi, vb);
     }
-    stats_vec<DT, KIND, kB1, true>(A, g.c, vt, va, vb, kk, q);
+    stats_vec<DT, KIND, kB1, DM, true>(A, g.c, vt, va, vb, kk, q);
   }
-  publish_stats<DT, KIND>(A, g, m, rel0, q, sm);
+  publish_stats<DT, KIND, DM>(A, g, m, rel0, q, sm);
 }
 
 // Fast path; kMask for the first and last chunk of a row (elements outside
 // the row are masked, without branches).  Returns false, without publishing,
 // when the chunk must be redone on the generic path.
-template <int DT, int KIND, bool kB1, bool kMask>
+template <int DT, int KIND, bool kB1, int DM, bool kMask>
 DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   using TR = KindTraits<KIND>;
   constexpr int VE = Elem<DT>::VE;
@@ -282,7 +282,7 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
     }
     // masked elements have a = b = -inf, so f is NaN there: the boundary
     // chunks clamp the exponent of f
-    stats_vec<DT, KIND, kB1, kMask>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl], buf[NS == 3 ? 2 : 0][sl], j, q);
+    stats_vec<DT, KIND, kB1, DM, kMask>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl], buf[NS == 3 ? 2 : 0][sl], j, q);
     if (j + kWin < kVecs) {
       #pragma unroll
       for (int s = 0; s < NS; ++s) buf[s][sl] = buf_load_nt(r[s], off0 + (uint32_t)(vec_rel(j + kWin) * 16));
@@ -295,11 +295,11 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   // chunk redone on the NaN-safe path.  The test is workgroup-wide, so every
   // thread takes the same path.
   if (kDraft && !kMask && __syncthreads_or(q.F.s != q.F.s)) return false;
-  publish_stats<DT, KIND>(A, g, m, rel0, q, sm);
+  publish_stats<DT, KIND, DM>(A, g, m, rel0, q, sm);
   return true;
 }
 
-template <int DT, int KIND, bool kB1>
+template <int DT, int KIND, bool kB1, int DM>
 DEV void stats_item(const KArgs& A, int row, int m, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
   const RowGeo g = row_geo<DT>(A, row);
@@ -308,10 +308,10 @@ DEV void stats_item(const KArgs& A, int row, int m, Smem& sm) {
   if (!has_tail(A, c0, c1)) {
     // a chunk whose vectors lie wholly inside the row needs no masking
     const bool interior = c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V;
-    done = interior ? stats_fast<DT, KIND, kB1, false>(A, g, m, sm)
-                    : stats_fast<DT, KIND, kB1, true>(A, g, m, sm);
+    done = interior ? stats_fast<DT, KIND, kB1, DM, false>(A, g, m, sm)
+                    : stats_fast<DT, KIND, kB1, DM, true>(A, g, m, sm);
   }
-  if (!done) stats_slow<DT, KIND, kB1>(A, g, m, sm);
+  if (!done) stats_slow<DT, KIND, kB1, DM>(A, g, m, sm);
 }
 
 }  // namespace asym

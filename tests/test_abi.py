@@ -56,12 +56,12 @@ def _call(**over):
     lib = asp.load_library()
     fake = 1 << 20          # 16-B and 256-B aligned fake device addresses
     kw = dict(t=fake, a=fake, b=fake, dtype=0, d=fake, dp=None, u=fake, tau=fake,
-              B=2, K=2, V=64, beta=1.0, gamma=0.5, mode=0, flags=0,
+              B=2, K=2, V=64, beta=1.0, gamma=0.5, mode=0, flags=0, delta=0, lam=0.1,
               acc=fake, nxt=fake, flp=fake, gate=None, ws=fake, wsb=None, stream=None)
     kw.update(over)
     if kw["wsb"] is None:
         kw["wsb"] = asp.workspace_size(max(kw["B"], 1), max(kw["K"], 0), max(kw["V"], 1), 0) or 1 << 20
-    p = asp._Params(kw["beta"], kw["gamma"], kw["mode"], kw["flags"])
+    p = asp._Params(kw["beta"], kw["gamma"], kw["mode"], kw["flags"], kw["delta"], kw["lam"])
     return lib.asymspec_fuse_verify(kw["t"], kw["a"], kw["b"], kw["dtype"], kw["d"], kw["dp"],
                                     kw["u"], kw["tau"], kw["B"], kw["K"], kw["V"], ctypes.byref(p),
                                     kw["acc"], kw["nxt"], kw["flp"], kw["gate"], kw["ws"], kw["wsb"],
@@ -85,7 +85,12 @@ def _call(**over):
     (dict(beta=float("inf")), asp.E_ARG),
     (dict(gamma=0.0), asp.E_ARG),
     (dict(gamma=1.5), asp.E_ARG),
-    (dict(mode=3), asp.E_ARG),
+    (dict(mode=4), asp.E_ARG),
+    (dict(mode=-1), asp.E_ARG),
+    (dict(delta=3), asp.E_ARG),
+    (dict(delta=-1), asp.E_ARG),
+    (dict(mode=3, lam=float("inf")), asp.E_ARG),
+    (dict(mode=3, lam=float("nan")), asp.E_ARG),
     (dict(flags=1), asp.E_ARG),
     (dict(t=(1 << 20) + 4), asp.E_ALIGN),
     (dict(b=(1 << 20) + 8), asp.E_ALIGN),

@@ -128,3 +128,47 @@ def test_workload_4_sampled(gpu):
     sample = list(range(0, 8)) + list(range(250, 254)) + list(range(504, 512))
     r = compare(x, g, requests=sample, label="workload 4 sampled")
     _note(r)
+
+
+# --------------------------------------------- gate and fusion variants --
+# App. B (fixed and tuned-lambda gates), App. C (KL gate), Sec. 5 ablation
+# (delta = a, delta = t - b), each against the oracle.
+VARIANTS = [(2, 0), (3, 0), (0, 1), (0, 2), (2, 2), (3, 1), (1, 2)]
+
+
+@pytest.mark.parametrize("gate,delta", VARIANTS)
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("tau", [0.0, 1.0, 0.7])
+def test_variants_small(gpu, gate, delta, dtype, tau):
+    x = synth.generate(B=6, K=3, V=5000, dtype=dtype, rho=("uniform", 0.0, 2.0), tau=tau,
+                       seed=100 + 10 * gate + delta)
+    for lam in ((0.1, -2.0) if gate == 3 else (0.1,)):
+        g = run_gpu(x, gate_mode=gate, delta_mode=delta, lam=lam)
+        _note(compare(x, g, gate_mode=gate, delta_mode=delta, lam=lam,
+                      label=f"variant gate={gate} delta={delta} lam={lam} {dtype} tau={tau}"))
+
+
+@pytest.mark.parametrize("gate,delta", VARIANTS)
+def test_variants_edges_and_masks(gpu, gate, delta):
+    for V, K in ((1, 1), (4097, 2), (8193, 4)):
+        x = synth.generate(B=4, K=K, V=V, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                           tau=("alternate", 0.0, 1.0), seed=V + K + gate)
+        g = run_gpu(x, gate_mode=gate, delta_mode=delta)
+        _note(compare(x, g, gate_mode=gate, delta_mode=delta, label=f"variant edge V={V} K={K} g={gate} d={delta}"))
+    x = synth.generate(B=4, K=3, V=3000, dtype="fp32", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=7 + gate)
+    # tokens every view masks, and tokens only the verifier masks (inputs
+    # with b = -inf under a finite a or t give f = +inf: outside the contract)
+    x.a[:, :, 10:20] = -np.inf
+    x.b[:, :, 10:20] = -np.inf
+    x.t[:, :, 10:25] = -np.inf
+    x.b[1] = x.a[1]                     # identical views: D = 0 exactly
+    g = run_gpu(x, gate_mode=gate, delta_mode=delta)
+    _note(compare(x, g, gate_mode=gate, delta_mode=delta, label=f"variant masks g={gate} d={delta}"))
+
+
+@pytest.mark.parametrize("gate,delta", [(2, 0), (3, 0), (0, 1), (0, 2)])
+def test_variants_workload_1(gpu, gate, delta):
+    x = synth.workload_inputs(1)
+    g = run_gpu(x, gate_mode=gate, delta_mode=delta)
+    _note(compare(x, g, gate_mode=gate, delta_mode=delta, label=f"variant workload 1 g={gate} d={delta}"))
