@@ -147,6 +147,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--gate", action="store_true", help="also return (D, gamma_eff) per row")
+    ap.add_argument("--gate-mode", choices=["cda", "fixed", "kl", "lambda"], default="cda",
+                    help="acceptance gate (cda: the paper's; the others are its baselines)")
+    ap.add_argument("--delta-mode", choices=["a-b", "a", "t-b"], default="a-b",
+                    help="source of delta in f = t + beta delta (a-b: the paper's)")
+    ap.add_argument("--lam", type=float, default=0.1, help="scale of the lambda gate")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-requests", type=int, default=128)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -200,12 +205,16 @@ def main():
     tau = dev_tensor(x.temperature)
     B, K, V = x.B, x.K, x.V
     ws = asp.Workspace(dev)
-    outs = asp.fuse_verify(*copies[0], d, q, u, tau, return_gate=args.gate, workspace=ws)
+    gm = {"cda": asp.GATE_CDA, "fixed": asp.GATE_FIXED, "kl": asp.GATE_KL,
+          "lambda": asp.GATE_LAMBDA}[args.gate_mode]
+    dm = {"a-b": asp.DELTA_AB, "a": asp.DELTA_A, "t-b": asp.DELTA_TB}[args.delta_mode]
+    var = dict(gate_mode=gm, delta_mode=dm, lam=args.lam)
+    outs = asp.fuse_verify(*copies[0], d, q, u, tau, return_gate=args.gate, workspace=ws, **var)
     outs = tuple(o for o in outs)
 
     def step(i):
         return asp.fuse_verify(*copies[i % len(copies)], d, q, u, tau, return_gate=args.gate,
-                               workspace=ws, out=outs if args.gate else outs + (None,))
+                               workspace=ws, out=outs if args.gate else outs + (None,), **var)
 
     for i in range(args.warmup):
         step(i)
@@ -265,6 +274,7 @@ def main():
         "data": "synthetic (seeded generator; stands in for the paper's datasets)",
         "config": {"workload": wl.name, "B": B, "K": K, "V": V, "rows_per_step": rows,
                    "bytes_per_step": nbytes, "gate_output": bool(args.gate),
+                   "gate_mode": args.gate_mode, "delta_mode": args.delta_mode,
                    "input_copies": len(copies), "mean_accept_len": float(acc.mean()),
                    "parallelism": "single GPU"},
         "hbm_GBps": achieved,
