@@ -152,6 +152,8 @@ def main():
     ap.add_argument("--delta-mode", choices=["a-b", "a", "t-b"], default="a-b",
                     help="source of delta in f = t + beta delta (a-b: the paper's)")
     ap.add_argument("--lam", type=float, default=0.1, help="scale of the lambda gate")
+    ap.add_argument("--fuse-bonus", action="store_true",
+                    help="take the bonus token from the fused row f_K (reads rows K of a and b)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-requests", type=int, default=128)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -208,7 +210,7 @@ def main():
     gm = {"cda": asp.GATE_CDA, "fixed": asp.GATE_FIXED, "kl": asp.GATE_KL,
           "lambda": asp.GATE_LAMBDA}[args.gate_mode]
     dm = {"a-b": asp.DELTA_AB, "a": asp.DELTA_A, "t-b": asp.DELTA_TB}[args.delta_mode]
-    var = dict(gate_mode=gm, delta_mode=dm, lam=args.lam)
+    var = dict(gate_mode=gm, delta_mode=dm, lam=args.lam, fuse_bonus=args.fuse_bonus)
     outs = asp.fuse_verify(*copies[0], d, q, u, tau, return_gate=args.gate, workspace=ws, **var)
     outs = tuple(o for o in outs)
 
@@ -237,7 +239,7 @@ def main():
     ms_step = total_ms / args.steps
     kern_ms = float(np.mean(per))
     rows = B * (K + 1)
-    nbytes = x.nbytes_read()
+    nbytes = x.nbytes_read(args.fuse_bonus)
     achieved = nbytes / (kern_ms * 1e-3) / 1e9
 
     if args.calibrate_copy:
@@ -251,7 +253,9 @@ def main():
     acc = outs[0].cpu().numpy()
     traffic = None
     tpath = os.path.join(ROOT, "profiles", f"traffic_{wl.name}.json")
-    if os.path.exists(tpath):
+    default_variant = (args.gate_mode == "cda" and args.delta_mode == "a-b" and not args.gate
+                       and not args.fuse_bonus)
+    if default_variant and os.path.exists(tpath):
         try:
             tj = json.load(open(tpath))
             if tj.get("source_digest") == lib_digest():
@@ -275,6 +279,7 @@ def main():
         "config": {"workload": wl.name, "B": B, "K": K, "V": V, "rows_per_step": rows,
                    "bytes_per_step": nbytes, "gate_output": bool(args.gate),
                    "gate_mode": args.gate_mode, "delta_mode": args.delta_mode,
+                   "fuse_bonus": bool(args.fuse_bonus),
                    "input_copies": len(copies), "mean_accept_len": float(acc.mean()),
                    "parallelism": "single GPU"},
         "hbm_GBps": achieved,

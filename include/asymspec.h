@@ -15,6 +15,7 @@
  *   accept d_i iff softmax(t_i)[d_i] > gamma_eff * softmax(b_i)[d_i]  (Eq. 4)
  *   first rejection at j: emit argmax f_j; all accepted: emit argmax t_K
  *                                                           (Alg. 1)
+ *   (argmax f_K instead with the ASYMSPEC_FUSE_BONUS flag)
  *
  * The paper defines the step for greedy decoding (temperature 0).  For a
  * request with temperature tau > 0 the library uses the speculative-sampling
@@ -35,8 +36,8 @@
  *   - Errors are returned as negative status codes; argument checks happen on
  *     the host before anything is enqueued.  No exception crosses the ABI.
  *   - Layout: contiguous row-major; logits are [B][K+1][V] with row stride V;
- *     any V >= 1.  Row K of a and b is never read (the bonus token of Alg. 1
- *     uses the verifier alone).
+ *     any V >= 1.  Row K of a and b is read only with ASYMSPEC_FUSE_BONUS (the
+ *     bonus token of Alg. 1 uses the verifier alone).
  *   - Masked tokens: -inf logits are allowed.  A token whose fused logit is
  *     not a number (a = b = -inf) counts as masked.  NaN inputs otherwise give
  *     unspecified outputs.  Every row that is read must hold a finite logit.
@@ -79,11 +80,20 @@ extern "C" {
 #define ASYMSPEC_DELTA_A  1       /* delta = a, raw-augmented (Sec. 5 ablation)       */
 #define ASYMSPEC_DELTA_TB 2       /* delta = t - b, SCD-style (Sec. 5 ablation)       */
 
+/* ---- flags ------------------------------------------------------------- */
+#define ASYMSPEC_FUSE_BONUS 1u    /* the bonus token comes from the fused row
+                                     f_K = t_K + beta delta_K (greedy argmax, or a
+                                     draw from softmax(f_K/tau)) instead of t_K.
+                                     Alg. 1 appends argmax t_{K+1}, but the drafter
+                                     logits of position K+1 exist (Alg. 1 computes
+                                     a and b over all K+1 positions); this reads
+                                     rows K of a and b as well */
+
 typedef struct asymspec_params {
   float beta;         /* fusion weight of Eq. 2; finite, >= 0 (paper default 1.0) */
   float gamma;        /* base threshold of Eq. 3-4; in (0, 1] (paper default 0.5)  */
   int32_t gate_mode;  /* ASYMSPEC_GATE_*                                           */
-  uint32_t flags;     /* reserved, must be 0                                       */
+  uint32_t flags;     /* 0 or ASYMSPEC_FUSE_BONUS; other bits must be 0             */
   int32_t delta_mode; /* ASYMSPEC_DELTA_* (ASYMSPEC_DELTA_AB for the paper)        */
   float lambda;       /* scale of ASYMSPEC_GATE_LAMBDA, finite (paper default 0.1);
                          ignored by the other gates                                */
@@ -106,8 +116,10 @@ int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stre
  * forwards) for B independent requests with K drafts each.
  *
  *   verifier_logits     t [B][K+1][V]  (dtype)          16-byte aligned
- *   drafter_full_logits a [B][K+1][V]  (dtype)          16-byte aligned; rows 0..K-1 read
- *   drafter_comp_logits b [B][K+1][V]  (dtype)          16-byte aligned; rows 0..K-1 read
+ *   drafter_full_logits a [B][K+1][V]  (dtype)          16-byte aligned; rows 0..K-1 read,
+ *                                                       row K too with ASYMSPEC_FUSE_BONUS
+ *   drafter_comp_logits b [B][K+1][V]  (dtype)          same as a
+ *                       (a and b may be NULL when K = 0 without ASYMSPEC_FUSE_BONUS)
  *   draft_tokens        d [B][K] int32, each in [0, V)  (may be NULL when K = 0)
  *   draft_probs         q(d) [B][K] float, or NULL: the proposal probability of
  *                       each draft for sampling rows; NULL means softmax(a/tau)[d]
@@ -128,7 +140,7 @@ int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stre
  *                       greedy requests, tau for sampling ones); [K] = the
  *                       log-probability of next_token under the distribution
  *                       that emitted it (the fused row at the first rejection,
- *                       or the verifier's bonus row)
+ *                       or the bonus row: t_K, or f_K with ASYMSPEC_FUSE_BONUS)
  *   gate_out            [B][K][2] float out (D_i, gamma_eff_i), or NULL; D_i
  *                       is the JSD (CDA and fixed gates), the KL (KL gate) or
  *                       lambda * Delta_i(d_i) (lambda gate), and gamma_eff_i =

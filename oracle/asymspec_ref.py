@@ -56,6 +56,11 @@ Variants the paper compares against (Sec. 5 mechanism ablation; App. B
                Delta as a vector; the gate needs its value at d_i);
 * delta A      raw-augmented fusion, delta_i = a_i          (f = t + beta a);
 * delta TB     SCD-style fusion, delta_i = t_i - b_i        (f = t + beta (t - b)).
+
+``fuse_bonus`` fuses the bonus row too: Alg. 1 appends argmax(t_{K+1}), yet
+the drafter logits of position K+1 are computed as well; with the flag the
+bonus is taken from f_K = t_K + beta delta_K (greedy argmax, or a draw from
+softmax(f_K / tau)) and rows K of a and b are read.
 """
 
 from __future__ import annotations
@@ -271,7 +276,7 @@ def verify_request(t: np.ndarray, a: np.ndarray, b: np.ndarray,
                    uniforms: np.ndarray, temperature: float,
                    beta: float = 1.0, gamma: float = 0.5,
                    gate_mode: int = GATE_CDA, delta_mode: int = DELTA_AB,
-                   lam: float = 0.1) -> RequestResult:
+                   lam: float = 0.1, fuse_bonus: bool = False) -> RequestResult:
     """One request of Alg. 1's decision step.
 
     t, a, b: stored logits [K+1][V] (uint16 bf16 bits or fp32).  Row K is the
@@ -362,9 +367,10 @@ def verify_request(t: np.ndarray, a: np.ndarray, b: np.ndarray,
                 kind = "residual-empty"
             flp[K] = float(lpf[nxt])
     else:
-        tK = t32[K]
+        # Alg. 1 bonus: the verifier's last row, or its fused form
+        tK = fused_logits_f32(t32[K], a32[K], b32[K], beta, delta_mode) if fuse_bonus else t32[K]
         if greedy:
-            nxt = argmax_first(tK)                               # Alg. 1 bonus
+            nxt = argmax_first(tK)
             flp[K] = float(log_softmax(tK)[nxt])
             kind = "bonus-argmax"
         else:
@@ -381,7 +387,7 @@ def verify_request(t: np.ndarray, a: np.ndarray, b: np.ndarray,
 def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
                 beta: float = 1.0, gamma: float = 0.5,
                 gate_mode: int = GATE_CDA, requests=None,
-                delta_mode: int = DELTA_AB, lam: float = 0.1):
+                delta_mode: int = DELTA_AB, lam: float = 0.1, fuse_bonus: bool = False):
     """Batch form over requests: t, a, b [B][K+1][V]; draft_tokens [B][K];
     draft_probs [B][K] or None; uniforms [B][K+1]; temperature [B].
     ``requests`` restricts the work to a subset of request indices.
@@ -401,7 +407,7 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
                            None if draft_probs is None else draft_probs[bi],
                            uniforms[bi], float(temperature[bi]),
                            beta=beta, gamma=gamma, gate_mode=gate_mode,
-                           delta_mode=delta_mode, lam=lam)
+                           delta_mode=delta_mode, lam=lam, fuse_bonus=fuse_bonus)
         acc[k] = r.accept_len
         nxt[k] = r.next_token
         flp[k] = r.fused_logprobs

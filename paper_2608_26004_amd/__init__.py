@@ -13,7 +13,7 @@ import os
 
 __all__ = ["fuse_verify", "workspace_size", "Workspace", "load_library", "status_string",
            "BF16", "FP32", "GATE_CDA", "GATE_FIXED", "GATE_KL", "GATE_LAMBDA",
-           "DELTA_AB", "DELTA_A", "DELTA_TB", "AsymSpecError"]
+           "DELTA_AB", "DELTA_A", "DELTA_TB", "FUSE_BONUS", "AsymSpecError"]
 
 BF16 = 0
 FP32 = 1
@@ -24,6 +24,7 @@ GATE_LAMBDA = 3
 DELTA_AB = 0
 DELTA_A = 1
 DELTA_TB = 2
+FUSE_BONUS = 1
 
 OK = 0
 E_ARG = -1
@@ -113,14 +114,15 @@ _default_ws = {}
 def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
                 beta: float = 1.0, gamma: float = 0.5, gate_mode: int = GATE_CDA,
                 return_gate: bool = False, workspace: Workspace | None = None, out=None,
-                delta_mode: int = DELTA_AB, lam: float = 0.1):
+                delta_mode: int = DELTA_AB, lam: float = 0.1, fuse_bonus: bool = False):
     """One AsymSpec decision step on the current HIP stream.
 
     t, a, b: [B, K+1, V] torch.bfloat16 or torch.float32 on the GPU
     draft_tokens: [B, K] int32; draft_probs: [B, K] float32 or None;
     uniforms: [B, K+1] float32; temperature: [B] float32 (<= 0: greedy).
     gate_mode: GATE_CDA (the paper), GATE_FIXED, GATE_KL or GATE_LAMBDA (with
-    scale lam); delta_mode: DELTA_AB (the paper), DELTA_A or DELTA_TB.
+    scale lam); delta_mode: DELTA_AB (the paper), DELTA_A or DELTA_TB;
+    fuse_bonus: take the bonus token from f_K rather than t_K (FUSE_BONUS).
     Returns (accept_len [B] int32, next_token [B] int32,
              fused_logprobs [B, K+1] float32[, gate [B, K, 2] float32])."""
     import torch
@@ -163,7 +165,8 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     if workspace is None:
         workspace = _default_ws.setdefault(dev, Workspace(dev))
     wsbuf = workspace.get(ws_bytes, dev)
-    params = _Params(float(beta), float(gamma), int(gate_mode), 0, int(delta_mode), float(lam))
+    params = _Params(float(beta), float(gamma), int(gate_mode), FUSE_BONUS if fuse_bonus else 0,
+                     int(delta_mode), float(lam))
     st = lib.asymspec_fuse_verify(_ptr(t), _ptr(a), _ptr(b), dt, _ptr(draft_tokens),
                                   _ptr(draft_probs), _ptr(uniforms), _ptr(temperature),
                                   B, K, V, ctypes.byref(params), _ptr(acc), _ptr(nxt),

@@ -47,8 +47,14 @@ DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
   const int row = req * (A.K + 1) + i;
   const float tau = sload_f32(A.tau, req);
   if (i == A.K) {
-    if (tau > 0.0f) stats_item<DT, kSampleBonus, kB1, DM>(A, row, m, sm);
-    else stats_item<DT, kGreedyBonus, kB1, DM>(A, row, m, sm);
+    if (A.fuse_bonus) {
+      if (tau > 0.0f) stats_item<DT, kSampleBonusF, kB1, DM>(A, row, m, sm);
+      else stats_item<DT, kGreedyBonusF, kB1, DM>(A, row, m, sm);
+    } else if (tau > 0.0f) {
+      stats_item<DT, kSampleBonus, kB1, DM>(A, row, m, sm);
+    } else {
+      stats_item<DT, kGreedyBonus, kB1, DM>(A, row, m, sm);
+    }
   } else if (!(tau > 0.0f)) {
     stats_item<DT, kGreedyDraft, kB1, DM>(A, row, m, sm);
   } else if (tau == 1.0f) {
@@ -225,14 +231,16 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   if (t == nullptr || uniforms == nullptr || temperature == nullptr || accept_len == nullptr ||
       next_token == nullptr || fused_logprobs == nullptr || workspace == nullptr)
     return ASYMSPEC_E_ARG;
-  if (K > 0 && (a == nullptr || b == nullptr || draft_tokens == nullptr)) return ASYMSPEC_E_ARG;
+  const bool fb = (params->flags & ASYMSPEC_FUSE_BONUS) != 0u;
+  if (K > 0 && draft_tokens == nullptr) return ASYMSPEC_E_ARG;
+  if ((K > 0 || fb) && (a == nullptr || b == nullptr)) return ASYMSPEC_E_ARG;
   if (!std::isfinite(params->beta) || params->beta < 0.0f) return ASYMSPEC_E_ARG;
   if (!(params->gamma > 0.0f && params->gamma <= 1.0f)) return ASYMSPEC_E_ARG;
   if (params->gate_mode < ASYMSPEC_GATE_CDA || params->gate_mode > ASYMSPEC_GATE_LAMBDA) return ASYMSPEC_E_ARG;
   if (params->delta_mode < ASYMSPEC_DELTA_AB || params->delta_mode > ASYMSPEC_DELTA_TB) return ASYMSPEC_E_ARG;
   if (params->gate_mode == ASYMSPEC_GATE_LAMBDA && !std::isfinite(params->lambda)) return ASYMSPEC_E_ARG;
-  if (params->flags != 0u) return ASYMSPEC_E_ARG;
-  if (!aligned(t, 16) || (K > 0 && (!aligned(a, 16) || !aligned(b, 16)))) return ASYMSPEC_E_ALIGN;
+  if ((params->flags & ~(uint32_t)ASYMSPEC_FUSE_BONUS) != 0u) return ASYMSPEC_E_ARG;
+  if (!aligned(t, 16) || ((K > 0 || fb) && (!aligned(a, 16) || !aligned(b, 16)))) return ASYMSPEC_E_ALIGN;
   if (!aligned(uniforms, 4) || !aligned(temperature, 4) || !aligned(accept_len, 4) ||
       !aligned(next_token, 4) || !aligned(fused_logprobs, 4) ||
       (draft_tokens && !aligned(draft_tokens, 4)) || (draft_probs && !aligned(draft_probs, 4)) ||
@@ -245,7 +253,7 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
 
   KArgs A;
   std::memset(&A, 0, sizeof(A));
-  A.t = t; A.a = (K > 0) ? a : t; A.b = (K > 0) ? b : t;
+  A.t = t; A.a = (K > 0 || fb) ? a : t; A.b = (K > 0 || fb) ? b : t;
   A.d = (K > 0) ? draft_tokens : (const int32_t*)uniforms;
   A.dp = draft_probs; A.u = uniforms; A.tau = temperature;
   A.acc_out = accept_len; A.next_out = next_token; A.flp_out = fused_logprobs; A.gate_out = gate_out;
@@ -259,6 +267,7 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   A.beta = params->beta; A.gamma = params->gamma; A.gate_mode = params->gate_mode;
   A.want_gate = gate_out != nullptr;
   A.delta_mode = params->delta_mode;
+  A.fuse_bonus = fb ? 1 : 0;
   A.lam = params->gate_mode == ASYMSPEC_GATE_LAMBDA ? params->lambda : 0.0f;
   A.ln_gamma = std::log((double)params->gamma);
   A.epoch = next_epoch();

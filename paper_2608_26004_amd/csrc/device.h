@@ -45,8 +45,12 @@ typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 typedef const __attribute__((address_space(4))) uint32_t* cptr32;
 
 // Row kinds.  Every row of a request has the request's temperature; row K is
-// the bonus position.
-enum Kind { kGreedyDraft = 0, kSampleDraft1 = 1, kSampleDraftT = 2, kGreedyBonus = 3, kSampleBonus = 4 };
+// the bonus position, taken from t (Alg. 1) or, when the bonus row is fused,
+// from f = t + beta delta.
+enum Kind {
+  kGreedyDraft = 0, kSampleDraft1 = 1, kSampleDraftT = 2, kGreedyBonus = 3, kSampleBonus = 4,
+  kGreedyBonusF = 5, kSampleBonusF = 6
+};
 // Statistics slots: t, a and b at temperature 1 (greedy t, and the JSD of
 // Eq. 3 at temperature 1), f (fused logits, at the row's temperature), and a
 // at the row's temperature when that is not 1 (the proposal q).
@@ -100,6 +104,7 @@ struct KArgs {
   int B, K, V, S;
   float beta, gamma; int gate_mode; int want_gate;
   int delta_mode;     // source of delta in f = t + beta * delta
+  int fuse_bonus;     // the bonus row emits from f rather than t
   float lam;          // scale of the lambda gate
   double ln_gamma;
   uint32_t epoch;
@@ -500,7 +505,8 @@ DEV RowGeo row_geo(const KArgs& A, int row) {
   g.tau = sload_f32(A.tau, g.req);
   const bool samp = g.tau > 0.0f;
   const bool bonus = g.pos == A.K;
-  if (bonus) g.kind = samp ? kSampleBonus : kGreedyBonus;
+  if (bonus && A.fuse_bonus) g.kind = samp ? kSampleBonusF : kGreedyBonusF;
+  else if (bonus) g.kind = samp ? kSampleBonus : kGreedyBonus;
   else g.kind = samp ? (g.tau == 1.0f ? kSampleDraft1 : kSampleDraftT) : kGreedyDraft;
   g.c = samp ? (kL2E / g.tau) : kL2E;
   g.e0 = (long long)row * A.V;
@@ -509,7 +515,11 @@ DEV RowGeo row_geo(const KArgs& A, int row) {
   return g;
 }
 DEV bool kind_draft(int k) { return k == kGreedyDraft || k == kSampleDraft1 || k == kSampleDraftT; }
-DEV bool kind_samp(int k) { return k == kSampleDraft1 || k == kSampleDraftT || k == kSampleBonus; }
+DEV bool kind_samp(int k) {
+  return k == kSampleDraft1 || k == kSampleDraftT || k == kSampleBonus || k == kSampleBonusF;
+}
+// Rows whose statistics are those of the fused logits f (slot sF).
+DEV bool kind_fused(int k) { return kind_draft(k) || k == kGreedyBonusF || k == kSampleBonusF; }
 
 // Buffer resource over one stream's vectors of row g, clamped to the array
 // end: vectors past the row (or the array) read as zero.

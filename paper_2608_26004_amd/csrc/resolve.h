@@ -137,6 +137,18 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const f
       v[D_L2E_LO] = dlo(L2[sF]);
       v[D_L2E_HI] = dhi(L2[sF]);
     }
+  } else if (kind == kGreedyBonusF || kind == kSampleBonusF) {
+    // fused bonus row: greedy argmax of f, or a draw from softmax(f / tau),
+    // drawn through the residual weights with q = 0 (q's reference exponent
+    // +inf and scale 0 make its term vanish for every finite a)
+    v[D_RF] = __float_as_uint(R[sF]);
+    v[D_ISF] = __float_as_uint((float)(1.0 / Sp[sF]));
+    v[D_RQ] = __float_as_uint(INFINITY);
+    v[D_ISQ] = 0u;
+    v[D_L2E_LO] = dlo(L2[sF]);
+    v[D_L2E_HI] = dhi(L2[sF]);
+    v[D_ARG] = (uint32_t)arg;
+    v[D_LPEMIT] = __float_as_uint((float)(((double)M[sF] * (double)g.c - L2[sF]) * kLn2));
   } else {
     // bonus row (Alg. 1): greedy argmax of t, or a draw from softmax(t / tau)
     v[D_RF] = __float_as_uint(R[sT]);
@@ -182,6 +194,7 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
     if (have && ch == 0) gq = sgather<DT>(A, row_span<DT>(A, req * nrow + i));
     const RowGeo g = row_geo<DT>(A, req * nrow + i);
     const bool draft = kind_draft(g.kind);
+    const bool fused = kind_fused(g.kind);
     float cs[kSlots];
     cs[sT] = draft ? kL2E : g.c;
     cs[sA] = kL2E;
@@ -225,11 +238,11 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
     #pragma unroll
     for (int s = 0; s < kSlots; ++s) Rr[s] = M[s] * cs[s];
     if (have) {
-      const float Marg = draft ? M[sF] : M[sT];
+      const float Marg = fused ? M[sF] : M[sT];
       #pragma unroll
       for (int s = 0; s < kSlots; ++s)
         sm.dt[tid][s] = (double)payf(r[R1_S + s]) * exp2((double)(payf(r[R1_M + s]) * cs[s]) - (double)Rr[s]);
-      const float mine = draft ? payf(r[R1_M + sF]) : payf(r[R1_M + sT]);
+      const float mine = fused ? payf(r[R1_M + sF]) : payf(r[R1_M + sT]);
       sm.darg[tid] = mine == Marg ? (int)pay(r[R1_ARG]) : 0x7FFFFFFF;
       sm.dneq[tid] = (int)pay(r[R1_NEQ]);
     }
@@ -267,7 +280,8 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
     // lambda gate's D is known here
     if (is_draft && A.gate_mode != ASYMSPEC_GATE_LAMBDA && (open || (A.want_gate && neq))) task |= kTaskJsd;
     if (samp && is_draft && (open || lane == jstar)) task |= kTaskRes;
-    if (samp && lane == K && jstar == K) task |= kTaskBonus;
+    // the bonus draw: softmax(t / tau), or the fused row's p~ as a residual
+    if (samp && lane == K && jstar == K) task |= A.fuse_bonus ? kTaskRes : kTaskBonus;
     const unsigned long long tmask = __ballot(task != 0);
     const bool fin = !samp && !__any((task & kTaskJsd) != 0);
     if (row_ok) sm.rows[lane][D_TASK] = task;
@@ -464,7 +478,6 @@ DEV void pass2_sums_any(const KArgs& A, const RowGeo& g, long long rel0, long lo
 
 template <int DT, int DM>
 DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
-  constexpr int VE = Elem<DT>::VE;
   const int lane = lane_id(), w = wave_id();
   if (load_decision(A, req, sm) != kStatePending) return;
   unsigned long long tmask = (unsigned long long)sm.req[R_TASK_LO] | ((unsigned long long)sm.req[R_TASK_HI] << 32);
@@ -744,7 +757,7 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
   int next = sm.flags[1];
   float lpn = (float)sm.dd[0];
   if (samp) {
-    const bool bonus = j == K;
+    const bool bonus = j == K && !A.fuse_bonus;   // weights from t alone
     const double u = (double)uK;
     int pick = cdf_pick<DT, DM>(A, req, j, u, bonus, sm);
     const RowGeo g = row_span<DT>(A, req * (K + 1) + j);

@@ -43,6 +43,15 @@ template <> struct KindTraits<kSampleBonus> {
   static constexpr int NS = 1; static constexpr bool kArg = false; static constexpr int argslot = sT;
   static constexpr bool kT = true, kF = false, kA = false, kB = false, kAT = false;
 };
+// fused bonus row: f alone, from all three streams
+template <> struct KindTraits<kGreedyBonusF> {
+  static constexpr int NS = 3; static constexpr bool kArg = true; static constexpr int argslot = sF;
+  static constexpr bool kT = false, kF = true, kA = false, kB = false, kAT = false;
+};
+template <> struct KindTraits<kSampleBonusF> {
+  static constexpr int NS = 3; static constexpr bool kArg = false; static constexpr int argslot = sF;
+  static constexpr bool kT = false, kF = true, kA = false, kB = false, kAT = false;
+};
 
 // Offset, in vectors from the thread's first vector, of its j-th vector
 // (sub-tile j / kNV, step j % kNV).
@@ -190,13 +199,13 @@ DEV void stats_vec(const KArgs& A, float c, const u4& vt, const u4& va, const u4
     q.neq |= nm;
     if (TR::kT) acc_vec<VE, false, false>(q.T, xt, kL2E, kk);
     acc_vec<VE, kClamp, TR::kArg>(q.F, xf, c, kk);
-    acc_vec<VE, false, false>(q.A, xa, kL2E, kk);
-    acc_vec<VE, false, false>(q.B, xb, kL2E, kk);
+    if (TR::kA) acc_vec<VE, false, false>(q.A, xa, kL2E, kk);
+    if (TR::kB) acc_vec<VE, false, false>(q.B, xb, kL2E, kk);
     if (TR::kAT) acc_vec<VE, false, false>(q.AT, xa, c, kk);
     if (TR::kT) pin(q.T);
     pin(q.F);
-    pin(q.A);
-    pin(q.B);
+    if (TR::kA) pin(q.A);
+    if (TR::kB) pin(q.B);
     if (TR::kAT) pin(q.AT);
   } else {
     acc_vec<VE, false, TR::kArg>(q.T, xt, c, kk);

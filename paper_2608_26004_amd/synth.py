@@ -91,11 +91,12 @@ class Inputs:
     def V(self):
         return self.t.shape[2]
 
-    def nbytes_read(self) -> int:
+    def nbytes_read(self, fuse_bonus: bool = False) -> int:
         """Bytes the step reads from the logit streams: t rows 0..K, a and b
-        rows 0..K-1 (row K of a and b is not part of the step)."""
+        rows 0..K-1; row K of a and b only when the bonus row is fused."""
         elem = 2 if self.dtype == BF16 else 4
-        return self.B * (3 * self.K + 1) * self.V * elem
+        rows = 3 * (self.K + 1) if fuse_bonus else 3 * self.K + 1
+        return self.B * rows * self.V * elem
 
 
 def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:

@@ -29,7 +29,7 @@ def to_device(x, device="cuda"):
 
 
 def run_gpu(inp, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True, want_gate=True,
-            device="cuda", delta_mode=0, lam=0.1):
+            device="cuda", delta_mode=0, lam=0.1, fuse_bonus=False):
     import torch
     import paper_2608_26004_amd as asp
     t, a, b = (to_device(x, device) for x in (inp.t, inp.a, inp.b))
@@ -39,7 +39,7 @@ def run_gpu(inp, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True, want_gate=Tr
     tau = to_device(inp.temperature.astype(np.float32), device)
     out = asp.fuse_verify(t, a, b, d, q, u, tau, beta=beta, gamma=gamma,
                           gate_mode=gate_mode, return_gate=want_gate,
-                          delta_mode=delta_mode, lam=lam)
+                          delta_mode=delta_mode, lam=lam, fuse_bonus=fuse_bonus)
     torch.cuda.synchronize()
     res = [x.cpu().numpy() for x in out]
     if not want_gate:
@@ -48,7 +48,7 @@ def run_gpu(inp, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True, want_gate=Tr
 
 
 def compare(inp, gpu, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True,
-            requests=None, label="", delta_mode=0, lam=0.1):
+            requests=None, label="", delta_mode=0, lam=0.1, fuse_bonus=False):
     """Run the oracle on `requests` (all by default) and compare.  Returns a
     dict report; raises AssertionError on a parity failure."""
     acc_g, nxt_g, flp_g, gate_g = gpu
@@ -56,7 +56,7 @@ def compare(inp, gpu, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True,
     acc_o, nxt_o, flp_o, gate_o, res = O.fuse_verify(
         inp.t, inp.a, inp.b, inp.draft_tokens, inp.draft_probs if with_probs else None,
         inp.uniforms, inp.temperature, beta=beta, gamma=gamma, gate_mode=gate_mode,
-        requests=idx, delta_mode=delta_mode, lam=lam)
+        requests=idx, delta_mode=delta_mode, lam=lam, fuse_bonus=fuse_bonus)
     K = inp.K
     near, bad = [], []
     max_lp = 0.0

@@ -91,7 +91,11 @@ def _call(**over):
     (dict(delta=-1), asp.E_ARG),
     (dict(mode=3, lam=float("inf")), asp.E_ARG),
     (dict(mode=3, lam=float("nan")), asp.E_ARG),
-    (dict(flags=1), asp.E_ARG),
+    (dict(flags=2), asp.E_ARG),
+    (dict(flags=3), asp.E_ARG),
+    (dict(K=0, flags=1, a=None), asp.E_ARG),
+    (dict(K=0, flags=1, b=None), asp.E_ARG),
+    (dict(K=0, flags=1, a=(1 << 20) + 4), asp.E_ALIGN),
     (dict(t=(1 << 20) + 4), asp.E_ALIGN),
     (dict(b=(1 << 20) + 8), asp.E_ALIGN),
     (dict(flp=(1 << 20) + 2), asp.E_ALIGN),

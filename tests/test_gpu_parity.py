@@ -172,3 +172,69 @@ def test_variants_workload_1(gpu, gate, delta):
     x = synth.workload_inputs(1)
     g = run_gpu(x, gate_mode=gate, delta_mode=delta)
     _note(compare(x, g, gate_mode=gate, delta_mode=delta, label=f"variant workload 1 g={gate} d={delta}"))
+
+
+# ------------------------------------------------------ fused bonus row --
+def _reach_bonus(x, reqs):
+    """Requests `reqs` get identical views and verifier on their draft rows
+    (t = a = b), so Eq. 4 and its sampling form accept every draft (ratio
+    1 / gamma_eff >= 1; for sampling this needs delta = 0 there, i.e. not
+    delta = a) and the step ends at the bonus row; row K keeps its own a and
+    b.  Their draft probabilities are dropped (q computed from a)."""
+    K = x.K
+    for r in reqs:
+        x.a[r, :K] = x.t[r, :K]
+        x.b[r, :K] = x.t[r, :K]
+    return x
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("tau", [0.0, 1.0, 0.7])
+@pytest.mark.parametrize("gate,delta", [(0, 0), (2, 0), (3, 2), (1, 2), (1, 1)])
+def test_fuse_bonus_small(gpu, dtype, tau, gate, delta):
+    x = synth.generate(B=8, K=3, V=5000, dtype=dtype, rho=("uniform", 0.0, 2.0), tau=tau,
+                       seed=300 + 10 * gate + delta)
+    _reach_bonus(x, range(6))
+    g = run_gpu(x, gate_mode=gate, delta_mode=delta, with_probs=False, fuse_bonus=True)
+    r = compare(x, g, gate_mode=gate, delta_mode=delta, with_probs=False, fuse_bonus=True,
+                label=f"fuse_bonus {dtype} tau={tau} g={gate} d={delta}")
+    _note(r)
+    if delta != 1 or tau == 0.0:
+        assert (g[0][:6] == 3).all()
+    # the flag reaches the kernel: the unfused bonus differs on some request
+    g0 = run_gpu(x, gate_mode=gate, delta_mode=delta, with_probs=False)
+    _note(compare(x, g0, gate_mode=gate, delta_mode=delta, with_probs=False,
+                  label=f"unfused bonus {dtype} tau={tau} g={gate} d={delta}"))
+    bon = g[0][:6] == 3
+    if bon.any():
+        assert (g0[1][:6][bon] != g[1][:6][bon]).any() or (g0[2][:6, 3][bon] != g[2][:6, 3][bon]).any()
+
+
+@pytest.mark.parametrize("V,K", [(1, 0), (3, 0), (4097, 0), (4097, 2), (8193, 1)])
+def test_fuse_bonus_edges(gpu, V, K):
+    x = synth.generate(B=5, K=K, V=V, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=V + 7 * K)
+    _reach_bonus(x, range(4))
+    g = run_gpu(x, with_probs=False, fuse_bonus=True)
+    _note(compare(x, g, with_probs=False, fuse_bonus=True, label=f"fuse_bonus edge V={V} K={K}"))
+
+
+def test_fuse_bonus_masks(gpu):
+    x = synth.generate(B=6, K=2, V=3000, dtype="fp32", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=77)
+    _reach_bonus(x, range(6))
+    # tokens every view masks (f is NaN there: masked), tokens only the
+    # verifier masks, and a request whose bonus views agree (f_K = t_K)
+    x.a[:, :, 10:20] = -np.inf
+    x.b[:, :, 10:20] = -np.inf
+    x.t[:, :, 10:25] = -np.inf
+    x.b[2, 2] = x.a[2, 2]
+    g = run_gpu(x, with_probs=False, fuse_bonus=True)
+    _note(compare(x, g, with_probs=False, fuse_bonus=True, label="fuse_bonus masks"))
+
+
+def test_fuse_bonus_workload_1(gpu):
+    x = synth.workload_inputs(1)
+    _reach_bonus(x, range(0, x.B, 2))
+    g = run_gpu(x, with_probs=False, fuse_bonus=True)
+    _note(compare(x, g, with_probs=False, fuse_bonus=True, label="fuse_bonus workload 1"))

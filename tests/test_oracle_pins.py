@@ -465,3 +465,51 @@ def test_delta_modes_degenerate_cases():
     z = np.zeros_like(a)
     assert np.array_equal(O.fused_logits_f32(t, z, b, 1.0, O.DELTA_A).view(np.uint32), t.view(np.uint32))
     assert np.array_equal(O.fused_logits_f32(t, a, t, 1.0, O.DELTA_TB).view(np.uint32), t.view(np.uint32))
+
+
+# ------------------------------------------------------ fused bonus row --
+def _all_accepted(K, V, rng, tau):
+    """Rows where every draft is the verifier's own argmax and the drafter
+    views agree: Eq. 4 accepts each with margin, so the step reaches the
+    bonus row (Alg. 1)."""
+    t = rand_rows(V, K + 1, rng=rng)
+    a = t.copy()
+    b = t.copy()
+    d = np.array([int(np.argmax(t[i])) for i in range(K)], np.int32)
+    return t, a, b, d
+
+
+def test_fused_bonus_reduces_to_alg1_when_views_agree():
+    """Alg. 1 takes the bonus from t_{K+1}; with the flag it is taken from
+    f_K, which equals t_K bitwise when a_K == b_K (delta = a - b) or when
+    beta = 0, so the emitted token and its log-probability are unchanged."""
+    rng = np.random.default_rng(41)
+    for tau in (0.0, 1.0):
+        t, a, b, d = _all_accepted(3, 50, rng, tau)
+        u = np.full(4, 0.3, np.float32)
+        r0 = O.verify_request(t, a, b, d, None, u, tau)
+        assert r0.accept_len == 3
+        r1 = O.verify_request(t, a, b, d, None, u, tau, fuse_bonus=True)
+        assert (r1.accept_len, r1.next_token) == (r0.accept_len, r0.next_token)
+        assert r1.fused_logprobs[3] == r0.fused_logprobs[3]
+        b2 = b.copy(); b2[3] = rand_rows(50, 1, rng=rng)[0]
+        r2 = O.verify_request(t, a, b2, d, None, u, tau, beta=0.0, fuse_bonus=True)
+        r3 = O.verify_request(t, a, b2, d, None, u, tau, beta=0.0)
+        assert (r2.next_token, r2.fused_logprobs[3]) == (r3.next_token, r3.fused_logprobs[3])
+
+
+def test_fused_bonus_follows_the_fused_row():
+    """With the flag the greedy bonus is argmax of t_K + beta (a_K - b_K):
+    a bonus row where the fusion moves the argmax emits the fused one, with
+    log_softmax(f_K) at it (scipy)."""
+    rng = np.random.default_rng(42)
+    t, a, b, d = _all_accepted(2, 6, rng, 0.0)
+    t[2] = np.array([3.0, 2.5, 0.0, 0.0, 0.0, 0.0], np.float32)
+    a[2] = np.array([0.0, 2.0, 0.0, 0.0, 0.0, 0.0], np.float32)
+    b[2] = np.zeros(6, np.float32)
+    u = np.zeros(3, np.float32)
+    r = O.verify_request(t, a, b, d, None, u, 0.0, fuse_bonus=True)
+    assert r.accept_len == 2 and r.next_token == 1
+    f = np.array([3.0, 4.5, 0, 0, 0, 0])
+    assert abs(r.fused_logprobs[2] - sps.log_softmax(f)[1]) < 1e-12
+    assert O.verify_request(t, a, b, d, None, u, 0.0).next_token == 0
