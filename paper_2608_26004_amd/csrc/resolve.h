@@ -412,7 +412,9 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
 // kMode 0: interior chunk (no masking); 1: masked, branch-free; 2: generic
 // (one vector at a time, array-end repair).
 // kKL: the divergence term is KL's (the KL gate) rather than the JSD's.
-template <int DT, int kMode, int DM, bool kKL>
+// kNb: a and b differ somewhere in the row; otherwise b is a bitwise copy of
+// a and a's vectors stand in for it (such a row has no divergence task).
+template <int DT, int kMode, int DM, bool kKL, bool kNb>
 DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bool dr, bool db,
                     const ResidConst& rk, const JsdConst& jk, float& accj, float& seg) {
   constexpr int VE = Elem<DT>::VE;
@@ -429,7 +431,7 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bo
       const uint32_t off = (uint32_t)((rel0 + (long long)(k0 + k) * 64) * 16);
       vt[k] = nt ? buf_load_nt(rt, off) : u4{0, 0, 0, 0};
       va[k] = nab ? buf_load_nt(ra, off) : u4{0, 0, 0, 0};
-      vb[k] = nab ? buf_load_nt(rb, off) : u4{0, 0, 0, 0};
+      if (kNb) vb[k] = nab ? buf_load_nt(rb, off) : u4{0, 0, 0, 0};
     }
     #pragma unroll
     for (int k = 0; k < kG; ++k) {
@@ -437,14 +439,15 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bo
       if (kMode == 1) {
         mask_vec<DT>(A, g, vi, vt[k]);
         mask_vec<DT>(A, g, vi, va[k]);
-        mask_vec<DT>(A, g, vi, vb[k]);
+        if (kNb) mask_vec<DT>(A, g, vi, vb[k]);
       } else if (kMode == 2) {
         if (nt) fix_vec<DT>(A, g, A.t, vi, vt[k]);
         if (nab) {
           fix_vec<DT>(A, g, A.a, vi, va[k]);
-          fix_vec<DT>(A, g, A.b, vi, vb[k]);
+          if (kNb) fix_vec<DT>(A, g, A.b, vi, vb[k]);
         }
       }
+      if (!kNb) vb[k] = va[k];
       float vj[VE], vr[VE];
       #pragma unroll
       for (int e = 0; e < VE; ++e) {
@@ -463,17 +466,17 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bo
   }
 }
 
-template <int DT, int DM, bool kKL>
+template <int DT, int DM, bool kKL, bool kNb>
 DEV void pass2_sums_any(const KArgs& A, const RowGeo& g, long long rel0, long long c0, long long c1,
                         bool dj, bool dr, bool db, const ResidConst& rk, const JsdConst& jk, float& accj,
                         float& seg) {
   constexpr int VE = Elem<DT>::VE;
   if (has_tail(A, c0, c1))
-    pass2_sums<DT, 2, DM, kKL>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 2, DM, kKL, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
   else if (c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
-    pass2_sums<DT, 0, DM, kKL>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 0, DM, kKL, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
   else
-    pass2_sums<DT, 1, DM, kKL>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 1, DM, kKL, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
 }
 
 template <int DT, int DM>
@@ -494,11 +497,14 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
     const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
     float accj = 0.0f, seg = 0.0f;
     if (task != 0) {
-      // JSD rows of the KL gate take the KL term (a rare, separate instance)
+      // JSD rows of the KL gate take the KL term (a rare, separate instance);
+      // a row with a == b bitwise has no divergence task and skips b
       if (dj && A.gate_mode == ASYMSPEC_GATE_KL)
-        pass2_sums_any<DT, DM, true>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
+        pass2_sums_any<DT, DM, true, true>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
+      else if ((cst[D_STATUS] & kStNeq) != 0u)
+        pass2_sums_any<DT, DM, false, true>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
       else
-        pass2_sums_any<DT, DM, false>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
+        pass2_sums_any<DT, DM, false, false>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
     }
     const float wj = wave_sum(accj);
     const float wseg = wave_sum(seg);

@@ -64,20 +64,36 @@ ASYM_HD inline int sched_block(int parts, int K, int S) {
          ((parts & kPartPass2) ? S : 0) + ((parts & kPartPick) ? 1 : 0);
 }
 
+#ifndef ASYMSPEC_LAG_PCT
+#define ASYMSPEC_LAG_PCT 400
+#endif
+#ifndef ASYMSPEC_LAG2_PCT
+#define ASYMSPEC_LAG2_PCT ASYMSPEC_LAG_PCT
+#endif
+#ifndef ASYMSPEC_LAG3_PCT
+#define ASYMSPEC_LAG3_PCT ASYMSPEC_LAG2_PCT
+#endif
+
 // Lags in steps.  items_in_flight is the number of workgroups the chip holds
 // at once; the items of one request finish about that many items after the
 // first of them starts, and a resolve item that waits holds its workgroup, so
-// each lag spans lag_pct percent of items_in_flight statistics items.
-// Returns false when the schedule would not fit in 31-bit indices.
-inline bool sched_build(int B, int K, int S, int items_in_flight, Sched& sc, int lag_pct = 400) {
+// the decide lag spans lag_pct percent of items_in_flight statistics items,
+// and the pass-2 and pick lags add lag2_pct and lag3_pct percent to the lag
+// before them.  Returns false when the schedule would not fit in 31-bit
+// indices.
+inline bool sched_build(int B, int K, int S, int items_in_flight, Sched& sc,
+                        int lag_pct = ASYMSPEC_LAG_PCT, int lag2_pct = ASYMSPEC_LAG2_PCT,
+                        int lag3_pct = ASYMSPEC_LAG3_PCT) {
   if (B < 1 || K < 0 || S < 1 || items_in_flight < 1) return false;
   // steps hold at least the (K+1) * S statistics items of their request
   const long long per_step = (long long)(K + 1) * S;
-  const long long span = (long long)items_in_flight * lag_pct / 100;
-  const int window = (int)((span + per_step - 1) / per_step);
-  sc.L1 = window + 1;
-  sc.L2 = sc.L1 + window + 1;
-  sc.L3 = sc.L2 + window + 1;
+  auto window = [&](int pct) {
+    const long long span = (long long)items_in_flight * pct / 100;
+    return (int)((span + per_step - 1) / per_step);
+  };
+  sc.L1 = window(lag_pct) + 1;
+  sc.L2 = sc.L1 + window(lag2_pct) + 1;
+  sc.L3 = sc.L2 + window(lag3_pct) + 1;
   int bp[8] = {0, sc.L1, sc.L2, sc.L3, B, B + sc.L1, B + sc.L2, B + sc.L3};
   // sort the 8 boundaries (insertion sort) and drop duplicates
   for (int i = 1; i < 8; ++i)
