@@ -152,6 +152,8 @@ def main():
     ap.add_argument("--delta-mode", choices=["a-b", "a", "t-b"], default="a-b",
                     help="source of delta in f = t + beta delta (a-b: the paper's)")
     ap.add_argument("--lam", type=float, default=0.1, help="scale of the lambda gate")
+    ap.add_argument("--full", action="store_true",
+                    help="also write the full [B, K+1, V] fp32 log-probability rows (second kernel)")
     ap.add_argument("--fuse-bonus", action="store_true",
                     help="take the bonus token from the fused row f_K (reads rows K of a and b)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -210,13 +212,16 @@ def main():
     gm = {"cda": asp.GATE_CDA, "fixed": asp.GATE_FIXED, "kl": asp.GATE_KL,
           "lambda": asp.GATE_LAMBDA}[args.gate_mode]
     dm = {"a-b": asp.DELTA_AB, "a": asp.DELTA_A, "t-b": asp.DELTA_TB}[args.delta_mode]
-    var = dict(gate_mode=gm, delta_mode=dm, lam=args.lam, fuse_bonus=args.fuse_bonus)
+    var = dict(gate_mode=gm, delta_mode=dm, lam=args.lam, fuse_bonus=args.fuse_bonus,
+               return_full=args.full)
     outs = asp.fuse_verify(*copies[0], d, q, u, tau, return_gate=args.gate, workspace=ws, **var)
     outs = tuple(o for o in outs)
+    # (accept_len, next_token, fused_logprobs, gate or None[, full])
+    out_arg = outs[:3] + ((outs[3],) if args.gate else (None,)) + ((outs[-1],) if args.full else ())
 
     def step(i):
         return asp.fuse_verify(*copies[i % len(copies)], d, q, u, tau, return_gate=args.gate,
-                               workspace=ws, out=outs if args.gate else outs + (None,), **var)
+                               workspace=ws, out=out_arg, **var)
 
     for i in range(args.warmup):
         step(i)
@@ -240,6 +245,9 @@ def main():
     kern_ms = float(np.mean(per))
     rows = B * (K + 1)
     nbytes = x.nbytes_read(args.fuse_bonus)
+    if args.full:
+        # the second kernel reads the rows again and writes 4 bytes per element
+        nbytes += x.nbytes_read(args.fuse_bonus) + 4 * B * (K + 1) * V
     achieved = nbytes / (kern_ms * 1e-3) / 1e9
 
     if args.calibrate_copy:
@@ -254,7 +262,7 @@ def main():
     traffic = None
     tpath = os.path.join(ROOT, "profiles", f"traffic_{wl.name}.json")
     default_variant = (args.gate_mode == "cda" and args.delta_mode == "a-b" and not args.gate
-                       and not args.fuse_bonus)
+                       and not args.fuse_bonus and not args.full)
     if default_variant and os.path.exists(tpath):
         try:
             tj = json.load(open(tpath))
@@ -279,7 +287,7 @@ def main():
         "config": {"workload": wl.name, "B": B, "K": K, "V": V, "rows_per_step": rows,
                    "bytes_per_step": nbytes, "gate_output": bool(args.gate),
                    "gate_mode": args.gate_mode, "delta_mode": args.delta_mode,
-                   "fuse_bonus": bool(args.fuse_bonus),
+                   "fuse_bonus": bool(args.fuse_bonus), "full_logprobs": bool(args.full),
                    "input_copies": len(copies), "mean_accept_len": float(acc.mean()),
                    "parallelism": "single GPU"},
         "hbm_GBps": achieved,

@@ -145,6 +145,15 @@ int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stre
  *                       is the JSD (CDA and fixed gates), the KL (KL gate) or
  *                       lambda * Delta_i(d_i) (lambda gate), and gamma_eff_i =
  *                       gamma (fixed gate) or gamma * exp(-D_i)
+ *   fused_logprobs_full [B][K+1][V] float out, or NULL; 16-byte aligned.  Every
+ *                       element's log-probability under its row's distribution:
+ *                       rows i < K log softmax(f_i/tau), row K log softmax(t_K/tau)
+ *                       (of f_K with ASYMSPEC_FUSE_BONUS), tau = 1 for greedy
+ *                       requests; -inf where f is not a number.  Written by a
+ *                       second kernel on `stream` that reads the logits again
+ *                       (3 (K+1) V elements) and writes 4 (K+1) V bytes per request;
+ *                       one workgroup per 32 KiB chunk of a row, so B (K+1) times
+ *                       the chunks per row must stay below 2^32 (else E_ARG)
  *   workspace           device scratch of >= asymspec_workspace_size bytes,
  *                       256-byte aligned, contents opaque between calls
  *   stream              hipStream_t or NULL
@@ -166,6 +175,7 @@ int asymspec_fuse_verify(const void* verifier_logits,
                          int32_t* next_token,
                          float* fused_logprobs,
                          float* gate_out,
+                         float* fused_logprobs_full,
                          void* workspace, size_t workspace_bytes,
                          void* stream);
 

@@ -416,3 +416,27 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
             gate[k, i, 1] = row.gamma_eff
         res.append(r)
     return acc, nxt, flp, gate, res
+
+
+def fused_logprobs_full(t, a, b, temperature, beta: float = 1.0,
+                        delta_mode: int = DELTA_AB, fuse_bonus: bool = False):
+    """Every element's log-probability under its row's distribution, fp64
+    [B][K+1][V]: rows i < K the fused target log softmax(f_i / tau) (Eq. 2,
+    f in fp32 as in ``fused_logits_f32``, a NaN there counted as masked);
+    row K the bonus distribution log softmax(t_K / tau) of Alg. 1, or of f_K
+    with ``fuse_bonus``.  tau = 1 for a greedy request (tau <= 0), as for
+    ``fused_logprobs``."""
+    t32, a32, b32 = to_f32(t), to_f32(a), to_f32(b)
+    B, Kp1, V = t32.shape
+    K = Kp1 - 1
+    out = np.empty((B, Kp1, V), dtype=np.float64)
+    for bi in range(B):
+        tau = float(temperature[bi])
+        tau = tau if tau > 0.0 else 1.0
+        for i in range(Kp1):
+            if i < K or fuse_bonus:
+                x = fused_logits_f32(t32[bi, i], a32[bi, i], b32[bi, i], beta, delta_mode)
+            else:
+                x = t32[bi, i]
+            out[bi, i] = log_softmax(x, tau)
+    return out

@@ -65,7 +65,7 @@ def load_library(path: str | None = None):
     lib.asymspec_workspace_clear.argtypes = [vp, sz, vp]
     lib.asymspec_workspace_clear.restype = i32
     lib.asymspec_fuse_verify.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, i32, i32, i32,
-                                         ctypes.POINTER(_Params), vp, vp, vp, vp, vp, sz, vp]
+                                         ctypes.POINTER(_Params), vp, vp, vp, vp, vp, vp, sz, vp]
     lib.asymspec_fuse_verify.restype = i32
     lib.asymspec_status_string.argtypes = [i32]
     lib.asymspec_status_string.restype = ctypes.c_char_p
@@ -114,7 +114,8 @@ _default_ws = {}
 def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
                 beta: float = 1.0, gamma: float = 0.5, gate_mode: int = GATE_CDA,
                 return_gate: bool = False, workspace: Workspace | None = None, out=None,
-                delta_mode: int = DELTA_AB, lam: float = 0.1, fuse_bonus: bool = False):
+                delta_mode: int = DELTA_AB, lam: float = 0.1, fuse_bonus: bool = False,
+                return_full: bool = False):
     """One AsymSpec decision step on the current HIP stream.
 
     t, a, b: [B, K+1, V] torch.bfloat16 or torch.float32 on the GPU
@@ -122,9 +123,12 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     uniforms: [B, K+1] float32; temperature: [B] float32 (<= 0: greedy).
     gate_mode: GATE_CDA (the paper), GATE_FIXED, GATE_KL or GATE_LAMBDA (with
     scale lam); delta_mode: DELTA_AB (the paper), DELTA_A or DELTA_TB;
-    fuse_bonus: take the bonus token from f_K rather than t_K (FUSE_BONUS).
+    fuse_bonus: take the bonus token from f_K rather than t_K (FUSE_BONUS);
+    return_full: also return every element's log-probability under its row's
+    distribution, [B, K+1, V] float32 (a second pass over the logits).
     Returns (accept_len [B] int32, next_token [B] int32,
-             fused_logprobs [B, K+1] float32[, gate [B, K, 2] float32])."""
+             fused_logprobs [B, K+1] float32[, gate [B, K, 2] float32]
+             [, full [B, K+1, V] float32])."""
     import torch
     lib = load_library()
     if t.dtype == torch.bfloat16:
@@ -157,8 +161,10 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
         nxt = torch.empty(B, dtype=torch.int32, device=dev)
         flp = torch.empty(B, K + 1, dtype=torch.float32, device=dev)
         gate = torch.empty(B, K, 2, dtype=torch.float32, device=dev) if return_gate else None
+        full = torch.empty(B, K + 1, V, dtype=torch.float32, device=dev) if return_full else None
     else:
-        acc, nxt, flp, gate = out
+        acc, nxt, flp, gate = out[:4]
+        full = out[4] if len(out) > 4 else None
     ws_bytes = workspace_size(B, K, V, dt)
     if ws_bytes == 0:
         raise AsymSpecError(E_ARG, "invalid shape")
@@ -170,10 +176,13 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     st = lib.asymspec_fuse_verify(_ptr(t), _ptr(a), _ptr(b), dt, _ptr(draft_tokens),
                                   _ptr(draft_probs), _ptr(uniforms), _ptr(temperature),
                                   B, K, V, ctypes.byref(params), _ptr(acc), _ptr(nxt),
-                                  _ptr(flp), _ptr(gate), _ptr(wsbuf), wsbuf.numel(),
+                                  _ptr(flp), _ptr(gate), _ptr(full), _ptr(wsbuf), wsbuf.numel(),
                                   _stream_handle(dev))
     if st != OK:
         raise AsymSpecError(st, status_string(st))
+    res = (acc, nxt, flp)
     if return_gate:
-        return acc, nxt, flp, gate
-    return acc, nxt, flp
+        res += (gate,)
+    if return_full:
+        res += (full,)
+    return res

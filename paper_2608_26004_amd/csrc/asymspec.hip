@@ -35,6 +35,7 @@
 
 #include "asymspec.h"
 #include "device.h"
+#include "dump.h"
 #include "resolve.h"
 #include "schedule.h"
 #include "stats.h"
@@ -152,6 +153,15 @@ static const void* kernel_ptr(int dtype, bool beta1, int dm) {
   return dtype == ASYMSPEC_BF16 ? kernel_ptr_dt<ASYMSPEC_BF16>(beta1, dm)
                                 : kernel_ptr_dt<ASYMSPEC_FP32>(beta1, dm);
 }
+template <int DT>
+static const void* dump_ptr_dt(int dm) {
+  if (dm == kDeltaA) return (const void*)dump_kernel<DT, kDeltaA>;
+  if (dm == kDeltaTB) return (const void*)dump_kernel<DT, kDeltaTB>;
+  return (const void*)dump_kernel<DT, kDeltaAB>;
+}
+static const void* dump_ptr(int dtype, int dm) {
+  return dtype == ASYMSPEC_BF16 ? dump_ptr_dt<ASYMSPEC_BF16>(dm) : dump_ptr_dt<ASYMSPEC_FP32>(dm);
+}
 
 static const DevInfo* device_info() {
   int dev = 0;
@@ -223,8 +233,8 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
                          const float* uniforms, const float* temperature,
                          int B, int K, int V, const asymspec_params* params,
                          int32_t* accept_len, int32_t* next_token, float* fused_logprobs,
-                         float* gate_out, void* workspace, size_t workspace_bytes,
-                         void* stream) {
+                         float* gate_out, float* fused_logprobs_full, void* workspace,
+                         size_t workspace_bytes, void* stream) {
   Layout L;
   if (params == nullptr) return ASYMSPEC_E_ARG;
   if (!make_layout(B, K, V, dtype, L)) return ASYMSPEC_E_ARG;
@@ -244,7 +254,7 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   if (!aligned(uniforms, 4) || !aligned(temperature, 4) || !aligned(accept_len, 4) ||
       !aligned(next_token, 4) || !aligned(fused_logprobs, 4) ||
       (draft_tokens && !aligned(draft_tokens, 4)) || (draft_probs && !aligned(draft_probs, 4)) ||
-      (gate_out && !aligned(gate_out, 4)))
+      (gate_out && !aligned(gate_out, 4)) || (fused_logprobs_full && !aligned(fused_logprobs_full, 16)))
     return ASYMSPEC_E_ALIGN;
   if (!aligned(workspace, 256)) return ASYMSPEC_E_ALIGN;
   if (workspace_bytes < L.total) return ASYMSPEC_E_WORKSPACE;
@@ -275,9 +285,18 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   if (!sched_build(B, K, L.S, di->max_blocks[dtype], A.sc)) return ASYMSPEC_E_ARG;
   const int grid = A.sc.total;
 
+  const unsigned long long nblk = (unsigned long long)B * (K + 1) * L.S;
+  if (fused_logprobs_full != nullptr && nblk > 0xFFFFFFFFull) return ASYMSPEC_E_ARG;
   void* args[] = {&A};
-  const hipError_t e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f, params->delta_mode), dim3(grid),
-                                       dim3(kThreads), args, 0, (hipStream_t)stream);
+  hipError_t e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f, params->delta_mode), dim3(grid),
+                                 dim3(kThreads), args, 0, (hipStream_t)stream);
+  if (e == hipSuccess && fused_logprobs_full != nullptr) {
+    // one workgroup per (row, chunk), after the decision kernel on the stream
+    float* full = fused_logprobs_full;
+    void* dargs[] = {&A, &full};
+    e = hipLaunchKernel(dump_ptr(dtype, params->delta_mode), dim3((unsigned)nblk), dim3(kThreads), dargs, 0,
+                        (hipStream_t)stream);
+  }
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return ASYMSPEC_E_DEVICE;
@@ -296,6 +315,6 @@ const char* asymspec_status_string(int status) {
   }
 }
 
-int asymspec_version(void) { return 200; }
+int asymspec_version(void) { return 300; }
 
 }  // extern "C"

@@ -93,6 +93,8 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const f
       v[D_LPD] = __float_as_uint((float)lpd);
       v[D_LPEMIT] = __float_as_uint((float)(((double)M[sF] * (double)kL2E - L2[sF]) * kLn2));
       v[D_ARG] = (uint32_t)arg;
+      v[D_L2E_LO] = dlo(L2[sF]);
+      v[D_L2E_HI] = dhi(L2[sF]);
       // D >= 0 for the divergence gates (and D = 0 when a == b bitwise),
       // D <= ln 2 for the JSD; outside those bounds the row stays open
       if (gm == ASYMSPEC_GATE_LAMBDA) accept = m0 + Dl > 0.0;

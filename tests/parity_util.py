@@ -29,7 +29,7 @@ def to_device(x, device="cuda"):
 
 
 def run_gpu(inp, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True, want_gate=True,
-            device="cuda", delta_mode=0, lam=0.1, fuse_bonus=False):
+            device="cuda", delta_mode=0, lam=0.1, fuse_bonus=False, want_full=False):
     import torch
     import paper_2608_26004_amd as asp
     t, a, b = (to_device(x, device) for x in (inp.t, inp.a, inp.b))
@@ -39,11 +39,12 @@ def run_gpu(inp, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True, want_gate=Tr
     tau = to_device(inp.temperature.astype(np.float32), device)
     out = asp.fuse_verify(t, a, b, d, q, u, tau, beta=beta, gamma=gamma,
                           gate_mode=gate_mode, return_gate=want_gate,
-                          delta_mode=delta_mode, lam=lam, fuse_bonus=fuse_bonus)
+                          delta_mode=delta_mode, lam=lam, fuse_bonus=fuse_bonus,
+                          return_full=want_full)
     torch.cuda.synchronize()
     res = [x.cpu().numpy() for x in out]
     if not want_gate:
-        res.append(None)
+        res.insert(3, None)
     return res
 
 
@@ -51,7 +52,7 @@ def compare(inp, gpu, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True,
             requests=None, label="", delta_mode=0, lam=0.1, fuse_bonus=False):
     """Run the oracle on `requests` (all by default) and compare.  Returns a
     dict report; raises AssertionError on a parity failure."""
-    acc_g, nxt_g, flp_g, gate_g = gpu
+    acc_g, nxt_g, flp_g, gate_g = gpu[:4]
     idx = list(range(inp.B)) if requests is None else list(requests)
     acc_o, nxt_o, flp_o, gate_o, res = O.fuse_verify(
         inp.t, inp.a, inp.b, inp.draft_tokens, inp.draft_probs if with_probs else None,
@@ -92,3 +93,19 @@ def compare(inp, gpu, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True,
     assert max_lp <= LP_TOL, f"{label}: fused_logprobs error {max_lp}"
     assert max_gate <= LP_TOL, f"{label}: gate error {max_gate}"
     return report
+
+
+def compare_full(inp, full_g, beta=1.0, delta_mode=0, fuse_bonus=False, requests=None, label=""):
+    """Element-by-element check of the full log-probability rows against the
+    oracle on `requests` (all by default): -inf exactly where the oracle has
+    it, otherwise within LP_TOL absolute.  Returns the largest error."""
+    idx = list(range(inp.B)) if requests is None else list(requests)
+    full_o = O.fused_logprobs_full(inp.t[idx], inp.a[idx], inp.b[idx], inp.temperature[idx],
+                                   beta=beta, delta_mode=delta_mode, fuse_bonus=fuse_bonus)
+    g = full_g[idx].astype(np.float64)
+    fin_o = np.isfinite(full_o)
+    assert np.array_equal(fin_o, np.isfinite(g)), f"{label}: -inf pattern differs"
+    assert (g[~fin_o] == full_o[~fin_o]).all(), f"{label}: non-finite values differ"
+    err = float(np.abs(g[fin_o] - full_o[fin_o]).max()) if fin_o.any() else 0.0
+    assert err <= LP_TOL, f"{label}: full log-prob error {err}"
+    return err

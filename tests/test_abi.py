@@ -57,14 +57,14 @@ def _call(**over):
     fake = 1 << 20          # 16-B and 256-B aligned fake device addresses
     kw = dict(t=fake, a=fake, b=fake, dtype=0, d=fake, dp=None, u=fake, tau=fake,
               B=2, K=2, V=64, beta=1.0, gamma=0.5, mode=0, flags=0, delta=0, lam=0.1,
-              acc=fake, nxt=fake, flp=fake, gate=None, ws=fake, wsb=None, stream=None)
+              acc=fake, nxt=fake, flp=fake, gate=None, full=None, ws=fake, wsb=None, stream=None)
     kw.update(over)
     if kw["wsb"] is None:
         kw["wsb"] = asp.workspace_size(max(kw["B"], 1), max(kw["K"], 0), max(kw["V"], 1), 0) or 1 << 20
     p = asp._Params(kw["beta"], kw["gamma"], kw["mode"], kw["flags"], kw["delta"], kw["lam"])
     return lib.asymspec_fuse_verify(kw["t"], kw["a"], kw["b"], kw["dtype"], kw["d"], kw["dp"],
                                     kw["u"], kw["tau"], kw["B"], kw["K"], kw["V"], ctypes.byref(p),
-                                    kw["acc"], kw["nxt"], kw["flp"], kw["gate"], kw["ws"], kw["wsb"],
+                                    kw["acc"], kw["nxt"], kw["flp"], kw["gate"], kw["full"], kw["ws"], kw["wsb"],
                                     kw["stream"])
 
 
@@ -99,6 +99,7 @@ def _call(**over):
     (dict(t=(1 << 20) + 4), asp.E_ALIGN),
     (dict(b=(1 << 20) + 8), asp.E_ALIGN),
     (dict(flp=(1 << 20) + 2), asp.E_ALIGN),
+    (dict(full=(1 << 20) + 4), asp.E_ALIGN),
     (dict(ws=(1 << 20) + 64), asp.E_ALIGN),
     (dict(wsb=16), asp.E_WORKSPACE),
 ])

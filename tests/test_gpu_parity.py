@@ -6,7 +6,7 @@ import pytest
 
 from paper_2608_26004_amd import synth
 
-from parity_util import compare, run_gpu
+from parity_util import compare, compare_full, run_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -238,3 +238,48 @@ def test_fuse_bonus_workload_1(gpu):
     _reach_bonus(x, range(0, x.B, 2))
     g = run_gpu(x, with_probs=False, fuse_bonus=True)
     _note(compare(x, g, with_probs=False, fuse_bonus=True, label="fuse_bonus workload 1"))
+
+
+# --------------------------------------------- full log-probability rows --
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("tau", [0.0, 1.0, 0.7])
+@pytest.mark.parametrize("delta,fb", [(0, False), (0, True), (1, False), (2, True)])
+def test_full_logprobs_small(gpu, dtype, tau, delta, fb):
+    x = synth.generate(B=5, K=3, V=5000, dtype=dtype, rho=("alternate", 0.0, 2.0), tau=tau,
+                       seed=400 + delta)
+    g = run_gpu(x, delta_mode=delta, fuse_bonus=fb, want_full=True)
+    # the decision outputs are those of the call without the full rows
+    g0 = run_gpu(x, delta_mode=delta, fuse_bonus=fb)
+    for u, v in zip(g[:4], g0[:4]):
+        assert np.array_equal(u, v)
+    _note(compare(x, g, delta_mode=delta, fuse_bonus=fb, label=f"full {dtype} tau={tau} d={delta} fb={fb}"))
+    err = compare_full(x, g[4], delta_mode=delta, fuse_bonus=fb, label=f"full {dtype} tau={tau}")
+    print(f"[full] {dtype} tau={tau} delta={delta} fb={fb}: max abs err {err:.2e}")
+
+
+@pytest.mark.parametrize("V,K", [(1, 0), (1, 2), (3, 1), (4097, 0), (4097, 3), (16385, 2)])
+def test_full_logprobs_edges(gpu, V, K):
+    x = synth.generate(B=3, K=K, V=V, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=V + K)
+    for fb in (False, True):
+        g = run_gpu(x, fuse_bonus=fb, want_full=True)
+        compare_full(x, g[4], fuse_bonus=fb, label=f"full edge V={V} K={K} fb={fb}")
+
+
+def test_full_logprobs_masks_and_beta(gpu):
+    x = synth.generate(B=4, K=2, V=3000, dtype="fp32", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 0.8), seed=91)
+    x.a[:, :, 10:20] = -np.inf
+    x.b[:, :, 10:20] = -np.inf
+    x.t[:, :, 10:25] = -np.inf
+    x.b[1] = x.a[1]
+    for beta in (1.0, 0.35):
+        g = run_gpu(x, beta=beta, want_full=True)
+        compare_full(x, g[4], beta=beta, label=f"full masks beta={beta}")
+
+
+def test_full_logprobs_workload_1(gpu):
+    x = synth.workload_inputs(1)
+    g = run_gpu(x, want_full=True)
+    err = compare_full(x, g[4], requests=[0, 3, 7], label="full workload 1")
+    print(f"[full] workload 1: max abs err {err:.2e}")

@@ -513,3 +513,48 @@ def test_fused_bonus_follows_the_fused_row():
     f = np.array([3.0, 4.5, 0, 0, 0, 0])
     assert abs(r.fused_logprobs[2] - sps.log_softmax(f)[1]) < 1e-12
     assert O.verify_request(t, a, b, d, None, u, 0.0).next_token == 0
+
+
+# ------------------------------------------------ full log-prob rows --
+def test_full_logprobs_pinned_to_scipy_and_outputs():
+    """Each row of the full dump is scipy's log_softmax of that row's
+    distribution (fused rows at 1/tau, the unfused bonus row from t alone),
+    normalised to 1, and agrees with the per-draft fused log-probability the
+    decision step reports (Alg. 1 outputs)."""
+    rng = np.random.default_rng(51)
+    B, K, V = 3, 2, 40
+    t = rng.normal(0, 2, (B, K + 1, V)).astype(np.float32)
+    a = rng.normal(0, 2, (B, K + 1, V)).astype(np.float32)
+    b = (a + rng.normal(0, 1, (B, K + 1, V))).astype(np.float32)
+    d = rng.integers(0, V, (B, K)).astype(np.int32)
+    u = rng.random((B, K + 1)).astype(np.float32)
+    tau = np.array([0.0, 1.0, 0.6], np.float32)
+    full = O.fused_logprobs_full(t, a, b, tau, beta=0.5)
+    for bi in range(B):
+        tt = tau[bi] if tau[bi] > 0 else 1.0
+        for i in range(K):
+            # f in fp32 (Eq. 2 as stored), then scipy in fp64
+            f = (t[bi, i] + np.float32(0.5) * (a[bi, i] - b[bi, i])).astype(np.float64)
+            np.testing.assert_allclose(full[bi, i], sps.log_softmax(f / tt), atol=1e-12)
+        np.testing.assert_allclose(full[bi, K], sps.log_softmax(t[bi, K].astype(np.float64) / tt), atol=1e-12)
+        assert abs(sps.logsumexp(full[bi], axis=1)).max() < 1e-12
+        r = O.verify_request(t[bi], a[bi], b[bi], d[bi], None, u[bi], tau[bi], beta=0.5)
+        for i in range(K):
+            assert abs(full[bi, i, d[bi, i]] - r.fused_logprobs[i]) < 1e-12
+    fb = O.fused_logprobs_full(t, a, b, tau, beta=0.5, fuse_bonus=True)
+    f_k = (t[:, K] + np.float32(0.5) * (a[:, K] - b[:, K])).astype(np.float64)
+    np.testing.assert_allclose(fb[0, K], sps.log_softmax(f_k[0]), atol=1e-12)
+    assert (fb[:, :K] == full[:, :K]).all()
+
+
+def test_full_logprobs_masked_tokens():
+    """A token both drafter views mask (a = b = -inf) has a NaN fused logit:
+    it gets -inf, and the rest of the row still sums to one."""
+    t = np.zeros((1, 2, 5), np.float32)
+    a = np.zeros((1, 2, 5), np.float32)
+    b = np.zeros((1, 2, 5), np.float32)
+    a[0, 0, 1] = b[0, 0, 1] = -np.inf
+    full = O.fused_logprobs_full(t, a, b, np.array([1.0], np.float32))
+    assert full[0, 0, 1] == -np.inf
+    np.testing.assert_allclose(full[0, 0, [0, 2, 3, 4]], np.log(0.25), atol=1e-15)
+    np.testing.assert_allclose(full[0, 1], np.log(0.2), atol=1e-15)
