@@ -154,6 +154,8 @@ def main():
     ap.add_argument("--lam", type=float, default=0.1, help="scale of the lambda gate")
     ap.add_argument("--full", action="store_true",
                     help="also write the full [B, K+1, V] fp32 log-probability rows (second kernel)")
+    ap.add_argument("--xvocab", type=str, default=None, metavar="VD:SHARED",
+                    help="cross-family drafter: vocabulary size and shared tokens, e.g. 128256:109566")
     ap.add_argument("--fuse-bonus", action="store_true",
                     help="take the bonus token from the fused row f_K (reads rows K of a and b)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -185,7 +187,7 @@ def main():
     print(f"[bench] generated {wl.name} in {t_gen:.1f} s", file=sys.stderr, flush=True)
 
     cpu = None
-    if not args.no_cpu:
+    if not args.no_cpu and not args.xvocab:
         cpu = cpu_baseline(x, args.cpu_requests, args.cpu_seconds)
         print(f"[bench] cpu baseline {cpu['value']:.1f} rows/s on {cpu['cores']} cores",
               file=sys.stderr, flush=True)
@@ -201,7 +203,20 @@ def main():
             return torch.from_numpy(arr.view(np.int16)).to(dev).view(torch.bfloat16)
         return torch.from_numpy(np.ascontiguousarray(arr)).to(dev)
 
-    base = [dev_tensor(v) for v in (x.t, x.a, x.b)]
+    vmap = None
+    xv_bytes = None
+    if args.xvocab:
+        vd, nsh = (int(s) for s in args.xvocab.split(":"))
+        ad, bd, vm, dx = synth.cross_vocab(x, vd, nsh, seed=1)
+        x.draft_tokens = dx
+        base = [dev_tensor(x.t), dev_tensor(ad), dev_tensor(bd)]
+        vmap = dev_tensor(vm)
+        el = 2 if wl.dtype == "bf16" else 4
+        # t rows, the shared entries of the drafter rows, the map once
+        xv_bytes = x.B * ((x.K + 1) * x.V + 2 * x.K * int((vm >= 0).sum())) * el + 4 * x.V
+        del ad, bd
+    else:
+        base = [dev_tensor(v) for v in (x.t, x.a, x.b)]
     copies = [base] + [[v.clone() for v in base] for _ in range(max(0, args.copies - 1))]
     d = dev_tensor(x.draft_tokens)
     q = dev_tensor(x.draft_probs)
@@ -213,7 +228,7 @@ def main():
           "lambda": asp.GATE_LAMBDA}[args.gate_mode]
     dm = {"a-b": asp.DELTA_AB, "a": asp.DELTA_A, "t-b": asp.DELTA_TB}[args.delta_mode]
     var = dict(gate_mode=gm, delta_mode=dm, lam=args.lam, fuse_bonus=args.fuse_bonus,
-               return_full=args.full)
+               return_full=args.full, vocab_map=vmap)
     outs = asp.fuse_verify(*copies[0], d, q, u, tau, return_gate=args.gate, workspace=ws, **var)
     outs = tuple(o for o in outs)
     # (accept_len, next_token, fused_logprobs, gate or None[, full])
@@ -244,7 +259,7 @@ def main():
     ms_step = total_ms / args.steps
     kern_ms = float(np.mean(per))
     rows = B * (K + 1)
-    nbytes = x.nbytes_read(args.fuse_bonus)
+    nbytes = x.nbytes_read(args.fuse_bonus) if xv_bytes is None else xv_bytes
     if args.full:
         # the second kernel reads the rows again and writes 4 bytes per element
         nbytes += x.nbytes_read(args.fuse_bonus) + 4 * B * (K + 1) * V
@@ -262,7 +277,7 @@ def main():
     traffic = None
     tpath = os.path.join(ROOT, "profiles", f"traffic_{wl.name}.json")
     default_variant = (args.gate_mode == "cda" and args.delta_mode == "a-b" and not args.gate
-                       and not args.fuse_bonus and not args.full)
+                       and not args.fuse_bonus and not args.full and not args.xvocab)
     if default_variant and os.path.exists(tpath):
         try:
             tj = json.load(open(tpath))
@@ -288,6 +303,7 @@ def main():
                    "bytes_per_step": nbytes, "gate_output": bool(args.gate),
                    "gate_mode": args.gate_mode, "delta_mode": args.delta_mode,
                    "fuse_bonus": bool(args.fuse_bonus), "full_logprobs": bool(args.full),
+                   "xvocab": args.xvocab,
                    "input_copies": len(copies), "mean_accept_len": float(acc.mean()),
                    "parallelism": "single GPU"},
         "hbm_GBps": achieved,

@@ -70,15 +70,15 @@ extern "C" {
                                      hyperparameters") */
 #define ASYMSPEC_GATE_KL     2    /* gamma_eff = gamma * exp(-KL(P || Q)), P and Q the
                                      drafter views' softmaxes: the KL instantiation of
-                                     D in the JSD-vs-KL table (App. C); not bounded */
+                                     D in the JSD-vs-KL table (App. G); not bounded */
 #define ASYMSPEC_GATE_LAMBDA 3    /* gamma_eff = gamma * exp(-lambda * Delta(d)),
                                      Delta = log softmax(a) - log softmax(b) at the
                                      draft token: the tuned-lambda gate (App. B) */
 
 /* ---- sources of the context-gain signal delta (Eq. 1-2) ---------------- */
 #define ASYMSPEC_DELTA_AB 0       /* delta = a - b (Eq. 1, the paper's method)        */
-#define ASYMSPEC_DELTA_A  1       /* delta = a, raw-augmented (Sec. 5 ablation)       */
-#define ASYMSPEC_DELTA_TB 2       /* delta = t - b, SCD-style (Sec. 5 ablation)       */
+#define ASYMSPEC_DELTA_A  1       /* delta = a, raw-augmented (Sec. 6.2 ablation)     */
+#define ASYMSPEC_DELTA_TB 2       /* delta = t - b, SCD-style (Sec. 6.2 ablation)     */
 
 /* ---- flags ------------------------------------------------------------- */
 #define ASYMSPEC_FUSE_BONUS 1u    /* the bonus token comes from the fused row
@@ -178,6 +178,51 @@ int asymspec_fuse_verify(const void* verifier_logits,
                          float* fused_logprobs_full,
                          void* workspace, size_t workspace_bytes,
                          void* stream);
+
+/*
+ * The same step for a drafter and a verifier with different vocabularies
+ * (Sec. 6.4 and App. D): delta is computed in the
+ * drafter's vocabulary and carried to the verifier's through the
+ * string-identical tokens the two share, and committed tokens are restricted
+ * to that shared set.
+ *
+ *   verifier_logits     t [B][K+1][V] in the verifier's vocabulary, 16-byte aligned
+ *   drafter_full_logits a [B][K+1][Vd] in the drafter's vocabulary, 4-byte aligned
+ *   drafter_comp_logits b [B][K+1][Vd], 4-byte aligned
+ *   vocab_map           [V] int32 device array: vocab_map[x] is the drafter id of
+ *                       verifier token x, or -1 when x has no shared counterpart
+ *                       (entries outside [0, Vd) count as -1); 4-byte aligned
+ *   Vd                  drafter vocabulary size, B*(K+1)*Vd < 2^40
+ *   draft_tokens        verifier ids of the drafts
+ *   everything else     as for asymspec_fuse_verify
+ *
+ * Reading: every distribution of the step is taken over the shared set, as
+ * if each row were first carried into the verifier's vocabulary with the
+ * tokens outside the set masked in all three views: f(x) = t(x) + beta delta
+ * (vocab_map[x]), the log-softmaxes of Eq. 3-4 (so D and p_b), the sampling
+ * target and proposal, the emission and the bonus token.  Drafter tokens
+ * that no verifier token maps to are never read.  A draft outside the set has
+ * no mass in any view and is rejected.  The drafter rows are gathered element
+ * by element (a map is in general no permutation of contiguous runs).
+ */
+int asymspec_fuse_verify_xvocab(const void* verifier_logits,
+                                const void* drafter_full_logits,
+                                const void* drafter_comp_logits,
+                                int dtype,
+                                const int32_t* vocab_map, int Vd,
+                                const int32_t* draft_tokens,
+                                const float* draft_probs,
+                                const float* uniforms,
+                                const float* temperature,
+                                int B, int K, int V,
+                                const asymspec_params* params,
+                                int32_t* accept_len,
+                                int32_t* next_token,
+                                float* fused_logprobs,
+                                float* gate_out,
+                                float* fused_logprobs_full,
+                                void* workspace, size_t workspace_bytes,
+                                void* stream);
 
 /* Static text for a status code. */
 const char* asymspec_status_string(int status);

@@ -44,8 +44,8 @@ Conventions fixed here (each is listed with its reason in the design doc):
 * Each request's drafts/uniforms come in as inputs; this module draws no
   random numbers.
 
-Variants the paper compares against (Sec. 5 mechanism ablation; App. B
-"Models and hyperparameters" and the JSD-vs-KL table of App. C), selected by
+Variants the paper compares against (Sec. 6.2 mechanism ablation; App. B
+"Models and hyperparameters" and the JSD-vs-KL table of App. G), selected by
 ``gate_mode`` and ``delta_mode``:
 
 * gate FIXED   gamma_eff = gamma (standard speculative acceptance);
@@ -74,12 +74,12 @@ LN2 = math.log(2.0)
 
 GATE_CDA = 0      # gamma_eff = gamma * exp(-D)         (Sec. 3.3, Eq. 3)
 GATE_FIXED = 1    # gamma_eff = gamma  (fixed-gamma baseline of App. B)
-GATE_KL = 2       # gamma * exp(-KL(P || Q))            (App. C, JSD vs. KL)
+GATE_KL = 2       # gamma * exp(-KL(P || Q))            (App. G, JSD vs. KL)
 GATE_LAMBDA = 3   # gamma * exp(-lambda * Delta(d))     (App. B, tuned-lambda foil)
 
 DELTA_AB = 0      # delta = a - b   (Eq. 1, the paper's same-model source)
-DELTA_A = 1       # delta = a       (raw-augmented, Sec. 5 ablation)
-DELTA_TB = 2      # delta = t - b   (SCD-style, Sec. 5 ablation)
+DELTA_A = 1       # delta = a       (raw-augmented, Sec. 6.2 ablation)
+DELTA_TB = 2      # delta = t - b   (SCD-style, Sec. 6.2 ablation)
 
 
 # --------------------------------------------------------------------------
@@ -440,3 +440,37 @@ def fused_logprobs_full(t, a, b, temperature, beta: float = 1.0,
                 x = t32[bi, i]
             out[bi, i] = log_softmax(x, tau)
     return out
+
+
+# --------------------------------------------------------------------------
+# Sec. 6.4 and App. D: drafter and verifier from different model families.
+# delta is computed in the drafter's vocabulary and carried to the
+# verifier's through the string-identical tokens the two share; committed
+# tokens are restricted to that set.  Reading: every distribution of the
+# step is taken over the shared set, which is the same-vocabulary step on
+# rows carried into the verifier's vocabulary with the unshared tokens masked
+# in all three views.
+# --------------------------------------------------------------------------
+def map_to_verifier(t, a, b, vocab_map):
+    """t [B][K+1][V] (verifier vocabulary), a and b [B][K+1][Vd] (drafter
+    vocabulary), vocab_map [V] (drafter id of verifier token x, or -1).
+    Returns (t', a', b') over the verifier vocabulary in the stored dtype:
+    a'(x) = a(vocab_map[x]), b' likewise, and t' = t, where x is shared;
+    -inf in all three where it is not."""
+    vm = np.asarray(vocab_map, dtype=np.int64)
+    Vd = a.shape[-1]
+    shared = (vm >= 0) & (vm < Vd)
+    j = np.where(shared, vm, 0)
+    neg = np.uint16(0xFF80) if t.dtype == np.uint16 else np.float32(-np.inf)
+    t2 = np.where(shared, t, neg).astype(t.dtype)
+    a2 = np.where(shared, a[..., j], neg).astype(a.dtype)
+    b2 = np.where(shared, b[..., j], neg).astype(b.dtype)
+    return t2, a2, b2
+
+
+def fuse_verify_xvocab(t, a, b, vocab_map, draft_tokens, draft_probs, uniforms,
+                       temperature, **kw):
+    """fuse_verify for a cross-family pair: the rows carried into the
+    verifier's vocabulary first (``map_to_verifier``)."""
+    t2, a2, b2 = map_to_verifier(t, a, b, vocab_map)
+    return fuse_verify(t2, a2, b2, draft_tokens, draft_probs, uniforms, temperature, **kw)

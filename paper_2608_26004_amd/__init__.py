@@ -67,6 +67,9 @@ def load_library(path: str | None = None):
     lib.asymspec_fuse_verify.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, i32, i32, i32,
                                          ctypes.POINTER(_Params), vp, vp, vp, vp, vp, vp, sz, vp]
     lib.asymspec_fuse_verify.restype = i32
+    lib.asymspec_fuse_verify_xvocab.argtypes = [vp, vp, vp, i32, vp, i32, vp, vp, vp, vp, i32, i32, i32,
+                                                ctypes.POINTER(_Params), vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.asymspec_fuse_verify_xvocab.restype = i32
     lib.asymspec_status_string.argtypes = [i32]
     lib.asymspec_status_string.restype = ctypes.c_char_p
     lib.asymspec_version.argtypes = []
@@ -115,7 +118,7 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
                 beta: float = 1.0, gamma: float = 0.5, gate_mode: int = GATE_CDA,
                 return_gate: bool = False, workspace: Workspace | None = None, out=None,
                 delta_mode: int = DELTA_AB, lam: float = 0.1, fuse_bonus: bool = False,
-                return_full: bool = False):
+                return_full: bool = False, vocab_map=None):
     """One AsymSpec decision step on the current HIP stream.
 
     t, a, b: [B, K+1, V] torch.bfloat16 or torch.float32 on the GPU
@@ -125,7 +128,10 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     scale lam); delta_mode: DELTA_AB (the paper), DELTA_A or DELTA_TB;
     fuse_bonus: take the bonus token from f_K rather than t_K (FUSE_BONUS);
     return_full: also return every element's log-probability under its row's
-    distribution, [B, K+1, V] float32 (a second pass over the logits).
+    distribution, [B, K+1, V] float32 (a second pass over the logits);
+    vocab_map: for a drafter of another model family, [V] int32 on the GPU
+    (drafter id of each verifier token, -1 if not shared); a and b are then
+    [B, K+1, Vd] in the drafter's vocabulary.
     Returns (accept_len [B] int32, next_token [B] int32,
              fused_logprobs [B, K+1] float32[, gate [B, K, 2] float32]
              [, full [B, K+1, V] float32])."""
@@ -142,10 +148,18 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     B, Kp1, V = t.shape
     K = Kp1 - 1
     dev = t.device
+    Vd = V
+    if vocab_map is not None:
+        if vocab_map.dtype != torch.int32 or tuple(vocab_map.shape) != (V,) or vocab_map.device != dev:
+            raise ValueError("vocab_map must be int32 [V] on the logits' device")
+        if a.dim() != 3 or tuple(a.shape[:2]) != (B, Kp1):
+            raise ValueError("a must be [B, K+1, Vd]")
+        Vd = a.shape[2]
     for name, x in (("a", a), ("b", b)):
-        if x.shape != t.shape or x.dtype != t.dtype or x.device != dev:
-            raise ValueError(f"{name} must match t in shape, dtype and device")
-    for x in (t, a, b, draft_tokens, uniforms, temperature) + ((draft_probs,) if draft_probs is not None else ()):
+        if tuple(x.shape) != (B, Kp1, Vd) or x.dtype != t.dtype or x.device != dev:
+            raise ValueError(f"{name} must be [B, K+1, {Vd}] with t's dtype and device")
+    extra = (vocab_map,) if vocab_map is not None else ()
+    for x in (t, a, b, draft_tokens, uniforms, temperature) + extra + ((draft_probs,) if draft_probs is not None else ()):
         if not x.is_contiguous():
             raise ValueError("all tensors must be contiguous")
     if draft_tokens.dtype != torch.int32 or tuple(draft_tokens.shape) != (B, K):
@@ -173,11 +187,13 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     wsbuf = workspace.get(ws_bytes, dev)
     params = _Params(float(beta), float(gamma), int(gate_mode), FUSE_BONUS if fuse_bonus else 0,
                      int(delta_mode), float(lam))
-    st = lib.asymspec_fuse_verify(_ptr(t), _ptr(a), _ptr(b), dt, _ptr(draft_tokens),
-                                  _ptr(draft_probs), _ptr(uniforms), _ptr(temperature),
-                                  B, K, V, ctypes.byref(params), _ptr(acc), _ptr(nxt),
-                                  _ptr(flp), _ptr(gate), _ptr(full), _ptr(wsbuf), wsbuf.numel(),
-                                  _stream_handle(dev))
+    tail = (_ptr(draft_tokens), _ptr(draft_probs), _ptr(uniforms), _ptr(temperature),
+            B, K, V, ctypes.byref(params), _ptr(acc), _ptr(nxt), _ptr(flp), _ptr(gate), _ptr(full),
+            _ptr(wsbuf), wsbuf.numel(), _stream_handle(dev))
+    if vocab_map is None:
+        st = lib.asymspec_fuse_verify(_ptr(t), _ptr(a), _ptr(b), dt, *tail)
+    else:
+        st = lib.asymspec_fuse_verify_xvocab(_ptr(t), _ptr(a), _ptr(b), dt, _ptr(vocab_map), Vd, *tail)
     if st != OK:
         raise AsymSpecError(st, status_string(st))
     res = (acc, nxt, flp)

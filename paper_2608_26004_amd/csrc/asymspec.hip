@@ -43,8 +43,7 @@
 namespace asym {
 
 template <int DT, bool kB1, int DM>
-DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
-  const int i = sub / A.S, m = sub - (sub / A.S) * A.S;
+DEV void stats_chunk(const KArgs& A, int req, int i, int m, Smem& sm) {
   const int row = req * (A.K + 1) + i;
   const float tau = sload_f32(A.tau, req);
   if (i == A.K) {
@@ -63,6 +62,18 @@ DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
   } else {
     stats_item<DT, kSampleDraftT, kB1, DM>(A, row, m, sm);
   }
+}
+
+// Workgroups go to the 8 XCDs in turn, so consecutive items of a request
+// sit on different XCDs.  Through a vocabulary map every chunk of a row
+// gathers from the whole of the row's drafter logits; the items of a request
+// are then renumbered so that those sharing an XCD take consecutive chunks
+// of the same rows, and each XCD's L2 holds few drafter rows at a time.
+template <int DT, bool kB1, int DM>
+DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
+  const int p = A.vmap != nullptr ? xcd_grouped(sub, (A.K + 1) * A.S) : sub;
+  const int i = p / A.S, m = p - i * A.S;
+  stats_chunk<DT, kB1, DM>(A, req, i, m, sm);
 }
 
 #ifndef ASYMSPEC_WAVES
@@ -228,13 +239,14 @@ int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stre
   return hipGetLastError() == hipSuccess ? ASYMSPEC_OK : ASYMSPEC_E_DEVICE;
 }
 
-int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
-                         const int32_t* draft_tokens, const float* draft_probs,
-                         const float* uniforms, const float* temperature,
-                         int B, int K, int V, const asymspec_params* params,
-                         int32_t* accept_len, int32_t* next_token, float* fused_logprobs,
-                         float* gate_out, float* fused_logprobs_full, void* workspace,
-                         size_t workspace_bytes, void* stream) {
+// Both entry points: vmap == nullptr for one shared vocabulary, else a and b
+// are [B][K+1][Vd] drafter rows reached through vmap.
+static int fuse_verify_impl(const void* t, const void* a, const void* b, int dtype, const int32_t* vmap,
+                            int Vd, const int32_t* draft_tokens, const float* draft_probs,
+                            const float* uniforms, const float* temperature, int B, int K, int V,
+                            const asymspec_params* params, int32_t* accept_len, int32_t* next_token,
+                            float* fused_logprobs, float* gate_out, float* fused_logprobs_full,
+                            void* workspace, size_t workspace_bytes, void* stream) {
   Layout L;
   if (params == nullptr) return ASYMSPEC_E_ARG;
   if (!make_layout(B, K, V, dtype, L)) return ASYMSPEC_E_ARG;
@@ -250,7 +262,14 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   if (params->delta_mode < ASYMSPEC_DELTA_AB || params->delta_mode > ASYMSPEC_DELTA_TB) return ASYMSPEC_E_ARG;
   if (params->gate_mode == ASYMSPEC_GATE_LAMBDA && !std::isfinite(params->lambda)) return ASYMSPEC_E_ARG;
   if ((params->flags & ~(uint32_t)ASYMSPEC_FUSE_BONUS) != 0u) return ASYMSPEC_E_ARG;
-  if (!aligned(t, 16) || ((K > 0 || fb) && (!aligned(a, 16) || !aligned(b, 16)))) return ASYMSPEC_E_ALIGN;
+  if (vmap != nullptr) {
+    // drafter rows are read element by element through the map
+    if (Vd < 1 || (unsigned long long)B * (K + 1) * (unsigned long long)Vd >= (1ull << 40)) return ASYMSPEC_E_ARG;
+    if (!aligned(vmap, 4) || ((K > 0 || fb) && (!aligned(a, 4) || !aligned(b, 4)))) return ASYMSPEC_E_ALIGN;
+    if (!aligned(t, 16)) return ASYMSPEC_E_ALIGN;
+  } else if (!aligned(t, 16) || ((K > 0 || fb) && (!aligned(a, 16) || !aligned(b, 16)))) {
+    return ASYMSPEC_E_ALIGN;
+  }
   if (!aligned(uniforms, 4) || !aligned(temperature, 4) || !aligned(accept_len, 4) ||
       !aligned(next_token, 4) || !aligned(fused_logprobs, 4) ||
       (draft_tokens && !aligned(draft_tokens, 4)) || (draft_probs && !aligned(draft_probs, 4)) ||
@@ -278,6 +297,8 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
   A.want_gate = gate_out != nullptr;
   A.delta_mode = params->delta_mode;
   A.fuse_bonus = fb ? 1 : 0;
+  A.vmap = vmap;
+  A.Vd = vmap != nullptr ? Vd : V;
   A.lam = params->gate_mode == ASYMSPEC_GATE_LAMBDA ? params->lambda : 0.0f;
   A.ln_gamma = std::log((double)params->gamma);
   A.epoch = next_epoch();
@@ -302,6 +323,32 @@ int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
     return ASYMSPEC_E_DEVICE;
   }
   return ASYMSPEC_OK;
+}
+
+int asymspec_fuse_verify(const void* t, const void* a, const void* b, int dtype,
+                         const int32_t* draft_tokens, const float* draft_probs,
+                         const float* uniforms, const float* temperature,
+                         int B, int K, int V, const asymspec_params* params,
+                         int32_t* accept_len, int32_t* next_token, float* fused_logprobs,
+                         float* gate_out, float* fused_logprobs_full, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  return fuse_verify_impl(t, a, b, dtype, nullptr, 0, draft_tokens, draft_probs, uniforms, temperature, B, K, V,
+                          params, accept_len, next_token, fused_logprobs, gate_out, fused_logprobs_full,
+                          workspace, workspace_bytes, stream);
+}
+
+int asymspec_fuse_verify_xvocab(const void* t, const void* a, const void* b, int dtype,
+                                const int32_t* vocab_map, int Vd, const int32_t* draft_tokens,
+                                const float* draft_probs, const float* uniforms,
+                                const float* temperature, int B, int K, int V,
+                                const asymspec_params* params, int32_t* accept_len,
+                                int32_t* next_token, float* fused_logprobs, float* gate_out,
+                                float* fused_logprobs_full, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  if (vocab_map == nullptr) return ASYMSPEC_E_ARG;
+  return fuse_verify_impl(t, a, b, dtype, vocab_map, Vd, draft_tokens, draft_probs, uniforms, temperature, B, K,
+                          V, params, accept_len, next_token, fused_logprobs, gate_out, fused_logprobs_full,
+                          workspace, workspace_bytes, stream);
 }
 
 const char* asymspec_status_string(int status) {

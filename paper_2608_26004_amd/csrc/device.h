@@ -106,6 +106,11 @@ struct KArgs {
   int delta_mode;     // source of delta in f = t + beta * delta
   int fuse_bonus;     // the bonus row emits from f rather than t
   float lam;          // scale of the lambda gate
+  // cross-family vocabularies: a and b are [B][K+1][Vd] in the drafter's
+  // vocabulary and vmap[x] is the drafter id of verifier token x (or < 0 /
+  // >= Vd: not shared); null when both sides share one vocabulary
+  const int32_t* vmap;
+  int Vd;
   double ln_gamma;
   uint32_t epoch;
   Sched sc;
@@ -446,7 +451,7 @@ DEV float jsd_elem(float a, float b, const JsdConst& k) {
   const float g = 1.0f - __builtin_amdgcn_logf(fmaxf(P + Q, 1e-37f));
   return __builtin_fmaf(P, lp + g, Q * (lq + g));
 }
-// KL term P log2(P/Q) of KL(softmax(a) || softmax(b)) (the gate of App. C),
+// KL term P log2(P/Q) of KL(softmax(a) || softmax(b)) (the gate of App. G),
 // 0 where P = 0.
 DEV float kl_elem(float a, float b, const JsdConst& k) {
   const float lp = (fmaxf(__builtin_fmaf(a, kL2E, -k.Ra), kFloorM) - k.kahi) - k.kalo;
@@ -528,6 +533,9 @@ DEV __amdgpu_buffer_rsrc_t row_rsrc(const KArgs& A, const void* base, const RowG
   unsigned long long span = (unsigned long long)(g.vend - g.vbeg) * 16ull;
   const unsigned long long rem = A.stream_bytes - rbase;
   if (span > rem) span = rem;
+  // drafter rows of another vocabulary are reached through the map only:
+  // a resource over them reads zeros and touches no memory
+  if (A.vmap != nullptr && base != A.t) span = 0;
   return make_rsrc((const char*)base + rbase, span);
 }
 
@@ -557,6 +565,7 @@ template <int DT>
 DEV void fix_vec(const KArgs& A, const RowGeo& g, const void* src, long long vi, u4& v) {
   constexpr int VE = Elem<DT>::VE;
   constexpr int ES = 16 / VE;
+  if (A.vmap != nullptr && src != A.t) return;   // drafter rows: map_vecs
   const long long last_full = (long long)(A.stream_bytes / 16ull);
   if (vi >= last_full && vi < g.vend) {
     const long long n_el = (long long)(A.stream_bytes / ES);
@@ -576,6 +585,55 @@ DEV void fix_vec(const KArgs& A, const RowGeo& g, const void* src, long long vi,
     const int ihi = (int)(hi < 0 ? 0 : (hi > VE ? VE : hi));
     Elem<DT>::mask_to_neginf(v, ilo, ihi);
   }
+}
+
+// Cross-family vocabularies (the alignment of App. "Cross-family
+// portability"): the drafter logits of verifier token x are a[vmap[x]] and
+// b[vmap[x]]; a verifier token without a shared counterpart cannot be
+// committed, so it counts as masked in every view (t = a = b = -inf).
+DEV int map_id(const KArgs& A, long long x) {
+  if (x < 0 || x >= A.V) return -1;
+  const int j = A.vmap[x];
+  return (j >= 0 && j < A.Vd) ? j : -1;
+}
+// The vector vi of row g in the verifier's layout: vt (loaded and repaired)
+// gets -inf where the token is not shared, and, when ab, va and vb are
+// gathered from the drafter rows through the map (-inf where not shared).
+template <int DT>
+DEV void map_vecs(const KArgs& A, const RowGeo& g, long long vi, u4& vt, u4& va, u4& vb, bool ab) {
+  constexpr int VE = Elem<DT>::VE;
+  u4 t2 = {0, 0, 0, 0}, a2 = t2, b2 = t2;
+  const long long dbase = (long long)g.row * A.Vd;
+  #pragma unroll
+  for (int e = 0; e < VE; ++e) {
+    const int j = map_id(A, vi * VE + e - g.e0);
+    float xt = -INFINITY, xa = -INFINITY, xb = -INFINITY;
+    if (j >= 0) {
+      xt = Elem<DT>::get(vt, e);
+      if (ab) {
+        xa = Elem<DT>::load_one(A.a, dbase + j);
+        xb = Elem<DT>::load_one(A.b, dbase + j);
+      }
+    }
+    Elem<DT>::put_one(t2, e, xt);
+    Elem<DT>::put_one(a2, e, xa);
+    Elem<DT>::put_one(b2, e, xb);
+  }
+  vt = t2;
+  if (ab) { va = a2; vb = b2; }
+}
+// The three logits of verifier token x (0 <= x < V) of row g, mapped.
+template <int DT>
+DEV void mapped_tab(const KArgs& A, const RowGeo& g, int x, float& t, float& a, float& b) {
+  const int j = A.vmap != nullptr ? map_id(A, x) : ((x >= 0 && x < A.V) ? x : -1);
+  if (j < 0) {
+    t = a = b = -INFINITY;
+    return;
+  }
+  t = Elem<DT>::load_one(A.t, g.e0 + x);
+  const long long d = A.vmap != nullptr ? (long long)g.row * A.Vd + j : g.e0 + x;
+  a = Elem<DT>::load_one(A.a, d);
+  b = Elem<DT>::load_one(A.b, d);
 }
 
 // Draft-token gathers of one row through the scalar cache (wave-uniform
@@ -600,9 +658,22 @@ DEV Gather sgather(const KArgs& A, const RowGeo& g) {
     int dtok = (int)((cptr32)(const void*)A.d)[g.req * A.K + g.pos];
     dtok = dtok < 0 ? 0 : (dtok >= A.V ? A.V - 1 : dtok);
     const long long idx = g.e0 + dtok;
-    q.t = sload_elem<DT>(A.t, idx);
-    q.a = sload_elem<DT>(A.a, idx);
-    q.b = sload_elem<DT>(A.b, idx);
+    if (A.vmap != nullptr) {
+      // a draft outside the shared set has no mass in any view
+      const int j = ((cptr32)(const void*)A.vmap)[dtok];
+      if (j >= 0 && j < A.Vd) {
+        const long long di = (long long)g.row * A.Vd + j;
+        q.t = sload_elem<DT>(A.t, idx);
+        q.a = sload_elem<DT>(A.a, di);
+        q.b = sload_elem<DT>(A.b, di);
+      } else {
+        q.t = q.a = q.b = -INFINITY;
+      }
+    } else {
+      q.t = sload_elem<DT>(A.t, idx);
+      q.a = sload_elem<DT>(A.a, idx);
+      q.b = sload_elem<DT>(A.b, idx);
+    }
     if (A.dp != nullptr) q.p = sload_f32(A.dp, (long long)g.req * A.K + g.pos);
     q.u = sload_f32(A.u, (long long)g.req * (A.K + 1) + g.pos);
   }

@@ -60,11 +60,14 @@ __global__ __launch_bounds__(kThreads) void dump_kernel(KArgs A, float* out) {
     if (vi >= g.vend) break;
     const uint32_t off = (uint32_t)(rel * 16);
     u4 vt = buf_load_nt(rt, off), va = vt, vb = vt;
-    if (fused) {
+    if (A.vmap != nullptr) {
+      fix_vec<DT>(A, g, A.t, vi, vt);
+      map_vecs<DT>(A, g, vi, vt, va, vb, fused);
+    } else if (fused) {
       va = buf_load_nt(ra, off);
       vb = nb ? buf_load_nt(rb, off) : va;
     }
-    if (tail) {
+    if (tail && A.vmap == nullptr) {
       fix_vec<DT>(A, g, A.t, vi, vt);
       if (fused) {
         fix_vec<DT>(A, g, A.a, vi, va);

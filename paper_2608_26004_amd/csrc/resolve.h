@@ -444,7 +444,9 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bo
         if (kNb) mask_vec<DT>(A, g, vi, vb[k]);
       } else if (kMode == 2) {
         if (nt) fix_vec<DT>(A, g, A.t, vi, vt[k]);
-        if (nab) {
+        if (A.vmap != nullptr) {
+          map_vecs<DT>(A, g, vi, vt[k], va[k], vb[k], nab);
+        } else if (nab) {
           fix_vec<DT>(A, g, A.a, vi, va[k]);
           if (kNb) fix_vec<DT>(A, g, A.b, vi, vb[k]);
         }
@@ -473,7 +475,7 @@ DEV void pass2_sums_any(const KArgs& A, const RowGeo& g, long long rel0, long lo
                         bool dj, bool dr, bool db, const ResidConst& rk, const JsdConst& jk, float& accj,
                         float& seg) {
   constexpr int VE = Elem<DT>::VE;
-  if (has_tail(A, c0, c1))
+  if (A.vmap != nullptr || has_tail(A, c0, c1))
     pass2_sums<DT, 2, DM, kKL, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
   else if (c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
     pass2_sums<DT, 0, DM, kKL, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
@@ -503,7 +505,7 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
       // a row with a == b bitwise has no divergence task and skips b
       if (dj && A.gate_mode == ASYMSPEC_GATE_KL)
         pass2_sums_any<DT, DM, true, true>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
-      else if ((cst[D_STATUS] & kStNeq) != 0u)
+      else if ((cst[D_STATUS] & kStNeq) != 0u || A.vmap != nullptr)
         pass2_sums_any<DT, DM, false, true>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
       else
         pass2_sums_any<DT, DM, false, false>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
@@ -636,7 +638,11 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
     vt[k] = buf_load(rt, off);
     va[k] = bonus ? vt[k] : buf_load(ra, off);
     vb[k] = nb ? buf_load(rb, off) : u4{0, 0, 0, 0};
-    if (tail) {
+    if (A.vmap != nullptr) {
+      fix_vec<DT>(A, g, A.t, vi, vt[k]);
+      map_vecs<DT>(A, g, vi, vt[k], va[k], vb[k], !bonus);
+      if (bonus) va[k] = vt[k];
+    } else if (tail) {
       fix_vec<DT>(A, g, A.t, vi, vt[k]);
       if (!bonus) fix_vec<DT>(A, g, A.a, vi, va[k]);
       if (nb) fix_vec<DT>(A, g, A.b, vi, vb[k]);
@@ -695,9 +701,9 @@ DEV int row_argmax_f(const KArgs& A, const RowGeo& g, Smem& sm) {
   float best = kFloorM;
   int bi = 0x7FFFFFFF;
   for (int x = wave_id() * 64 + lane_id(); x < A.V; x += kThreads) {
-    const long long idx = g.e0 + x;
-    const float f = fuse_rt(Elem<DT>::load_one(A.t, idx), Elem<DT>::load_one(A.a, idx),
-                            Elem<DT>::load_one(A.b, idx), A.beta, A.delta_mode);
+    float xt, xa, xb;
+    mapped_tab<DT>(A, g, x, xt, xa, xb);
+    const float f = fuse_rt(xt, xa, xb, A.beta, A.delta_mode);
     if (f > best) { best = f; bi = x; }
   }
   const float M = wave_max(best);
@@ -707,7 +713,8 @@ DEV int row_argmax_f(const KArgs& A, const RowGeo& g, Smem& sm) {
   float Mb = sm.wj[0];
   #pragma unroll
   for (int q = 1; q < kWaves; ++q) Mb = fmaxf(Mb, sm.wj[q]);
-  return block_min_i(best == Mb ? bi : 0x7FFFFFFF, sm);
+  const int r = block_min_i(best == Mb ? bi : 0x7FFFFFFF, sm);
+  return r == 0x7FFFFFFF ? 0 : r;   // a row with no finite f: token 0, as argmax of all -inf
 }
 
 template <int DT, int DM>
@@ -776,9 +783,9 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
     if (have_x) {
       x = (float)sm.dd[3];
     } else {
-      const long long idx = g.e0 + next;
-      x = Elem<DT>::load_one(A.t, idx);
-      if (!bonus) x = fuse_masked(x, Elem<DT>::load_one(A.a, idx), Elem<DT>::load_one(A.b, idx), A.beta, A.delta_mode);
+      float xa, xb;
+      mapped_tab<DT>(A, g, next, x, xa, xb);
+      if (!bonus) x = fuse_masked(x, xa, xb, A.beta, A.delta_mode);
     }
     const double c = (double)__uint_as_float(sm.rows[j][D_C]);
     const double l2 = u2d(sm.rows[j][D_L2E_LO], sm.rows[j][D_L2E_HI]);

@@ -152,6 +152,17 @@ ASYM_HD inline Item sched_item(const Sched& sc, int K, int S, int idx) {
   return it;
 }
 
+// Renumbering of the n consecutive items of one block so that items 8 apart
+// (which the hardware sends to the same XCD) take consecutive positions:
+// position = (items of the block in lower residue classes mod 8) + sub / 8.
+// A bijection on [0, n).
+ASYM_HD inline int xcd_grouped(int sub, int n) {
+  const int r = sub & 7;
+  int before = 0;
+  for (int c = 0; c < r; ++c) before += (n - c + 7) >> 3;
+  return before + (sub >> 3);
+}
+
 }  // namespace asym
 
 #endif  // ASYMSPEC_SCHEDULE_H_

@@ -116,7 +116,9 @@ DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, c
         u4 vt = buf_load(row_rsrc(A, A.t, g), off);
         fix_vec<DT>(A, g, A.t, vi, vt);
         u4 va = vt, vb = vt;
-        if (kDraft) {
+        if (A.vmap != nullptr) {
+          map_vecs<DT>(A, g, vi, vt, va, vb, kDraft);
+        } else if (kDraft) {
           va = buf_load(row_rsrc(A, A.a, g), off);
           vb = buf_load(row_rsrc(A, A.b, g), off);
           fix_vec<DT>(A, g, A.a, vi, va);
@@ -220,7 +222,8 @@ DEV void stats_init(StatsAcc& q, float c) {
 
 // Generic path: one vector at a time, every vector repaired (row boundary,
 // array end), NaN-safe exponent for f.  Used for the chunk that holds a
-// ragged array end and to redo a chunk whose f sum came out NaN.
+// ragged array end, to redo a chunk whose f sum came out NaN, and for every
+// chunk when the drafter rows are reached through a vocabulary map.
 template <int DT, int KIND, bool kB1, int DM>
 DEV void stats_slow(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   using TR = KindTraits<KIND>;
@@ -239,7 +242,9 @@ DEV void stats_slow(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
     const long long vi = g.vbeg + rv;
     u4 vt = buf_load(rt, off), va = vt, vb = vt;
     fix_vec<DT>(A, g, A.t, vi, vt);
-    if (kDraft) {
+    if (A.vmap != nullptr) {
+      map_vecs<DT>(A, g, vi, vt, va, vb, kDraft);
+    } else if (kDraft) {
       va = buf_load(ra, off);
       vb = buf_load(rb, off);
       fix_vec<DT>(A, g, A.a, vi, va);
@@ -314,7 +319,7 @@ DEV void stats_item(const KArgs& A, int row, int m, Smem& sm) {
   const RowGeo g = row_geo<DT>(A, row);
   const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
   bool done = false;
-  if (!has_tail(A, c0, c1)) {
+  if (A.vmap == nullptr && !has_tail(A, c0, c1)) {
     // a chunk whose vectors lie wholly inside the row needs no masking
     const bool interior = c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V;
     done = interior ? stats_fast<DT, KIND, kB1, DM, false>(A, g, m, sm)

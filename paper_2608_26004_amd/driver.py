@@ -5,7 +5,7 @@ K tokens autoregressively from its full-context view, the three logit rows of
 every position are produced (drafter full view a, drafter compressed view b,
 verifier t; Alg. 1 runs the three forwards), ``fuse_verify`` decides, and the
 accepted drafts plus the emitted token are committed.  It reports the two
-acceptance diagnostics of the paper's acceptance table (App. C):
+acceptance diagnostics of the paper's acceptance table (App. F):
 
   AR   accepted drafts / drafts evaluated, where the drafts evaluated in a
        step are the accepted ones plus the first rejected one (Alg. 1 stops

@@ -290,3 +290,31 @@ def replicate_for_mc(t_rows: np.ndarray, a_rows: np.ndarray, b_rows: np.ndarray,
     b = np.broadcast_to(b_rows, (n, Kp1, V)).copy()
     temperature = np.full(n, tau, np.float32)
     return t, a, b, drafts, dprobs, uniforms, temperature
+
+
+def cross_vocab(inp: Inputs, Vd: int, n_shared: int, seed: int = 0):
+    """A drafter of another model family for `inp` (App. D's setting):
+    drafter rows over a vocabulary of Vd tokens that hold inp.a / inp.b at
+    the drafter ids of n_shared verifier tokens (both chosen at random, a
+    stand-in for the string-identical tokens of two tokenizers), the other
+    drafter tokens filled with N(0, 3^2) noise, and the map [V] int32 (drafter
+    id of each verifier token, -1 for the unshared ones).  Drafts that fall
+    outside the shared set are moved to a shared token of the same request
+    (the drafter commits shared tokens only).  Returns (a_d, b_d, vocab_map,
+    draft_tokens)."""
+    rng = np.random.default_rng(seed)
+    B, Kp1, V = inp.t.shape
+    n = min(V, Vd, n_shared)
+    xs = np.sort(rng.choice(V, n, replace=False))
+    vm = np.full(V, -1, np.int32)
+    vm[xs] = rng.choice(Vd, n, replace=False).astype(np.int32)
+    def noise():
+        x = rng.normal(0.0, 3.0, (B, Kp1, Vd))
+        return f64_to_bf16_bits(x) if inp.dtype == BF16 else x.astype(np.float32)
+    ad, bd = noise(), noise()
+    ad[..., vm[xs]] = inp.a[..., xs]
+    bd[..., vm[xs]] = inp.b[..., xs]
+    d = inp.draft_tokens.copy()
+    bad = vm[d] < 0
+    d[bad] = xs[rng.integers(0, n, int(bad.sum()))]
+    return ad, bd, vm, d

@@ -29,10 +29,16 @@ def to_device(x, device="cuda"):
 
 
 def run_gpu(inp, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True, want_gate=True,
-            device="cuda", delta_mode=0, lam=0.1, fuse_bonus=False, want_full=False):
+            device="cuda", delta_mode=0, lam=0.1, fuse_bonus=False, want_full=False, vocab=None):
+    """vocab = (a_d, b_d, vocab_map): drafter rows in another vocabulary,
+    passed in place of inp.a and inp.b."""
     import torch
     import paper_2608_26004_amd as asp
     t, a, b = (to_device(x, device) for x in (inp.t, inp.a, inp.b))
+    vm = None
+    if vocab is not None:
+        a, b = (to_device(x, device) for x in vocab[:2])
+        vm = to_device(np.asarray(vocab[2], np.int32), device)
     d = to_device(inp.draft_tokens.astype(np.int32), device)
     q = to_device(inp.draft_probs.astype(np.float32), device) if with_probs else None
     u = to_device(inp.uniforms.astype(np.float32), device)
@@ -40,7 +46,7 @@ def run_gpu(inp, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True, want_gate=Tr
     out = asp.fuse_verify(t, a, b, d, q, u, tau, beta=beta, gamma=gamma,
                           gate_mode=gate_mode, return_gate=want_gate,
                           delta_mode=delta_mode, lam=lam, fuse_bonus=fuse_bonus,
-                          return_full=want_full)
+                          return_full=want_full, vocab_map=vm)
     torch.cuda.synchronize()
     res = [x.cpu().numpy() for x in out]
     if not want_gate:
@@ -70,7 +76,8 @@ def compare(inp, gpu, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True,
                                            int(acc_o[k]), int(nxt_o[k])))
         hi = K + 1 if same else K
         if hi > 0:
-            d = np.abs(flp_g[bi, :hi].astype(np.float64) - flp_o[k, :hi])
+            with np.errstate(invalid="ignore"):     # -inf - -inf where both are masked
+                d = np.abs(flp_g[bi, :hi].astype(np.float64) - flp_o[k, :hi])
             finite = np.isfinite(flp_o[k, :hi])
             if np.any(finite != np.isfinite(flp_g[bi, :hi])):
                 bad.append((bi, "non-finite mismatch", flp_g[bi, :hi].tolist(), flp_o[k, :hi].tolist()))
@@ -109,3 +116,38 @@ def compare_full(inp, full_g, beta=1.0, delta_mode=0, fuse_bonus=False, requests
     err = float(np.abs(g[fin_o] - full_o[fin_o]).max()) if fin_o.any() else 0.0
     assert err <= LP_TOL, f"{label}: full log-prob error {err}"
     return err
+
+
+def make_xvocab(inp, Vd, shared_frac, seed, unshared_drafts=False):
+    """A cross-family version of `inp`: drafter rows in a vocabulary of Vd
+    tokens holding inp.a / inp.b at the drafter ids of the shared verifier
+    tokens (a random injection), drafter-only tokens filled with noise, and
+    the map.  Returns (a_d, b_d, vocab_map, mapped) where `mapped` is `inp`
+    with the rows the oracle sees (``map_to_verifier``)."""
+    import copy
+    rng = np.random.default_rng(seed)
+    B, Kp1, V = inp.t.shape
+    n_sh = min(V, Vd, max(1, int(round(shared_frac * V))))
+    xs = np.sort(rng.choice(V, n_sh, replace=False))
+    vm = np.full(V, -1, np.int32)
+    vm[xs] = rng.choice(Vd, n_sh, replace=False)
+    if inp.a.dtype == np.uint16:
+        noise = lambda: f64_bits(rng.normal(0, 3, (B, Kp1, Vd)))
+    else:
+        noise = lambda: rng.normal(0, 3, (B, Kp1, Vd)).astype(np.float32)
+    ad, bd = noise(), noise()
+    ad[..., vm[xs]] = inp.a[..., xs]
+    bd[..., vm[xs]] = inp.b[..., xs]
+    mapped = copy.copy(inp)
+    if not unshared_drafts and inp.K > 0:
+        d = inp.draft_tokens.copy()
+        bad = vm[d] < 0
+        d[bad] = xs[rng.integers(0, n_sh, bad.sum())]
+        mapped.draft_tokens = d
+    mapped.t, mapped.a, mapped.b = O.map_to_verifier(inp.t, ad, bd, vm)
+    return ad, bd, vm, mapped
+
+
+def f64_bits(x):
+    from paper_2608_26004_amd import synth
+    return synth.f64_to_bf16_bits(x)

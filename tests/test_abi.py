@@ -116,3 +116,41 @@ def test_k0_allows_missing_drafter_arrays():
         pytest.skip("host-only check")
     st = _call(K=0, a=None, b=None, d=None)
     assert st in (asp.OK, asp.E_DEVICE)
+
+
+def _call_xv(**over):
+    lib = asp.load_library()
+    fake = 1 << 20
+    kw = dict(t=fake, a=fake, b=fake, dtype=0, vm=fake, Vd=50, d=fake, dp=None, u=fake, tau=fake,
+              B=2, K=2, V=64, acc=fake, nxt=fake, flp=fake, gate=None, full=None, ws=fake, wsb=None)
+    kw.update(over)
+    if kw["wsb"] is None:
+        kw["wsb"] = asp.workspace_size(max(kw["B"], 1), max(kw["K"], 0), max(kw["V"], 1), 0) or 1 << 20
+    p = asp._Params(1.0, 0.5, 0, 0, 0, 0.1)
+    return lib.asymspec_fuse_verify_xvocab(kw["t"], kw["a"], kw["b"], kw["dtype"], kw["vm"], kw["Vd"],
+                                           kw["d"], kw["dp"], kw["u"], kw["tau"], kw["B"], kw["K"], kw["V"],
+                                           ctypes.byref(p), kw["acc"], kw["nxt"], kw["flp"], kw["gate"],
+                                           kw["full"], kw["ws"], kw["wsb"], None)
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(vm=None), asp.E_ARG),
+    (dict(Vd=0), asp.E_ARG),
+    (dict(Vd=-3), asp.E_ARG),
+    (dict(B=1 << 20, K=62, Vd=1 << 20, V=8), asp.E_ARG),     # B (K+1) Vd >= 2^40
+    (dict(a=None), asp.E_ARG),
+    (dict(vm=(1 << 20) + 2), asp.E_ALIGN),
+    (dict(a=(1 << 20) + 2), asp.E_ALIGN),
+    (dict(t=(1 << 20) + 4), asp.E_ALIGN),
+])
+def test_xvocab_invalid_arguments_rejected_on_host(over, code):
+    assert _call_xv(**over) == code
+
+
+def test_xvocab_drafter_rows_need_only_element_alignment():
+    # 4-byte aligned drafter rows pass validation (they are gathered element
+    # by element); without a GPU the call then fails at the device stage
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("host-only check")
+    assert _call_xv(a=(1 << 20) + 4, b=(1 << 20) + 8) in (asp.OK, asp.E_DEVICE)

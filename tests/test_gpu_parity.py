@@ -131,7 +131,7 @@ def test_workload_4_sampled(gpu):
 
 
 # --------------------------------------------- gate and fusion variants --
-# App. B (fixed and tuned-lambda gates), App. C (KL gate), Sec. 5 ablation
+# App. B (fixed and tuned-lambda gates), App. G (KL gate), Sec. 6.2 ablation
 # (delta = a, delta = t - b), each against the oracle.
 VARIANTS = [(2, 0), (3, 0), (0, 1), (0, 2), (2, 2), (3, 1), (1, 2)]
 
@@ -283,3 +283,56 @@ def test_full_logprobs_workload_1(gpu):
     g = run_gpu(x, want_full=True)
     err = compare_full(x, g[4], requests=[0, 3, 7], label="full workload 1")
     print(f"[full] workload 1: max abs err {err:.2e}")
+
+
+# ------------------------------------------- cross-family vocabularies --
+# Sec. 6.4 / App. D: the drafter in its own vocabulary, reached through the
+# map; the oracle sees the rows carried into the verifier's vocabulary.
+def _run_xv(x, Vd, frac, seed, **kw):
+    from parity_util import make_xvocab
+    ad, bd, vm, mx = make_xvocab(x, Vd, frac, seed, unshared_drafts=kw.pop("unshared_drafts", False))
+    g = run_gpu(mx, vocab=(ad, bd, vm), **kw)
+    return g, mx
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("tau", [0.0, 1.0, 0.7])
+@pytest.mark.parametrize("Vd,frac", [(4000, 0.7), (7000, 0.95), (5000, 1.0)])
+def test_xvocab_small(gpu, dtype, tau, Vd, frac):
+    x = synth.generate(B=5, K=3, V=5000, dtype=dtype, rho=("alternate", 0.0, 2.0), tau=tau,
+                       seed=500 + Vd % 97)
+    g, mx = _run_xv(x, Vd, frac, seed=Vd, want_full=True)
+    _note(compare(mx, g, label=f"xvocab {dtype} tau={tau} Vd={Vd} frac={frac}"))
+    compare_full(mx, g[4], label=f"xvocab full {dtype} tau={tau}")
+    vm = np.asarray(_xv_map(mx))
+    assert (vm[g[1]] >= 0).all()          # commits stay in the shared set
+
+
+def _xv_map(mx):
+    # the shared set as the oracle sees it: finite somewhere in t'
+    fin = np.isfinite(synth.stored_to_f64(mx.t)).any(axis=(0, 1))
+    return np.where(fin, 0, -1)
+
+
+@pytest.mark.parametrize("gate,delta,fb", [(0, 0, True), (2, 0, False), (3, 2, False), (1, 1, True)])
+def test_xvocab_variants(gpu, gate, delta, fb):
+    x = synth.generate(B=6, K=2, V=3001, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=600 + gate)
+    g, mx = _run_xv(x, 2500, 0.6, seed=gate, gate_mode=gate, delta_mode=delta, fuse_bonus=fb)
+    _note(compare(mx, g, gate_mode=gate, delta_mode=delta, fuse_bonus=fb,
+                  label=f"xvocab g={gate} d={delta} fb={fb}"))
+
+
+@pytest.mark.parametrize("V,K,Vd", [(1, 1, 3), (7, 0, 5), (4097, 2, 300), (8193, 1, 9000)])
+def test_xvocab_edges(gpu, V, K, Vd):
+    x = synth.generate(B=3, K=K, V=V, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=V + Vd)
+    g, mx = _run_xv(x, Vd, 0.8, seed=K, unshared_drafts=True, fuse_bonus=True, want_full=True)
+    _note(compare(mx, g, fuse_bonus=True, label=f"xvocab edge V={V} K={K} Vd={Vd}"))
+    compare_full(mx, g[4], fuse_bonus=True, label=f"xvocab edge full V={V}")
+
+
+def test_xvocab_workload_1(gpu):
+    x = synth.workload_inputs(1)
+    g, mx = _run_xv(x, 120000, 0.85, seed=3)
+    _note(compare(mx, g, label="xvocab workload 1"))

@@ -349,8 +349,8 @@ def test_draft_probs_given_or_computed_agree():
 
 
 # ------------------------------------------- gate and fusion variants --
-# App. B (fixed and tuned-lambda gates), App. C (KL in place of the JSD),
-# Sec. 5 mechanism ablation (delta = a and delta = t - b).
+# App. B (fixed and tuned-lambda gates), App. G (KL in place of the JSD),
+# Sec. 6.2 mechanism ablation (delta = a and delta = t - b).
 
 def test_kl_matches_scipy_rel_entr():
     """KL(softmax(a) || softmax(b)) in natural log, against scipy."""
@@ -401,7 +401,7 @@ def test_log_ratio_at_draft_token():
 
 
 def test_worked_example_kl_and_lambda_gates():
-    """App. B/C gates on the two-token example of tests/golden: the KL gate
+    """App. B and G gates on the two-token example of tests/golden: the KL gate
     accepts like CDA, the lambda gate (Delta < 0 raises gamma_eff above
     gamma) rejects like the fixed gate."""
     g = json.load(open(os.path.join(GOLDEN, "worked_example_v2.json")))
@@ -440,7 +440,7 @@ def _lognorm(x):
 
 
 def test_delta_modes_as_products_of_experts():
-    """Sec. 5 ablation sources, by shift invariance of softmax: the fused
+    """Sec. 6.2 ablation sources, by shift invariance of softmax: the fused
     distribution is p_t p_a^beta / p_b^beta (ours), p_t p_a^beta
     (raw-augmented) and p_t^(1+beta) / p_b^beta (SCD-style), up to the fp32
     rounding of f."""
@@ -558,3 +558,77 @@ def test_full_logprobs_masked_tokens():
     assert full[0, 0, 1] == -np.inf
     np.testing.assert_allclose(full[0, 0, [0, 2, 3, 4]], np.log(0.25), atol=1e-15)
     np.testing.assert_allclose(full[0, 1], np.log(0.2), atol=1e-15)
+
+
+# ------------------------------------------- cross-family vocabularies --
+def _xv_problem(rng, B=3, K=3, V=60, tau=(0.0, 1.0, 0.7)):
+    t = rng.normal(0, 2, (B, K + 1, V)).astype(np.float32)
+    a = (t * 0.5 + rng.normal(0, 2, (B, K + 1, V))).astype(np.float32)
+    b = (a + rng.normal(0, 1, (B, K + 1, V))).astype(np.float32)
+    d = rng.integers(0, V, (B, K)).astype(np.int32)
+    u = rng.random((B, K + 1)).astype(np.float32)
+    return t, a, b, d, u, np.array(tau[:B], np.float32)
+
+
+def _same(r0, r1):
+    for x, y in zip(r0[:4], r1[:4]):
+        assert np.array_equal(x, y, equal_nan=True)
+
+
+def test_xvocab_identity_map_is_the_plain_step():
+    rng = np.random.default_rng(61)
+    t, a, b, d, u, tau = _xv_problem(rng)
+    vm = np.arange(t.shape[-1], dtype=np.int32)
+    _same(O.fuse_verify(t, a, b, d, None, u, tau), O.fuse_verify_xvocab(t, a, b, vm, d, None, u, tau))
+
+
+def test_xvocab_relabelled_drafter_vocabulary():
+    """App. D: delta lives in the drafter's vocabulary.  A drafter whose ids
+    are a permutation of the verifier's, inside a larger vocabulary with
+    drafter-only tokens, gives exactly the plain step when the map is that
+    permutation; the drafter-only tokens are never read (changing them
+    changes nothing)."""
+    rng = np.random.default_rng(62)
+    t, a, b, d, u, tau = _xv_problem(rng)
+    B, Kp1, V = t.shape
+    Vd = V + 25
+    perm = rng.permutation(Vd)[:V]                 # drafter id of verifier token x
+    ad = rng.normal(0, 9, (B, Kp1, Vd)).astype(np.float32)
+    bd = rng.normal(0, 9, (B, Kp1, Vd)).astype(np.float32)
+    ad[..., perm] = a
+    bd[..., perm] = b
+    plain = O.fuse_verify(t, a, b, d, None, u, tau, gate_mode=O.GATE_CDA)
+    _same(plain, O.fuse_verify_xvocab(t, ad, bd, perm, d, None, u, tau))
+    others = np.setdiff1d(np.arange(Vd), perm)
+    ad[..., others] = 50.0
+    bd[..., others] = -50.0
+    _same(plain, O.fuse_verify_xvocab(t, ad, bd, perm, d, None, u, tau))
+
+
+def test_xvocab_commits_restricted_to_shared_set():
+    """Committed tokens come from the shared set only: with a third of the
+    verifier tokens (always including each row's verifier argmax) unshared,
+    every emitted token is shared, and the full log-probabilities are -inf
+    off the set and normalised over it."""
+    rng = np.random.default_rng(63)
+    for trial in range(6):
+        t, a, b, d, u, tau = _xv_problem(rng, V=45)
+        B, Kp1, V = t.shape
+        vm = rng.permutation(V).astype(np.int32)
+        off = rng.random(V) < 0.33
+        off[np.argmax(t.reshape(-1, V), axis=1)] = True
+        vm[off] = -1
+        d = np.where(off[d], np.nonzero(~off)[0][0], d).astype(np.int32)   # drafts are shared
+        acc, nxt, flp, _, _ = O.fuse_verify_xvocab(t, a, b, vm, d, None, u, tau)
+        assert not off[nxt].any()
+        t2, a2, b2 = O.map_to_verifier(t, a, b, vm)
+        full = O.fused_logprobs_full(t2, a2, b2, tau)
+        assert np.isneginf(full[..., off]).all()
+        np.testing.assert_allclose(sps.logsumexp(full[..., ~off], axis=-1), 0.0, atol=1e-12)
+
+
+def test_xvocab_bf16_masks_are_bf16_infinities():
+    bits = np.full((1, 2, 4), 0x3F80, np.uint16)     # 1.0 in bf16
+    t2, a2, b2 = O.map_to_verifier(bits, bits[..., :3], bits[..., :3], np.array([2, -1, 0, 7]))
+    assert t2.dtype == np.uint16 and (t2[..., [1, 3]] == 0xFF80).all() and (t2[..., [0, 2]] == 0x3F80).all()
+    assert (a2[..., [1, 3]] == 0xFF80).all()

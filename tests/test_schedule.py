@@ -109,3 +109,30 @@ def test_lags_cover_the_items_in_flight(driver):
             seen += 1
         elif ty == 1 and seen < n_stats:
             assert idx - last_stat[req] >= G, (req, idx, last_stat[req])
+
+
+GROUP_DRIVER = r"""
+#include <cstdio>
+#include <cstdlib>
+#include "schedule.h"
+int main(int argc, char** argv) {
+  const int n = atoi(argv[1]);
+  for (int s = 0; s < n; ++s) printf("%d\n", asym::xcd_grouped(s, n));
+  return 0;
+}
+"""
+
+
+def test_xcd_grouped_renumbering(tmp_path):
+    """A bijection on [0, n) that gives the items one XCD runs (sub, sub + 8,
+    ...) consecutive positions, so a row's chunks share few XCDs."""
+    src = tmp_path / "g.cpp"
+    exe = tmp_path / "g"
+    src.write_text(GROUP_DRIVER)
+    subprocess.run(["g++", "-O1", "-std=c++17", "-I", CSRC, str(src), "-o", str(exe)], check=True)
+    for n in (1, 5, 7, 8, 9, 70, 71, 135, 512):
+        p = [int(x) for x in subprocess.run([str(exe), str(n)], check=True, capture_output=True,
+                                            text=True).stdout.split()]
+        assert sorted(p) == list(range(n))
+        for s in range(n - 8):
+            assert p[s + 8] == p[s] + 1
