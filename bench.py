@@ -173,8 +173,9 @@ def main():
                     help="distinct input copies rotated between steps (cold cache)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; the step shards by "
-                          "request with no communication (see DESIGN.md)", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "runs on one GPU only: the step shards by request with no "
+                          "communication, so N GPUs would each run fuse_verify on a B/N slice",
+                          "n_gpus": args.gpus}))
         sys.exit(2)
 
     wl = synth.WORKLOADS[args.workload]

@@ -32,7 +32,7 @@ implements the reading that reduces to standard speculative sampling
   r(x) = max(0, p~(x) - q(x)) by inverse CDF with the caller uniform u_K;
 * if all K drafts pass, draw the bonus from softmax(t_K / tau) with u_K.
 
-Conventions fixed here (each is listed with its reason in the design doc):
+Conventions fixed here (readings where the paper is silent or greedy-only):
 
 * The fused logits f = t + beta*(a - b) are formed in IEEE fp32 in that order
   (no fused multiply-add): the argmax decisions of Eq. 2 are taken on these
