@@ -156,6 +156,8 @@ def main():
                     help="also write the full [B, K+1, V] fp32 log-probability rows (second kernel)")
     ap.add_argument("--xvocab", type=str, default=None, metavar="VD:SHARED",
                     help="cross-family drafter: vocabulary size and shared tokens, e.g. 128256:109566")
+    ap.add_argument("--early-exit", type=int, default=0, metavar="ROWS",
+                    help="read the first ROWS rows, the others only without a sure rejection among them")
     ap.add_argument("--fuse-bonus", action="store_true",
                     help="take the bonus token from the fused row f_K (reads rows K of a and b)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -229,7 +231,7 @@ def main():
           "lambda": asp.GATE_LAMBDA}[args.gate_mode]
     dm = {"a-b": asp.DELTA_AB, "a": asp.DELTA_A, "t-b": asp.DELTA_TB}[args.delta_mode]
     var = dict(gate_mode=gm, delta_mode=dm, lam=args.lam, fuse_bonus=args.fuse_bonus,
-               return_full=args.full, vocab_map=vmap)
+               return_full=args.full, vocab_map=vmap, early_exit=args.early_exit)
     outs = asp.fuse_verify(*copies[0], d, q, u, tau, return_gate=args.gate, workspace=ws, **var)
     outs = tuple(o for o in outs)
     # (accept_len, next_token, fused_logprobs, gate or None[, full])
@@ -275,10 +277,20 @@ def main():
         del src, dst
 
     acc = outs[0].cpu().numpy()
+    if args.early_exit and args.early_exit <= K:
+        # bytes actually read: requests with a sure rejection in their first
+        # rows skipped the rest (their later draft outputs are NaN)
+        flp = outs[2].cpu().numpy()
+        skipped = np.isnan(flp[:, args.early_exit:K]).any(axis=1)
+        el = 2 if wl.dtype == "bf16" else 4
+        full_req = (3 * (K + 1) if args.fuse_bonus else 3 * K + 1) * V * el
+        nbytes = int(np.where(skipped, 3 * args.early_exit * V * el, full_req).sum())
+        achieved = nbytes / (kern_ms * 1e-3) / 1e9
     traffic = None
     tpath = os.path.join(ROOT, "profiles", f"traffic_{wl.name}.json")
     default_variant = (args.gate_mode == "cda" and args.delta_mode == "a-b" and not args.gate
-                       and not args.fuse_bonus and not args.full and not args.xvocab)
+                       and not args.fuse_bonus and not args.full and not args.xvocab
+                       and not args.early_exit)
     if default_variant and os.path.exists(tpath):
         try:
             tj = json.load(open(tpath))
@@ -304,7 +316,7 @@ def main():
                    "bytes_per_step": nbytes, "gate_output": bool(args.gate),
                    "gate_mode": args.gate_mode, "delta_mode": args.delta_mode,
                    "fuse_bonus": bool(args.fuse_bonus), "full_logprobs": bool(args.full),
-                   "xvocab": args.xvocab,
+                   "xvocab": args.xvocab, "early_exit_rows": args.early_exit,
                    "input_copies": len(copies), "mean_accept_len": float(acc.mean()),
                    "parallelism": "single GPU"},
         "hbm_GBps": achieved,

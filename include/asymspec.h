@@ -89,14 +89,25 @@ extern "C" {
                                      a and b over all K+1 positions); this reads
                                      rows K of a and b as well */
 
+#define ASYMSPEC_EARLY_EXIT 2u    /* Alg. 1 stops at the first rejection: the first
+                                     early_rows rows of a request are read and
+                                     classified first, and the other rows are read
+                                     only if none of those is surely rejected.
+                                     accept_len, next_token and fused_logprobs[K]
+                                     are unchanged; fused_logprobs[i] and gate_out[i]
+                                     of rows not read (all after the first rejection)
+                                     are NaN.  Not with fused_logprobs_full */
+
 typedef struct asymspec_params {
   float beta;         /* fusion weight of Eq. 2; finite, >= 0 (paper default 1.0) */
   float gamma;        /* base threshold of Eq. 3-4; in (0, 1] (paper default 0.5)  */
   int32_t gate_mode;  /* ASYMSPEC_GATE_*                                           */
-  uint32_t flags;     /* 0 or ASYMSPEC_FUSE_BONUS; other bits must be 0             */
+  uint32_t flags;     /* ASYMSPEC_FUSE_BONUS | ASYMSPEC_EARLY_EXIT; other bits 0     */
   int32_t delta_mode; /* ASYMSPEC_DELTA_* (ASYMSPEC_DELTA_AB for the paper)        */
   float lambda;       /* scale of ASYMSPEC_GATE_LAMBDA, finite (paper default 0.1);
                          ignored by the other gates                                */
+  int32_t early_rows; /* with ASYMSPEC_EARLY_EXIT: rows read before the verdict, in
+                         [0, 63] (0: 2); early_rows >= K + 1 reads every row        */
 } asymspec_params;
 
 /* Bytes of device workspace asymspec_fuse_verify needs for this shape

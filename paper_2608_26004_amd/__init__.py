@@ -13,7 +13,7 @@ import os
 
 __all__ = ["fuse_verify", "workspace_size", "Workspace", "load_library", "status_string",
            "BF16", "FP32", "GATE_CDA", "GATE_FIXED", "GATE_KL", "GATE_LAMBDA",
-           "DELTA_AB", "DELTA_A", "DELTA_TB", "FUSE_BONUS", "AsymSpecError"]
+           "DELTA_AB", "DELTA_A", "DELTA_TB", "FUSE_BONUS", "EARLY_EXIT", "AsymSpecError"]
 
 BF16 = 0
 FP32 = 1
@@ -25,6 +25,7 @@ DELTA_AB = 0
 DELTA_A = 1
 DELTA_TB = 2
 FUSE_BONUS = 1
+EARLY_EXIT = 2
 
 OK = 0
 E_ARG = -1
@@ -46,7 +47,8 @@ class AsymSpecError(RuntimeError):
 class _Params(ctypes.Structure):
     _fields_ = [("beta", ctypes.c_float), ("gamma", ctypes.c_float),
                 ("gate_mode", ctypes.c_int32), ("flags", ctypes.c_uint32),
-                ("delta_mode", ctypes.c_int32), ("lam", ctypes.c_float)]
+                ("delta_mode", ctypes.c_int32), ("lam", ctypes.c_float),
+                ("early_rows", ctypes.c_int32)]
 
 
 def load_library(path: str | None = None):
@@ -118,7 +120,7 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
                 beta: float = 1.0, gamma: float = 0.5, gate_mode: int = GATE_CDA,
                 return_gate: bool = False, workspace: Workspace | None = None, out=None,
                 delta_mode: int = DELTA_AB, lam: float = 0.1, fuse_bonus: bool = False,
-                return_full: bool = False, vocab_map=None):
+                return_full: bool = False, vocab_map=None, early_exit: int = 0):
     """One AsymSpec decision step on the current HIP stream.
 
     t, a, b: [B, K+1, V] torch.bfloat16 or torch.float32 on the GPU
@@ -131,7 +133,10 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     distribution, [B, K+1, V] float32 (a second pass over the logits);
     vocab_map: for a drafter of another model family, [V] int32 on the GPU
     (drafter id of each verifier token, -1 if not shared); a and b are then
-    [B, K+1, Vd] in the drafter's vocabulary.
+    [B, K+1, Vd] in the drafter's vocabulary;
+    early_exit: 0 reads every row; n > 0 reads the first n rows, then the
+    others only if none of those is surely rejected (EARLY_EXIT); the
+    per-draft outputs of rows not read are NaN.
     Returns (accept_len [B] int32, next_token [B] int32,
              fused_logprobs [B, K+1] float32[, gate [B, K, 2] float32]
              [, full [B, K+1, V] float32])."""
@@ -185,8 +190,9 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     if workspace is None:
         workspace = _default_ws.setdefault(dev, Workspace(dev))
     wsbuf = workspace.get(ws_bytes, dev)
-    params = _Params(float(beta), float(gamma), int(gate_mode), FUSE_BONUS if fuse_bonus else 0,
-                     int(delta_mode), float(lam))
+    flags = (FUSE_BONUS if fuse_bonus else 0) | (EARLY_EXIT if early_exit else 0)
+    params = _Params(float(beta), float(gamma), int(gate_mode), flags, int(delta_mode), float(lam),
+                     int(early_exit))
     tail = (_ptr(draft_tokens), _ptr(draft_probs), _ptr(uniforms), _ptr(temperature),
             B, K, V, ctypes.byref(params), _ptr(acc), _ptr(nxt), _ptr(flp), _ptr(gate), _ptr(full),
             _ptr(wsbuf), wsbuf.numel(), _stream_handle(dev))

@@ -9,6 +9,9 @@ ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc", "asymspec.hip")
 INC = os.path.join(ROOT, "include")
 OUT = os.path.join(HERE, "libasymspec.so")
+# per-kernel register and scratch use reported by the compiler for the last
+# build (a kernel that spills to scratch loses most of its read rate)
+RESOURCES = os.path.join(HERE, "libasymspec.resources.txt")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -22,18 +25,41 @@ FLAGS = [
 
 def build(verbose: bool = False, extra=()) -> str:
     tmp = OUT + ".tmp"
-    cmd = [HIPCC, *FLAGS, *extra, "-I", INC, SRC, "-o", tmp]
+    cmd = [HIPCC, *FLAGS, "-Rpass-analysis=kernel-resource-usage", "-fno-caret-diagnostics", *extra, "-I", INC, SRC, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
-    msg = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
-                    if "packed-fp32-ops" not in l and "unknown target feature" not in l)
+    lines = (r.stdout + r.stderr).splitlines()
+    usage = [l for l in lines if "kernel-resource-usage" in l]
+    msg = "\n".join(l for l in lines if "packed-fp32-ops" not in l and "unknown target feature" not in l
+                    and "kernel-resource-usage" not in l)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed ({r.returncode}):\n{msg}")
     if verbose and msg.strip():
         print(msg)
     os.replace(tmp, OUT)
+    with open(RESOURCES, "w") as f:
+        f.write(resource_report(usage))
     return OUT
+
+
+def resource_report(lines) -> str:
+    """One line per kernel: name, VGPRs, scratch bytes per lane, occupancy."""
+    rows, cur = [], {}
+    for l in lines:
+        txt = l.split("remark:", 1)[-1].split("[-Rpass", 1)[0].strip()
+        key, _, val = txt.partition(":")
+        key, val = key.strip(), val.strip()
+        if key == "Function Name":
+            if cur:
+                rows.append(cur)
+            cur = {"name": val}
+        elif key in ("VGPRs", "ScratchSize [bytes/lane]", "Occupancy [waves/SIMD]"):
+            cur[key.split()[0]] = val
+    if cur:
+        rows.append(cur)
+    return "".join(f"{r['name']} vgprs={r.get('VGPRs', '?')} scratch={r.get('ScratchSize', '?')} "
+                   f"occupancy={r.get('Occupancy', '?')}\n" for r in rows)
 
 
 if __name__ == "__main__":

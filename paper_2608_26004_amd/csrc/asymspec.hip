@@ -71,10 +71,16 @@ DEV void stats_chunk(const KArgs& A, int req, int i, int m, Smem& sm) {
 // of the same rows, and each XCD's L2 holds few drafter rows at a time.
 template <int DT, bool kB1, int DM>
 DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
-  const int p = A.vmap != nullptr ? xcd_grouped(sub, (A.K + 1) * A.S) : sub;
+  int p = sub;
+  if (A.vmap != nullptr) {
+    // within each group of rows (all rows, or the two groups of early exit)
+    const int n1 = A.sc.G * A.S, n = (A.K + 1) * A.S;
+    p = sub < n1 ? xcd_grouped(sub, n1) : n1 + xcd_grouped(sub - n1, n - n1);
+  }
   const int i = p / A.S, m = p - i * A.S;
   stats_chunk<DT, kB1, DM>(A, req, i, m, sm);
 }
+
 
 #ifndef ASYMSPEC_WAVES
 #define ASYMSPEC_WAVES 4
@@ -91,9 +97,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ASYMSP
 void fuse_verify_kernel(KArgs A) {
   __shared__ Smem sm;
   const Item it = sched_item(A.sc, A.K, A.S, (int)blockIdx.x);
-  switch (it.type) {
+  int type = it.type;
+  if (type == kItemStats2) {
+    // early exit: the rows after the first group are read unless the
+    // verdict found a sure rejection among the first rows
+    if (load_verdict(A, it.req, sm) == kVerdictSkip) return;
+    type = kItemStats;
+  }
+  // one call site per item kind keeps a single inlined copy of each
+  switch (type) {
     case kItemStats: stats_dispatch<DT, kB1, DM>(A, it.req, it.sub, sm); break;
-    case kItemDecide: decide_item<DT>(A, it.req, sm); break;
+    case kItemVerdict:
+    case kItemDecide: decide_item<DT>(A, it.req, sm, type == kItemVerdict); break;
     case kItemPass2: pass2_item<DT, DM>(A, it.req, it.sub, sm); break;
     case kItemPick: pick_item<DT, DM>(A, it.req, sm); break;
     default: break;
@@ -261,7 +276,11 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   if (params->gate_mode < ASYMSPEC_GATE_CDA || params->gate_mode > ASYMSPEC_GATE_LAMBDA) return ASYMSPEC_E_ARG;
   if (params->delta_mode < ASYMSPEC_DELTA_AB || params->delta_mode > ASYMSPEC_DELTA_TB) return ASYMSPEC_E_ARG;
   if (params->gate_mode == ASYMSPEC_GATE_LAMBDA && !std::isfinite(params->lambda)) return ASYMSPEC_E_ARG;
-  if ((params->flags & ~(uint32_t)ASYMSPEC_FUSE_BONUS) != 0u) return ASYMSPEC_E_ARG;
+  if ((params->flags & ~(uint32_t)(ASYMSPEC_FUSE_BONUS | ASYMSPEC_EARLY_EXIT)) != 0u) return ASYMSPEC_E_ARG;
+  const bool ee = (params->flags & ASYMSPEC_EARLY_EXIT) != 0u;
+  if (ee && (params->early_rows < 0 || params->early_rows > 63)) return ASYMSPEC_E_ARG;
+  // rows after the first rejection are not read, so they have no full rows
+  if (ee && fused_logprobs_full != nullptr) return ASYMSPEC_E_ARG;
   if (vmap != nullptr) {
     // drafter rows are read element by element through the map
     if (Vd < 1 || (unsigned long long)B * (K + 1) * (unsigned long long)Vd >= (1ull << 40)) return ASYMSPEC_E_ARG;
@@ -303,7 +322,8 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   A.ln_gamma = std::log((double)params->gamma);
   A.epoch = next_epoch();
   // lags scale with the number of workgroups the chip holds at once
-  if (!sched_build(B, K, L.S, di->max_blocks[dtype], A.sc)) return ASYMSPEC_E_ARG;
+  const int ee_rows = ee ? (params->early_rows > 0 ? params->early_rows : 2) : 0;
+  if (!sched_build(B, K, L.S, di->max_blocks[dtype], A.sc, ee_rows)) return ASYMSPEC_E_ARG;
   const int grid = A.sc.total;
 
   const unsigned long long nblk = (unsigned long long)B * (K + 1) * L.S;

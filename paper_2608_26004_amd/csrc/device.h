@@ -66,7 +66,10 @@ enum { R1_M = 0, R1_S = kSlots, R1_ARG = 2 * kSlots, R1_NEQ = 2 * kSlots + 1, R1
 // Decision record of one request: a header and one block per row, published
 // by the decide item; pass-2 and pick items load it into LDS (Smem::req,
 // Smem::rows).
-enum { H_STATE = 0, H_J = 1, H_TASK_LO = 2, H_TASK_HI = 3, H_SAMP = 4, H_USED = 5, kDecHdr = 8 };
+enum { H_STATE = 0, H_J = 1, H_TASK_LO = 2, H_TASK_HI = 3, H_SAMP = 4, H_USED = 5, H_VERDICT = 5, kDecHdr = 8 };
+// Early exit: the verdict on a request's first rows (a sure rejection among
+// them makes the other rows unneeded).
+enum { kVerdictRead = 1, kVerdictSkip = 2 };
 enum { kStateFinal = 1, kStatePending = 2 };
 enum { R_J = 0, R_TASK_LO = 1, R_TASK_HI = 2, R_FIN = 3, R_SAMP = 4, kReqWords = 5 };
 enum {
@@ -88,7 +91,8 @@ enum {
   kDecRow = 24
 };
 enum { kTaskJsd = 1, kTaskRes = 2, kTaskBonus = 4 };
-enum { kStDecided = 1, kStAccept = 2, kStDraft = 4, kStNeq = 8 };
+// kStSkip: a row after a sure rejection that early exit did not read.
+enum { kStDecided = 1, kStAccept = 2, kStDraft = 4, kStNeq = 8, kStSkip = 16 };
 
 // Pass-2 record of one (request, row, chunk): the chunk's JSD partial (fp64,
 // in log2 units) and the four wave-segment weight sums (fp64).
@@ -258,7 +262,10 @@ DEV u4 buf_load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
 // Streaming read of logits: the non-temporal cache policy (nt), which keeps
 // the once-read lines from displacing others and measurably raises the read
 // rate of the whole-chip sweep.
-constexpr int kAuxNT = 2;
+#ifndef ASYMSPEC_AUX_NT
+#define ASYMSPEC_AUX_NT 2
+#endif
+constexpr int kAuxNT = ASYMSPEC_AUX_NT;
 DEV u4 buf_load_nt(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kAuxNT);
 }

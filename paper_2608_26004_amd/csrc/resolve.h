@@ -165,24 +165,26 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const f
                 (neq ? kStNeq : 0);
 }
 
-// The decision of request req (Alg. 1, Eq. 2-4) from its statistics
-// records, into sm.rows (one decision block per row) and sm.req (first sure
-// rejection, pass-2 tasks, whether the request is final without pass 2).
-// Thread (i, ch) of a group of rows takes record ch of row i, so all records
-// arrive in one round trip; the row's maxima, sums, argmax and a-vs-b flag
-// are combined through LDS in chunk order and the row's first thread
-// classifies it.  Whole workgroup; S must not exceed kThreads.
+// The decision of request req (Alg. 1, Eq. 2-4) from the statistics records
+// of its first nread rows, into sm.rows (one decision block per row) and
+// sm.req (first sure rejection, pass-2 tasks, whether the request is final
+// without pass 2).  Rows from nread on (early exit: they follow a sure
+// rejection and were not read) get placeholder blocks.  Thread (i, ch) of a
+// group of rows takes record ch of row i, so all records arrive in one round
+// trip; the row's maxima, sums, argmax and a-vs-b flag are combined through
+// LDS in chunk order and the row's first thread classifies it.  Whole
+// workgroup; S must not exceed kThreads.
 template <int DT>
-DEV void decide_request(const KArgs& A, int req, Smem& sm) {
+DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
   const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
   const int K = A.K, S = A.S, nrow = K + 1;
   const int rpg = kThreads / S;                 // rows per group
   const int li = tid / S, ch = tid - li * S;
-  // the request's last statistics item in list order is about the last to
+  // the last statistics item read in list order is about the last to
   // finish: a waiting workgroup polls its record only
-  const uint64_t* sentinel = A.rec1 + (((size_t)req * nrow + K) * S + (S - 1)) * kR1 + R1_NEQ;
-  for (int r0 = 0; r0 < nrow; r0 += rpg) {
-    const int nr = min(rpg, nrow - r0);
+  const uint64_t* sentinel = A.rec1 + (((size_t)req * nrow + (nread - 1)) * S + (S - 1)) * kR1 + R1_NEQ;
+  for (int r0 = 0; r0 < nread; r0 += rpg) {
+    const int nr = min(rpg, nread - r0);
     const bool have = li < nr;
     const int i = r0 + (have ? li : 0);
     // first requests: the records, the draft token and its logits (row
@@ -264,6 +266,18 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
     }
     __syncthreads();
   }
+  if (nread < nrow) {
+    // unread rows: decided, not accepted, outputs not a number
+    for (int k = tid; k < (nrow - nread) * kDecRow; k += kThreads) {
+      const int i = nread + k / kDecRow, j = k - (k / kDecRow) * kDecRow;
+      uint32_t v = 0u;
+      if (j == D_STATUS) v = kStDecided | kStDraft | kStSkip;
+      else if (j == D_LPD || j == D_LPEMIT) v = 0x7FC00000u;
+      else if (j == D_GD_HI) v = 0x7FF80000u;
+      sm.rows[i][j] = v;
+    }
+    __syncthreads();
+  }
   // request level (wave 0, lane i = row i): the first sure rejection j*, and
   // the rows pass 2 must look at
   if (w == 0) {
@@ -301,15 +315,21 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm) {
 // Every output of request `req`, written by wave 0: lane i < K holds draft
 // i's fused log-probability and D_i.
 DEV void write_outputs(const KArgs& A, int req, int j, int next, float lp_next, float lpd_lane,
-                       double d_lane) {
+                       double d_lane, bool skip_lane) {
   const int lane = lane_id();
   const int K = A.K;
   if (lane < K) {
+    // a row early exit did not read has no outputs
+    if (skip_lane) {
+      lpd_lane = __builtin_nanf("");
+      d_lane = __builtin_nan("");
+    }
     A.flp_out[(size_t)req * (K + 1) + lane] = lpd_lane;
     if (A.gate_out != nullptr) {
       // gamma_eff = gamma (fixed gate) or gamma exp(-D) (Eq. 3 and the
       // KL and lambda variants)
-      const float ge = A.gate_mode == ASYMSPEC_GATE_FIXED ? A.gamma : (float)((double)A.gamma * exp(-d_lane));
+      float ge = A.gate_mode == ASYMSPEC_GATE_FIXED ? A.gamma : (float)((double)A.gamma * exp(-d_lane));
+      if (skip_lane) ge = __builtin_nanf("");
       A.gate_out[((size_t)req * K + lane) * 2 + 0] = (float)d_lane;
       A.gate_out[((size_t)req * K + lane) * 2 + 1] = ge;
     }
@@ -321,11 +341,44 @@ DEV void write_outputs(const KArgs& A, int req, int j, int next, float lp_next, 
   }
 }
 
+// Early exit: the verdict of request req (kVerdictRead or kVerdictSkip),
+// the same in every thread.  Whole workgroup.
+DEV uint32_t load_verdict(const KArgs& A, int req, Smem& sm) {
+  if (wave_id() == 0 && lane_id() == 0) {
+    // the verdict is written long before most readers come: a first read
+    // that may be served by this XCD's L2 (a stale line carries an older
+    // epoch and falls through to the polling read)
+    const uint64_t* p = dec_hdr(A, req) + H_VERDICT;
+    uint64_t v = __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (!tag_ok(v, A.epoch)) v = wait_tag(p, A);
+    // a verdict that never arrived (counted as a timeout) reads every row
+    sm.flags[3] = (tag_ok(v, A.epoch) && pay(v) == kVerdictSkip) ? 1 : 0;
+  }
+  __syncthreads();
+  const uint32_t r = sm.flags[3] ? kVerdictSkip : kVerdictRead;
+  __syncthreads();
+  return r;
+}
+
+// The decide item, and (verdict) the early-exit verdict item: it classifies
+// the first G rows only, and a sure rejection among them (Alg. 1 stops at
+// the first rejection) means the other rows need not be read.  Both share
+// one instance of decide_request.
 template <int DT>
-DEV void decide_item(const KArgs& A, int req, Smem& sm) {
+DEV void decide_item(const KArgs& A, int req, Smem& sm, bool verdict) {
   const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
   const int K = A.K, nrow = K + 1;
-  decide_request<DT>(A, req, sm);
+  int nread = nrow;
+  if (verdict || (A.sc.ee && load_verdict(A, req, sm) == kVerdictSkip)) nread = A.sc.G;
+  decide_request<DT>(A, req, sm, nread);
+  if (verdict) {
+    if (w == 0) {
+      const uint32_t st = lane < nread ? sm.rows[lane][D_STATUS] : 0u;
+      const bool skip = __any((st & kStDecided) != 0u && (st & kStAccept) == 0u);
+      if (lane == 0) st_tag(dec_hdr(A, req) + H_VERDICT, skip ? kVerdictSkip : kVerdictRead, A.epoch);
+    }
+    return;
+  }
   // publish: every word of every row block, then the header
   for (int k = tid; k < nrow * D_USED; k += kThreads) {
     const int i = k / D_USED, j = k - i * D_USED;
@@ -354,7 +407,8 @@ DEV void decide_item(const KArgs& A, int req, Smem& sm) {
       const double dl = (lane < K && A.gate_mode == ASYMSPEC_GATE_LAMBDA)
                             ? u2d(sm.rows[lane][D_GD_LO], sm.rows[lane][D_GD_HI])
                             : 0.0;
-      write_outputs(A, req, jstar, next, lpn, lpd, dl);
+      const bool skip = lane <= K && (sm.rows[lane][D_STATUS] & kStSkip) != 0u;
+      write_outputs(A, req, jstar, next, lpn, lpd, dl, skip);
     }
   }
 }
@@ -791,7 +845,10 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
     const double l2 = u2d(sm.rows[j][D_L2E_LO], sm.rows[j][D_L2E_HI]);
     lpn = (float)(((double)x * c - l2) * kLn2);
   }
-  if (w == 0) write_outputs(A, req, j, next, lpn, lpd, Dl);
+  if (w == 0) {
+    const bool skip = lane <= K && (sm.rows[lane][D_STATUS] & kStSkip) != 0u;
+    write_outputs(A, req, j, next, lpn, lpd, Dl, skip);
+  }
 }
 
 }  // namespace asym

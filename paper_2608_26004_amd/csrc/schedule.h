@@ -6,19 +6,24 @@
 // The step is a single ordered list of work items, one workgroup each, which
 // the hardware starts in index order.  Items are grouped in steps q = 0, 1,
 // 2, ...; step q holds
-//   * the statistics items of request q       ((K+1) * S items: one per row
-//     and vocabulary chunk), when q < B,
+//   * the statistics items of request q       (G * S items: one per row of
+//     the first G rows and vocabulary chunk), when q < B,
+//   * the verdict item of request q - Lv      (1 item; early exit only),
+//   * the statistics items of the other rows of request q - Ls
+//                                             ((K+1-G) * S items; early exit
+//                                             only),
 //   * the decide item of request q - L1       (1 item),
 //   * the pass-2 items of request q - L2      (S items, one per chunk),
 //   * the pick item of request q - L3         (1 item),
-// each present only when its request index lies in [0, B).  An item only ever
-// waits for items earlier in the list, so the lowest unfinished item can
-// always proceed.  The lags keep those waits rare: each spans a multiple of
-// the number of items in flight at once.
+// each present only when its request index lies in [0, B).  Without early
+// exit G = K + 1 and Lv = Ls = 0.  An item only ever waits for items earlier
+// in the list, so the lowest unfinished item can always proceed.  The lags
+// keep those waits rare: each spans a multiple of the number of items in
+// flight at once.
 //
-// Steps fall into at most 7 runs of equal composition (the boundaries are
-// 0, L1, L2, L3, B, B+L1, B+L2, B+L3); an item index is decoded by finding
-// its run.
+// Steps fall into at most 11 runs of equal composition (the boundaries are
+// 0, Lv, Ls, L1, L2, L3 and B plus each of them); an item index is decoded by
+// finding its run.
 
 #ifndef ASYMSPEC_SCHEDULE_H_
 #define ASYMSPEC_SCHEDULE_H_
@@ -29,15 +34,22 @@
 
 namespace asym {
 
-enum ItemType { kItemNone = -1, kItemStats = 0, kItemDecide = 1, kItemPass2 = 2, kItemPick = 3 };
-enum PartBits { kPartStats = 1, kPartDecide = 2, kPartPass2 = 4, kPartPick = 8 };
+enum ItemType {
+  kItemNone = -1, kItemStats = 0, kItemDecide = 1, kItemPass2 = 2, kItemPick = 3,
+  kItemVerdict = 4, kItemStats2 = 5
+};
+enum PartBits {
+  kPartStats = 1, kPartDecide = 2, kPartPass2 = 4, kPartPick = 8, kPartVerdict = 16, kPartStats2 = 32
+};
 
-constexpr int kMaxRuns = 8;
+constexpr int kMaxRuns = 12;
 
 struct Sched {
   int n_runs;
   int total;              // number of items
-  int L1, L2, L3;
+  int G;                  // rows in the first group (K + 1 without early exit)
+  int ee;                 // early exit: verdict and second-group items present
+  int Lv, Ls, L1, L2, L3;
   int q0[kMaxRuns];       // first step of the run
   int i0[kMaxRuns];       // index of the run's first item
   int blk[kMaxRuns];      // items per step in the run (> 0)
@@ -47,20 +59,25 @@ struct Sched {
 struct Item {
   int type;   // ItemType
   int req;    // request index
-  int sub;    // stats: row-in-request * S + chunk; pass 2: chunk; else 0
+  int sub;    // statistics: row-in-request * S + chunk; pass 2: chunk; else 0
 };
 
-ASYM_HD inline int sched_parts(int q, int B, int L1, int L2, int L3) {
+ASYM_HD inline bool sched_in(int q, int lag, int B) { return q - lag >= 0 && q - lag < B; }
+
+ASYM_HD inline int sched_parts(const Sched& sc, int q, int B) {
   int p = 0;
-  if (q >= 0 && q < B) p |= kPartStats;
-  if (q - L1 >= 0 && q - L1 < B) p |= kPartDecide;
-  if (q - L2 >= 0 && q - L2 < B) p |= kPartPass2;
-  if (q - L3 >= 0 && q - L3 < B) p |= kPartPick;
+  if (sched_in(q, 0, B)) p |= kPartStats;
+  if (sc.ee && sched_in(q, sc.Lv, B)) p |= kPartVerdict;
+  if (sc.ee && sched_in(q, sc.Ls, B)) p |= kPartStats2;
+  if (sched_in(q, sc.L1, B)) p |= kPartDecide;
+  if (sched_in(q, sc.L2, B)) p |= kPartPass2;
+  if (sched_in(q, sc.L3, B)) p |= kPartPick;
   return p;
 }
 
-ASYM_HD inline int sched_block(int parts, int K, int S) {
-  return ((parts & kPartStats) ? (K + 1) * S : 0) + ((parts & kPartDecide) ? 1 : 0) +
+ASYM_HD inline int sched_block(const Sched& sc, int parts, int K, int S) {
+  return ((parts & kPartStats) ? sc.G * S : 0) + ((parts & kPartVerdict) ? 1 : 0) +
+         ((parts & kPartStats2) ? (K + 1 - sc.G) * S : 0) + ((parts & kPartDecide) ? 1 : 0) +
          ((parts & kPartPass2) ? S : 0) + ((parts & kPartPick) ? 1 : 0);
 }
 
@@ -73,40 +90,57 @@ ASYM_HD inline int sched_block(int parts, int K, int S) {
 #ifndef ASYMSPEC_LAG3_PCT
 #define ASYMSPEC_LAG3_PCT ASYMSPEC_LAG2_PCT
 #endif
+#ifndef ASYMSPEC_LAGV_PCT
+#define ASYMSPEC_LAGV_PCT 150
+#endif
+#ifndef ASYMSPEC_LAGS_PCT
+#define ASYMSPEC_LAGS_PCT 100
+#endif
 
 // Lags in steps.  items_in_flight is the number of workgroups the chip holds
 // at once; the items of one request finish about that many items after the
 // first of them starts, and a resolve item that waits holds its workgroup, so
 // the decide lag spans lag_pct percent of items_in_flight statistics items,
 // and the pass-2 and pick lags add lag2_pct and lag3_pct percent to the lag
-// before them.  Returns false when the schedule would not fit in 31-bit
-// indices.
-inline bool sched_build(int B, int K, int S, int items_in_flight, Sched& sc,
+// before them.  With early exit (ee_rows in [1, K]) the first ee_rows rows of
+// a request are read first, its verdict follows LAGV_PCT later and the other
+// rows LAGS_PCT after that; the decide lag then counts from those.  Returns
+// false when the schedule would not fit in 31-bit indices.
+inline bool sched_build(int B, int K, int S, int items_in_flight, Sched& sc, int ee_rows = 0,
                         int lag_pct = ASYMSPEC_LAG_PCT, int lag2_pct = ASYMSPEC_LAG2_PCT,
                         int lag3_pct = ASYMSPEC_LAG3_PCT) {
-  if (B < 1 || K < 0 || S < 1 || items_in_flight < 1) return false;
+  if (B < 1 || K < 0 || S < 1 || items_in_flight < 1 || ee_rows < 0) return false;
   // steps hold at least the (K+1) * S statistics items of their request
   const long long per_step = (long long)(K + 1) * S;
   auto window = [&](int pct) {
     const long long span = (long long)items_in_flight * pct / 100;
     return (int)((span + per_step - 1) / per_step);
   };
-  sc.L1 = window(lag_pct) + 1;
+  sc.ee = (ee_rows >= 1 && ee_rows <= K) ? 1 : 0;
+  sc.G = sc.ee ? ee_rows : K + 1;
+  sc.Lv = sc.ee ? window(ASYMSPEC_LAGV_PCT) + 1 : 0;
+  sc.Ls = sc.ee ? sc.Lv + window(ASYMSPEC_LAGS_PCT) + 1 : 0;
+  sc.L1 = sc.Ls + window(lag_pct) + 1;
   sc.L2 = sc.L1 + window(lag2_pct) + 1;
   sc.L3 = sc.L2 + window(lag3_pct) + 1;
-  int bp[8] = {0, sc.L1, sc.L2, sc.L3, B, B + sc.L1, B + sc.L2, B + sc.L3};
-  // sort the 8 boundaries (insertion sort) and drop duplicates
-  for (int i = 1; i < 8; ++i)
+  const int lags[6] = {0, sc.Lv, sc.Ls, sc.L1, sc.L2, sc.L3};
+  int bp[12];
+  for (int i = 0; i < 6; ++i) {
+    bp[i] = lags[i];
+    bp[6 + i] = B + lags[i];
+  }
+  // sort the 12 boundaries (insertion sort); equal ones give empty runs
+  for (int i = 1; i < 12; ++i)
     for (int j = i; j > 0 && bp[j - 1] > bp[j]; --j) {
       const int t = bp[j]; bp[j] = bp[j - 1]; bp[j - 1] = t;
     }
   long long idx = 0;
   sc.n_runs = 0;
-  for (int i = 0; i + 1 < 8; ++i) {
+  for (int i = 0; i + 1 < 12; ++i) {
     const int qa = bp[i], qb = bp[i + 1];
     if (qb <= qa) continue;
-    const int parts = sched_parts(qa, B, sc.L1, sc.L2, sc.L3);
-    const int blk = sched_block(parts, K, S);
+    const int parts = sched_parts(sc, qa, B);
+    const int blk = sched_block(sc, parts, K, S);
     if (blk == 0) continue;
     if (sc.n_runs >= kMaxRuns) return false;
     sc.q0[sc.n_runs] = qa;
@@ -133,10 +167,18 @@ ASYM_HD inline Item sched_item(const Sched& sc, int K, int S, int idx) {
   int o = off - qs * blk;
   const int q = sc.q0[r] + qs;
   const int parts = sc.parts[r];
-  const int ns = (K + 1) * S;
+  const int n1 = sc.G * S, n2 = (K + 1 - sc.G) * S;
   if (parts & kPartStats) {
-    if (o < ns) { it.type = kItemStats; it.req = q; it.sub = o; return it; }
-    o -= ns;
+    if (o < n1) { it.type = kItemStats; it.req = q; it.sub = o; return it; }
+    o -= n1;
+  }
+  if (parts & kPartVerdict) {
+    if (o < 1) { it.type = kItemVerdict; it.req = q - sc.Lv; it.sub = 0; return it; }
+    o -= 1;
+  }
+  if (parts & kPartStats2) {
+    if (o < n2) { it.type = kItemStats2; it.req = q - sc.Ls; it.sub = n1 + o; return it; }
+    o -= n2;
   }
   if (parts & kPartDecide) {
     if (o < 1) { it.type = kItemDecide; it.req = q - sc.L1; it.sub = 0; return it; }

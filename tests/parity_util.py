@@ -29,7 +29,8 @@ def to_device(x, device="cuda"):
 
 
 def run_gpu(inp, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True, want_gate=True,
-            device="cuda", delta_mode=0, lam=0.1, fuse_bonus=False, want_full=False, vocab=None):
+            device="cuda", delta_mode=0, lam=0.1, fuse_bonus=False, want_full=False, vocab=None,
+            early_exit=0):
     """vocab = (a_d, b_d, vocab_map): drafter rows in another vocabulary,
     passed in place of inp.a and inp.b."""
     import torch
@@ -46,7 +47,7 @@ def run_gpu(inp, beta=1.0, gamma=0.5, gate_mode=0, with_probs=True, want_gate=Tr
     out = asp.fuse_verify(t, a, b, d, q, u, tau, beta=beta, gamma=gamma,
                           gate_mode=gate_mode, return_gate=want_gate,
                           delta_mode=delta_mode, lam=lam, fuse_bonus=fuse_bonus,
-                          return_full=want_full, vocab_map=vm)
+                          return_full=want_full, vocab_map=vm, early_exit=early_exit)
     torch.cuda.synchronize()
     res = [x.cpu().numpy() for x in out]
     if not want_gate:

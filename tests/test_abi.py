@@ -56,12 +56,12 @@ def _call(**over):
     lib = asp.load_library()
     fake = 1 << 20          # 16-B and 256-B aligned fake device addresses
     kw = dict(t=fake, a=fake, b=fake, dtype=0, d=fake, dp=None, u=fake, tau=fake,
-              B=2, K=2, V=64, beta=1.0, gamma=0.5, mode=0, flags=0, delta=0, lam=0.1,
+              B=2, K=2, V=64, beta=1.0, gamma=0.5, mode=0, flags=0, delta=0, lam=0.1, ee=0,
               acc=fake, nxt=fake, flp=fake, gate=None, full=None, ws=fake, wsb=None, stream=None)
     kw.update(over)
     if kw["wsb"] is None:
         kw["wsb"] = asp.workspace_size(max(kw["B"], 1), max(kw["K"], 0), max(kw["V"], 1), 0) or 1 << 20
-    p = asp._Params(kw["beta"], kw["gamma"], kw["mode"], kw["flags"], kw["delta"], kw["lam"])
+    p = asp._Params(kw["beta"], kw["gamma"], kw["mode"], kw["flags"], kw["delta"], kw["lam"], kw["ee"])
     return lib.asymspec_fuse_verify(kw["t"], kw["a"], kw["b"], kw["dtype"], kw["d"], kw["dp"],
                                     kw["u"], kw["tau"], kw["B"], kw["K"], kw["V"], ctypes.byref(p),
                                     kw["acc"], kw["nxt"], kw["flp"], kw["gate"], kw["full"], kw["ws"], kw["wsb"],
@@ -91,8 +91,11 @@ def _call(**over):
     (dict(delta=-1), asp.E_ARG),
     (dict(mode=3, lam=float("inf")), asp.E_ARG),
     (dict(mode=3, lam=float("nan")), asp.E_ARG),
-    (dict(flags=2), asp.E_ARG),
-    (dict(flags=3), asp.E_ARG),
+    (dict(flags=4), asp.E_ARG),
+    (dict(flags=7), asp.E_ARG),
+    (dict(flags=2, ee=-1), asp.E_ARG),
+    (dict(flags=2, ee=64), asp.E_ARG),
+    (dict(flags=2, full=1 << 20), asp.E_ARG),
     (dict(K=0, flags=1, a=None), asp.E_ARG),
     (dict(K=0, flags=1, b=None), asp.E_ARG),
     (dict(K=0, flags=1, a=(1 << 20) + 4), asp.E_ALIGN),
@@ -126,7 +129,7 @@ def _call_xv(**over):
     kw.update(over)
     if kw["wsb"] is None:
         kw["wsb"] = asp.workspace_size(max(kw["B"], 1), max(kw["K"], 0), max(kw["V"], 1), 0) or 1 << 20
-    p = asp._Params(1.0, 0.5, 0, 0, 0, 0.1)
+    p = asp._Params(1.0, 0.5, 0, 0, 0, 0.1, 0)
     return lib.asymspec_fuse_verify_xvocab(kw["t"], kw["a"], kw["b"], kw["dtype"], kw["vm"], kw["Vd"],
                                            kw["d"], kw["dp"], kw["u"], kw["tau"], kw["B"], kw["K"], kw["V"],
                                            ctypes.byref(p), kw["acc"], kw["nxt"], kw["flp"], kw["gate"],
@@ -154,3 +157,17 @@ def test_xvocab_drafter_rows_need_only_element_alignment():
     if torch.cuda.is_available():
         pytest.skip("host-only check")
     assert _call_xv(a=(1 << 20) + 4, b=(1 << 20) + 8) in (asp.OK, asp.E_DEVICE)
+
+
+def test_kernels_do_not_spill():
+    """The compiler's per-kernel report from the last build: no kernel of
+    the decision step or the full rows uses scratch (a spill costs most of
+    the read rate)."""
+    path = os.path.join(ROOT, "paper_2608_26004_amd", "libasymspec.resources.txt")
+    if not os.path.exists(path):
+        pytest.skip("no build report")
+    rows = [l.split() for l in open(path) if "fuse_verify_kernel" in l or "dump_kernel" in l]
+    assert len(rows) >= 12
+    for r in rows:
+        kv = dict(x.split("=") for x in r[1:])
+        assert kv["scratch"] == "0", r

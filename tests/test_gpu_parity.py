@@ -4,6 +4,7 @@ C ABI, on the seeded workloads and on edge shapes."""
 import numpy as np
 import pytest
 
+import oracle as O
 from paper_2608_26004_amd import synth
 
 from parity_util import compare, compare_full, run_gpu
@@ -336,3 +337,83 @@ def test_xvocab_workload_1(gpu):
     x = synth.workload_inputs(1)
     g, mx = _run_xv(x, 120000, 0.85, seed=3)
     _note(compare(mx, g, label="xvocab workload 1"))
+
+
+# ----------------------------------------------------------- early exit --
+def _check_early_exit(x, ee, **kw):
+    """Early exit against the full read of the same call (same kernels on
+    the rows both read, so bitwise) and against the oracle: accept_len,
+    next_token and fused_logprobs[K] agree; a draft row's outputs are NaN
+    only after the first rejection (Alg. 1), otherwise they agree."""
+    g0 = run_gpu(x, **kw)
+    g = run_gpu(x, early_exit=ee, **kw)
+    _note(compare(x, g0, label=f"early exit reference {kw}", **kw))
+    acc0, nxt0, flp0, gate0 = g0[:4]
+    acc, nxt, flp, gate = g[:4]
+    assert np.array_equal(acc, acc0) and np.array_equal(nxt, nxt0)
+    assert np.array_equal(flp[:, x.K], flp0[:, x.K], equal_nan=True)
+    skipped = 0
+    for r in range(x.B):
+        for i in range(x.K):
+            if np.isnan(flp[r, i]) and not np.isnan(flp0[r, i]):
+                assert i > acc[r] and i >= ee, (r, i, acc[r])
+                assert np.isnan(gate[r, i]).all()
+                skipped += 1
+            else:
+                assert flp[r, i] == flp0[r, i] or (np.isnan(flp[r, i]) and np.isnan(flp0[r, i]))
+                assert np.array_equal(gate[r, i], gate0[r, i], equal_nan=True)
+    return skipped
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("tau", [0.0, 1.0, 0.7])
+@pytest.mark.parametrize("ee", [1, 2, 4])
+def test_early_exit_small(gpu, dtype, tau, ee):
+    x = synth.generate(B=16, K=6, V=3000, dtype=dtype, rho=("alternate", 0.0, 2.0), tau=tau,
+                       seed=700 + ee)
+    n = _check_early_exit(x, ee)
+    print(f"[early exit] {dtype} tau={tau} ee={ee}: {n} draft rows not read")
+
+
+@pytest.mark.parametrize("gate,delta,fb", [(1, 0, True), (2, 0, False), (3, 2, True), (0, 1, False)])
+def test_early_exit_variants(gpu, gate, delta, fb):
+    x = synth.generate(B=12, K=5, V=4097, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=800 + gate)
+    _check_early_exit(x, 2, gate_mode=gate, delta_mode=delta, fuse_bonus=fb)
+
+
+@pytest.mark.parametrize("V,K,ee", [(1, 2, 1), (7, 1, 1), (8193, 3, 2), (5000, 2, 2), (300, 4, 9)])
+def test_early_exit_edges(gpu, V, K, ee):
+    x = synth.generate(B=6, K=K, V=V, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=V + K)
+    _check_early_exit(x, ee)
+
+
+def test_early_exit_xvocab(gpu):
+    from parity_util import make_xvocab
+    x = synth.generate(B=8, K=4, V=3000, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=901)
+    ad, bd, vm, mx = make_xvocab(x, 2600, 0.8, seed=5)
+    g0 = run_gpu(mx, vocab=(ad, bd, vm))
+    g = run_gpu(mx, vocab=(ad, bd, vm), early_exit=2)
+    _note(compare(mx, g0, label="early exit xvocab reference"))
+    assert np.array_equal(g[0], g0[0]) and np.array_equal(g[1], g0[1])
+
+
+def test_early_exit_workload_3_sampled(gpu):
+    """The bench workload with early exit after two rows."""
+    x = synth.workload_inputs(3)
+    g = run_gpu(x, early_exit=2)
+    sample = list(range(0, 6)) + list(range(64, 68)) + list(range(122, 128))
+    acc, nxt, flp = g[0], g[1], g[2]
+    acc_o, nxt_o, flp_o, _, res = O.fuse_verify(x.t, x.a, x.b, x.draft_tokens, x.draft_probs,
+                                                x.uniforms, x.temperature, requests=sample)
+    for k, bi in enumerate(sample):
+        if (acc[bi], nxt[bi]) != (acc_o[k], nxt_o[k]):
+            assert res[k].near_tie(1e-6), (bi, acc[bi], nxt[bi], acc_o[k], nxt_o[k])
+            continue
+        assert abs(flp[bi, x.K] - flp_o[k, x.K]) < 1e-5
+        for i in range(acc[bi] + 1):
+            if i < x.K:
+                assert abs(flp[bi, i] - flp_o[k, i]) < 1e-5
+    print(f"[early exit] workload 3: {int(np.isnan(flp[:, :x.K]).sum())} draft rows not read of {x.B * x.K}")

@@ -22,8 +22,9 @@ DRIVER = r"""
 using namespace asym;
 int main(int argc, char** argv) {
   const int B = atoi(argv[1]), K = atoi(argv[2]), S = atoi(argv[3]), G = atoi(argv[4]);
+  const int ee = argc > 5 ? atoi(argv[5]) : 0;
   Sched sc;
-  if (!sched_build(B, K, S, G, sc)) { printf("FAIL build\n"); return 1; }
+  if (!sched_build(B, K, S, G, sc, ee)) { printf("FAIL build\n"); return 1; }
   printf("T %d %d %d %d\n", sc.total, sc.L1, sc.L2, sc.L3);
   for (int i = 0; i < sc.total; ++i) {
     const Item it = sched_item(sc, K, S, i);
@@ -47,8 +48,8 @@ def driver():
     return exe
 
 
-def enumerate_items(exe, B, K, S, G):
-    out = subprocess.run([exe, str(B), str(K), str(S), str(G)], check=True,
+def enumerate_items(exe, B, K, S, G, ee=0):
+    out = subprocess.run([exe, str(B), str(K), str(S), str(G), str(ee)], check=True,
                          capture_output=True, text=True).stdout.split("\n")
     head = out[0].split()
     assert head[0] == "T"
@@ -136,3 +137,46 @@ def test_xcd_grouped_renumbering(tmp_path):
         assert sorted(p) == list(range(n))
         for s in range(n - 8):
             assert p[s + 8] == p[s] + 1
+
+
+EE_SHAPES = [(1, 1, 1, 1, 1), (128, 6, 10, 1024, 2), (128, 6, 10, 1024, 1), (32, 8, 10, 1024, 3),
+             (512, 8, 16, 1024, 2), (7, 2, 30, 2048, 2), (200, 3, 1, 3, 1), (5, 63, 2, 7, 60)]
+
+
+@pytest.mark.parametrize("B,K,S,G,ee", EE_SHAPES)
+def test_early_exit_order(driver, B, K, S, G, ee):
+    """With early exit the first ee rows of a request are read, then its
+    verdict, then the other rows (skipped after a sure rejection); every
+    item appears once and each comes after all items it waits for."""
+    items = enumerate_items(driver, B, K, S, G, ee)
+    n1 = ee * S
+    stats, verdict, decide, pass2, pick = {}, {}, {}, {}, {}
+    for idx, (ty, req, sub) in enumerate(items):
+        assert 0 <= req < B
+        if ty in (0, 5):
+            assert (sub < n1) == (ty == 0)
+            assert 0 <= sub < (K + 1) * S and (req, sub) not in stats
+            stats[(req, sub)] = idx
+        elif ty == 4:
+            assert req not in verdict
+            verdict[req] = idx
+        elif ty == 1:
+            decide[req] = idx
+        elif ty == 2:
+            pass2[(req, sub)] = idx
+        elif ty == 3:
+            pick[req] = idx
+        else:
+            pytest.fail(f"unknown item type {ty}")
+    assert len(stats) == B * (K + 1) * S and len(verdict) == len(decide) == len(pick) == B
+    for r in range(B):
+        assert verdict[r] > max(stats[(r, s)] for s in range(n1))
+        assert min(stats[(r, s)] for s in range(n1, (K + 1) * S)) > verdict[r]
+        assert decide[r] > max(stats[(r, s)] for s in range((K + 1) * S))
+        assert min(pass2[(r, m)] for m in range(S)) > decide[r]
+        assert pick[r] > max(pass2[(r, m)] for m in range(S))
+
+
+def test_early_exit_off_when_no_second_group(driver):
+    # ee >= K + 1 leaves nothing to skip: the plain schedule
+    assert enumerate_items(driver, 4, 2, 3, 64, 3) == enumerate_items(driver, 4, 2, 3, 64, 0)
