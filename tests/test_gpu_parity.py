@@ -417,3 +417,38 @@ def test_early_exit_workload_3_sampled(gpu):
             if i < x.K:
                 assert abs(flp[bi, i] - flp_o[k, i]) < 1e-5
     print(f"[early exit] workload 3: {int(np.isnan(flp[:, :x.K]).sum())} draft rows not read of {x.B * x.K}")
+
+
+# ------------------------------------------------------- maximum sizes --
+def test_max_drafts(gpu):
+    """K = 63: 64 rows per request, the most one wave's request-level logic
+    holds."""
+    x = synth.generate(B=2, K=63, V=1000, dtype="bf16", rho=("uniform", 0.0, 0.3),
+                       tau=("alternate", 0.0, 1.0), seed=63)
+    for ee in (0, 5):
+        g = run_gpu(x, early_exit=ee)
+        if ee == 0:
+            _note(compare(x, g, label="K=63"))
+        else:
+            g0 = run_gpu(x)
+            assert np.array_equal(g[0], g0[0]) and np.array_equal(g[1], g0[1])
+
+
+@pytest.mark.parametrize("dtype,V", [("bf16", 4194297), ("fp32", 2097149)])
+def test_max_vocabulary(gpu, dtype, V):
+    """The longest rows the workspace layout takes: 256 chunks per row, so
+    the decide item combines one row per group of 256 threads."""
+    x = synth.generate(B=1, K=2, V=V, dtype=dtype, rho=1.0, tau=("alternate", 1.0, 0.0), seed=V % 1000)
+    g = run_gpu(x, want_full=True)
+    _note(compare(x, g, label=f"max V {dtype}"))
+    compare_full(x, g[4], label=f"max V full {dtype}")
+
+
+def test_many_requests(gpu):
+    """A long item list: 3000 requests of tiny rows; the oracle checks a
+    sample spread over the list (its start, middle and end)."""
+    x = synth.generate(B=3000, K=1, V=64, dtype="fp32", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=3000)
+    g = run_gpu(x)
+    sample = list(range(0, 20)) + list(range(1490, 1510)) + list(range(2980, 3000))
+    _note(compare(x, g, requests=sample, label="B=3000"))
