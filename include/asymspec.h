@@ -164,7 +164,7 @@ int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stre
  *                       second kernel on `stream` that reads the logits again
  *                       (3 (K+1) V elements) and writes 4 (K+1) V bytes per request;
  *                       one workgroup per 32 KiB chunk of a row, so B (K+1) times
- *                       the chunks per row must stay below 2^32 (else E_ARG)
+ *                       the chunks per row must stay below 2^31 (else E_ARG)
  *   workspace           device scratch of >= asymspec_workspace_size bytes,
  *                       256-byte aligned, contents opaque between calls
  *   stream              hipStream_t or NULL

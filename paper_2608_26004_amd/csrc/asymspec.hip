@@ -151,10 +151,20 @@ static bool make_layout(int B, int K, int V, int dtype, Layout& L) {
   return true;
 }
 
+// Through a vocabulary map every chunk of a row gathers from the whole of
+// the row's drafter logits; launched with this much unused dynamic LDS per
+// workgroup, fewer workgroups share a CU, so each XCD works on fewer rows at
+// a time and its L2 keeps their drafter rows.
+#ifndef ASYMSPEC_XV_LDS
+#define ASYMSPEC_XV_LDS 49152
+#endif
+constexpr size_t kXvLds = ASYMSPEC_XV_LDS;
+
 struct DevInfo {
   int ok = 0;
   int n_cu = 0;
   int max_blocks[2] = {0, 0};   // co-resident workgroups, per dtype
+  int max_blocks_xv[2] = {0, 0};   // the same with kXvLds of dynamic LDS
 };
 
 static DevInfo g_dev[64];
@@ -200,17 +210,21 @@ static const DevInfo* device_info() {
   if (std::strncmp(pr.gcnArchName, "gfx950", 6) != 0) return nullptr;
   di.n_cu = pr.multiProcessorCount;
   for (int dt = 0; dt < 2; ++dt) {
-    int nb = 1 << 30;
+    int nb = 1 << 30, nx = 1 << 30;
     for (int b1 = 0; b1 < 2; ++b1)
       for (int dm = 0; dm < 3; ++dm) {
-        int x = 0;
+        int x = 0, y = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&x, kernel_ptr(dt, b1 != 0, dm), kThreads, 0) !=
-            hipSuccess)
+                hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&y, kernel_ptr(dt, b1 != 0, dm), kThreads, kXvLds) !=
+                hipSuccess)
           return nullptr;
         nb = std::min(nb, x);
+        nx = std::min(nx, y);
       }
-    if (nb < 1) return nullptr;
+    if (nb < 1 || nx < 1) return nullptr;
     di.max_blocks[dt] = nb * di.n_cu;
+    di.max_blocks_xv[dt] = nx * di.n_cu;
   }
   di.ok = 1;
   return &di;
@@ -323,20 +337,21 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   A.epoch = next_epoch();
   // lags scale with the number of workgroups the chip holds at once
   const int ee_rows = ee ? (params->early_rows > 0 ? params->early_rows : 2) : 0;
-  if (!sched_build(B, K, L.S, di->max_blocks[dtype], A.sc, ee_rows)) return ASYMSPEC_E_ARG;
+  const int in_flight = vmap != nullptr ? di->max_blocks_xv[dtype] : di->max_blocks[dtype];
+  if (!sched_build(B, K, L.S, in_flight, A.sc, ee_rows)) return ASYMSPEC_E_ARG;
   const int grid = A.sc.total;
 
   const unsigned long long nblk = (unsigned long long)B * (K + 1) * L.S;
-  if (fused_logprobs_full != nullptr && nblk > 0xFFFFFFFFull) return ASYMSPEC_E_ARG;
+  if (fused_logprobs_full != nullptr && nblk > 0x7FFFFFFFull) return ASYMSPEC_E_ARG;
   void* args[] = {&A};
   hipError_t e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f, params->delta_mode), dim3(grid),
-                                 dim3(kThreads), args, 0, (hipStream_t)stream);
+                                 dim3(kThreads), args, vmap != nullptr ? kXvLds : 0, (hipStream_t)stream);
   if (e == hipSuccess && fused_logprobs_full != nullptr) {
     // one workgroup per (row, chunk), after the decision kernel on the stream
     float* full = fused_logprobs_full;
     void* dargs[] = {&A, &full};
-    e = hipLaunchKernel(dump_ptr(dtype, params->delta_mode), dim3((unsigned)nblk), dim3(kThreads), dargs, 0,
-                        (hipStream_t)stream);
+    e = hipLaunchKernel(dump_ptr(dtype, params->delta_mode), dim3((unsigned)nblk), dim3(kThreads), dargs,
+                        vmap != nullptr ? kXvLds : 0, (hipStream_t)stream);
   }
   if (e != hipSuccess) {
     (void)hipGetLastError();

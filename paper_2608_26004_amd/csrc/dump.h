@@ -20,6 +20,7 @@
 #define ASYMSPEC_DUMP_H_
 
 #include "device.h"
+#include "schedule.h"
 
 namespace asym {
 
@@ -36,8 +37,11 @@ __global__ __launch_bounds__(kThreads) void dump_kernel(KArgs A, float* out) {
   constexpr int VE = Elem<DT>::VE;
   constexpr int kPerThread = kChunkVec / kThreads;
   const int S = A.S, nrow = A.K + 1;
-  const int row = (int)(blockIdx.x / (unsigned)S);
-  const int m = (int)blockIdx.x - row * S;
+  // through a vocabulary map, the workgroups one XCD runs take consecutive
+  // chunks of the same rows (each chunk gathers from the whole drafter row)
+  const int b = A.vmap != nullptr ? xcd_grouped((int)blockIdx.x, (int)gridDim.x) : (int)blockIdx.x;
+  const int row = b / S;
+  const int m = b - row * S;
   const int req = row / nrow, i = row - req * nrow;
   const uint64_t* blk = A.dec + (size_t)req * (kDecHdr + (size_t)nrow * kDecRow) + kDecHdr + (size_t)i * kDecRow;
   const double c = (double)payf(blk[D_C]);
