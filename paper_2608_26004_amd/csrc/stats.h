@@ -235,10 +235,7 @@ DEV void stats_slow(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   const long long rel0 = (long long)m * kChunkVec + (long long)w * (64 * kNV) + lane;
   StatsAcc q;
   stats_init(q, g.c);
-#ifndef ASYMSPEC_SLOW_UNROLL
-#define ASYMSPEC_SLOW_UNROLL 1
-#endif
-  #pragma unroll ASYMSPEC_SLOW_UNROLL
+  #pragma unroll 1
   for (int kk = 0; kk < kNSub * kNV; ++kk) {
     const long long rv = rel0 + (long long)(kk / kNV) * kTileVec + (kk % kNV) * 64;
     const uint32_t off = (uint32_t)(rv * 16);
