@@ -17,6 +17,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -31,15 +32,23 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "fused-verify rows/s and achieved HBM GB/s (% of peak), B=128 V=151936 bf16"
 
 
+def _code_only(src: str) -> str:
+    """C++ source without comments and blank space, so that the digest moves
+    with the code and not with its prose."""
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
 def lib_digest():
-    """Digest of the library sources: traffic figures measured on other
-    sources are not reported."""
+    """Digest of the library code (comments and blank space removed):
+    traffic figures measured on other code are not reported."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_26004_amd", "csrc")
     paths = sorted(os.path.join(csrc, n) for n in os.listdir(csrc) if n.endswith((".hip", ".h")))
     for p in paths + [os.path.join(ROOT, "include", "asymspec.h")]:
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p) as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

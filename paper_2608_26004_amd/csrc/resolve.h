@@ -1,4 +1,5 @@
-// Resolve items of one request: decide, pass 2 and pick.
+// Resolve items of one request: decide, pass 2 and pick (and, with early
+// exit, the verdict on the first rows, which is a decide over those rows).
 //
 // decide  combines the chunk statistics of the request's K+1 rows into their
 //         log-normalisers, gathers the draft tokens' logits, and classifies
@@ -10,7 +11,8 @@
 //         greedy request with nothing open is finished here.
 // pass 2  one chunk of every row that needs it: the JSD partial of Eq. 3 and
 //         the four wave-segment sums of the residual max(0, p~ - q) (sampling
-//         drafts that can emit) or of the bonus weights of softmax(t_K / tau).
+//         drafts that can emit, and a fused bonus row) or of the bonus
+//         weights of softmax(t_K / tau).
 // pick    D for the open drafts, the final accept length, and the emitted
 //         token: the fused argmax (greedy, Eq. 2) or an inverse-CDF draw with
 //         the caller's uniform u_K; then every output of the request.
