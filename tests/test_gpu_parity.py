@@ -452,3 +452,58 @@ def test_many_requests(gpu):
     g = run_gpu(x)
     sample = list(range(0, 20)) + list(range(1490, 1510)) + list(range(2980, 3000))
     _note(compare(x, g, requests=sample, label="B=3000"))
+
+
+# ------------------------------------------- the emitted law, sampled --
+def _mc_rows(seed, K, V, equal_ab=False):
+    rng = np.random.default_rng(seed)
+    rows = lambda: (1.2 * rng.standard_normal((K + 1, V))).astype(np.float32)
+    t, a = rows(), rows()
+    b = a.copy() if equal_ab else rows()
+    return t, a, b
+
+
+def _mc_gpu(t, a, b, tau, n, seed, **kw):
+    x = synth.Inputs(*synth.replicate_for_mc(t, a, b, tau, n, seed=seed), rho=np.zeros(n),
+                     dtype="fp32")
+    g = run_gpu(x, want_gate=False, **kw)
+    return x, g[0], g[1]
+
+
+@pytest.mark.parametrize("gamma,mode", [(0.5, 0), (0.7, 0), (1.0, 0), (0.5, 1)])
+def test_emitted_law_monte_carlo(gpu, gamma, mode):
+    """2^20 copies of one request in one launch, each with its own drafts
+    (from q) and uniforms: the histogram of (accept_len, next_token) against
+    the closed-form law of the sampling reading (oracle/emitted_law.py, an
+    enumeration, not the oracle's sampler)."""
+    import scipy.stats as sst
+    K, V, tau = 2, 5, 0.9
+    t, a, b = _mc_rows(31 + mode, K, V)
+    x, acc, nxt = _mc_gpu(t, a, b, tau, 1 << 20, seed=5 + mode, gamma=gamma, gate_mode=mode)
+    counts = np.zeros((K + 1, V))
+    np.add.at(counts, (acc, nxt), 1)
+    P = O.emitted_law(t, a, b, tau, gamma=gamma, gate_mode=mode)
+    stat, dof = O.chi_square_stat(counts, P)
+    p = sst.chi2.sf(stat, dof)
+    n = counts.sum()
+    z = np.abs(counts - n * P) / np.sqrt(np.maximum(n * P * (1 - P), 1e-12))
+    print(f"[mc] gamma={gamma} mode={mode}: chi2 {stat:.1f} on {dof} dof, p {p:.3f}, max |z| {z.max():.2f}")
+    assert p > 1e-3 and z.max() < 5.0
+
+
+def test_speculative_sampling_theorem_on_gpu(gpu):
+    """delta = 0 (a = b) and gamma = 1: the step is speculative sampling, so
+    the first committed token follows softmax(t_0 / tau) exactly
+    (Leviathan et al., Chen et al.), checked by chi-square over 2^20 copies."""
+    import scipy.stats as sst
+    import scipy.special as sps
+    K, V, tau = 3, 6, 0.8
+    t, a, b = _mc_rows(41, K, V, equal_ab=True)
+    x, acc, nxt = _mc_gpu(t, a, b, tau, 1 << 20, seed=9, gamma=1.0)
+    first = np.where(acc >= 1, x.draft_tokens[:, 0], nxt)
+    counts = np.bincount(first, minlength=V).astype(np.float64)
+    P = sps.softmax(t[0].astype(np.float64) / tau)
+    stat, dof = O.chi_square_stat(counts, P)
+    p = sst.chi2.sf(stat, dof)
+    print(f"[mc] SD theorem: chi2 {stat:.1f} on {dof} dof, p {p:.3f}")
+    assert p > 1e-3
