@@ -507,3 +507,21 @@ def test_speculative_sampling_theorem_on_gpu(gpu):
     p = sst.chi2.sf(stat, dof)
     print(f"[mc] SD theorem: chi2 {stat:.1f} on {dof} dof, p {p:.3f}")
     assert p > 1e-3
+
+
+def test_workload_3_invariants(gpu):
+    """Properties that hold at any size, on the full bench workload: every
+    full log-probability row normalises (Eq. 2 fused target), gamma_eff lies
+    in [gamma/2, gamma] (Sec. 3.3), and the requests whose drafter views are
+    bitwise equal (even b) have D = 0 and gamma_eff = gamma exactly."""
+    import scipy.special as sps
+    x = synth.workload_inputs(3)
+    g = run_gpu(x, want_full=True)
+    acc, nxt, flp, gate, full = g
+    lse = sps.logsumexp(full.astype(np.float64), axis=-1)
+    assert np.abs(lse).max() < 1e-5, np.abs(lse).max()
+    ge = gate[..., 1]
+    assert (ge >= 0.25 - 1e-7).all() and (ge <= 0.5 + 1e-7).all()
+    even = np.arange(x.B) % 2 == 0
+    assert (gate[even, :, 0] == 0.0).all() and (gate[even, :, 1] == np.float32(0.5)).all()
+    assert (gate[~even, :, 0] > 0.0).all()
