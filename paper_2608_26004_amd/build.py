@@ -62,6 +62,23 @@ def resource_report(lines) -> str:
                    f"occupancy={r.get('Occupancy', '?')}\n" for r in rows)
 
 
+EXAMPLE_SRC = os.path.join(HERE, "examples", "fuse_verify_c.cpp")
+EXAMPLE = os.path.join(HERE, "examples", "fuse_verify_c")
+
+
+def build_example(verbose: bool = False) -> str:
+    """The C-ABI example, a host program linked against libasymspec.so."""
+    cmd = [HIPCC, "--offload-arch=gfx950", "-O2", "-std=c++17", "-I", INC, EXAMPLE_SRC,
+           "-L", HERE, "-lasymspec", f"-Wl,-rpath,{HERE}", "-o", EXAMPLE]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"example build failed ({r.returncode}):\n{r.stdout}{r.stderr}")
+    if verbose:
+        print(f"built {EXAMPLE}")
+    return EXAMPLE
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    build_example(verbose=True)
     sys.exit(0)

@@ -525,3 +525,36 @@ def test_workload_3_invariants(gpu):
     even = np.arange(x.B) % 2 == 0
     assert (gate[even, :, 0] == 0.0).all() and (gate[even, :, 1] == np.float32(0.5)).all()
     assert (gate[~even, :, 0] > 0.0).all()
+
+
+# ------------------------------------------------- a C caller, no Python --
+def test_c_abi_example_program(gpu, tmp_path):
+    """The example program calls the C ABI directly (hipMalloc, upload,
+    asymspec_fuse_verify on its own stream, synchronise); its outputs match
+    the oracle."""
+    import os
+    import subprocess
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    exe = os.path.join(root, "paper_2608_26004_amd", "examples", "fuse_verify_c")
+    if not os.path.exists(exe):
+        pytest.fail("the example program is not built (run __graft_entry__.build())")
+    x = synth.generate(B=6, K=3, V=5003, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=2024)
+    inp, out = tmp_path / "in.bin", tmp_path / "out.bin"
+    with open(inp, "wb") as f:
+        np.array([x.B, x.K, x.V, 0], np.int32).tofile(f)
+        for arr in (x.t, x.a, x.b):
+            np.ascontiguousarray(arr).tofile(f)
+        x.draft_tokens.astype(np.int32).tofile(f)
+        x.draft_probs.astype(np.float32).tofile(f)
+        x.uniforms.astype(np.float32).tofile(f)
+        x.temperature.astype(np.float32).tofile(f)
+    r = subprocess.run([exe, str(inp), str(out)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    raw = np.fromfile(out, np.uint8)
+    B, K = x.B, x.K
+    acc = raw[:4 * B].view(np.int32)
+    nxt = raw[4 * B:8 * B].view(np.int32)
+    flp = raw[8 * B:8 * B + 4 * B * (K + 1)].view(np.float32).reshape(B, K + 1)
+    gate = raw[8 * B + 4 * B * (K + 1):].view(np.float32).reshape(B, K, 2)
+    _note(compare(x, [acc, nxt, flp, gate], label="C example"))
