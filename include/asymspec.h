@@ -204,6 +204,7 @@ int asymspec_fuse_verify(const void* verifier_logits,
  *                       verifier token x, or -1 when x has no shared counterpart
  *                       (entries outside [0, Vd) count as -1); 4-byte aligned
  *   Vd                  drafter vocabulary size, B*(K+1)*Vd < 2^40
+ *   workspace           >= asymspec_workspace_size_xvocab(B, K, V, Vd, dtype) bytes
  *   draft_tokens        verifier ids of the drafts
  *   everything else     as for asymspec_fuse_verify
  *
@@ -214,8 +215,13 @@ int asymspec_fuse_verify(const void* verifier_logits,
  * target and proposal, the emission and the bonus token.  Drafter tokens
  * that no verifier token maps to are never read.  A draft outside the set has
  * no mass in any view and is rejected.  The drafter rows are gathered element
- * by element (a map is in general no permutation of contiguous runs).
+ * by element (a map is in general no permutation of contiguous runs); when
+ * no two verifier tokens share a drafter id, rows with no argmax to find read
+ * the drafter rows in their own order and gather t instead.
  */
+/* Workspace bytes of asymspec_fuse_verify_xvocab (0 for invalid arguments). */
+size_t asymspec_workspace_size_xvocab(int B, int K, int V, int Vd, int dtype);
+
 int asymspec_fuse_verify_xvocab(const void* verifier_logits,
                                 const void* drafter_full_logits,
                                 const void* drafter_comp_logits,

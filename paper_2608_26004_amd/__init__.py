@@ -72,6 +72,8 @@ def load_library(path: str | None = None):
     lib.asymspec_fuse_verify_xvocab.argtypes = [vp, vp, vp, i32, vp, i32, vp, vp, vp, vp, i32, i32, i32,
                                                 ctypes.POINTER(_Params), vp, vp, vp, vp, vp, vp, sz, vp]
     lib.asymspec_fuse_verify_xvocab.restype = i32
+    lib.asymspec_workspace_size_xvocab.argtypes = [i32, i32, i32, i32, i32]
+    lib.asymspec_workspace_size_xvocab.restype = sz
     lib.asymspec_status_string.argtypes = [i32]
     lib.asymspec_status_string.restype = ctypes.c_char_p
     lib.asymspec_version.argtypes = []
@@ -184,7 +186,8 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     else:
         acc, nxt, flp, gate = out[:4]
         full = out[4] if len(out) > 4 else None
-    ws_bytes = workspace_size(B, K, V, dt)
+    ws_bytes = (workspace_size(B, K, V, dt) if vocab_map is None
+                else int(lib.asymspec_workspace_size_xvocab(B, K, V, Vd, dt)))
     if ws_bytes == 0:
         raise AsymSpecError(E_ARG, "invalid shape")
     if workspace is None:

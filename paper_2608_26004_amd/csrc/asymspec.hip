@@ -115,6 +115,20 @@ void fuse_verify_kernel(KArgs A) {
   }
 }
 
+// The drafter-to-verifier map of a cross-family call: inv[j] = x for the
+// verifier token x with vmap[x] = j, else -1; inv[Vd] is set when two
+// verifier tokens name the same drafter id (the map is then not used).
+__global__ void inv_clear_kernel(int32_t* inv, int Vd) {
+  for (int j = blockIdx.x * blockDim.x + threadIdx.x; j <= Vd; j += gridDim.x * blockDim.x)
+    inv[j] = j < Vd ? -1 : 0;
+}
+__global__ void inv_fill_kernel(const int32_t* vmap, int V, int32_t* inv, int Vd) {
+  for (int x = blockIdx.x * blockDim.x + threadIdx.x; x < V; x += gridDim.x * blockDim.x) {
+    const int j = vmap[x];
+    if (j >= 0 && j < Vd && atomicCAS(&inv[j], -1, x) != -1) inv[Vd] = 1;
+  }
+}
+
 __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     p[i] = 0u;
@@ -124,19 +138,23 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
 struct Layout {
   int S, VE;
   size_t rows;
-  size_t off_rec1, off_dec, off_rec2, off_err, total;
+  size_t off_rec1, off_dec, off_rec2, off_err, off_inv, total;
 };
 
 static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-static bool make_layout(int B, int K, int V, int dtype, Layout& L) {
-  if (B < 1 || K < 0 || K > kMaxK || V < 1) return false;
+// Vd > 0: a drafter vocabulary of Vd tokens (cross-family calls); rows then
+// have as many chunks as the longer of the two vocabularies needs, and the
+// workspace holds the drafter-to-verifier map.
+static bool make_layout(int B, int K, int V, int dtype, Layout& L, int Vd = 0) {
+  if (B < 1 || K < 0 || K > kMaxK || V < 1 || Vd < 0) return false;
   if (dtype != ASYMSPEC_BF16 && dtype != ASYMSPEC_FP32) return false;
   const long double elems = (long double)B * (K + 1) * V;
   if (elems >= (long double)(1ull << 40)) return false;
+  if ((long double)B * (K + 1) * Vd >= (long double)(1ull << 40)) return false;
   L.VE = dtype == ASYMSPEC_BF16 ? 8 : 4;
   // a row spans at most this many 16-byte vectors (it may start mid-vector)
-  const long long nvec_max = ((long long)V + 2LL * L.VE - 2) / L.VE;
+  const long long nvec_max = ((long long)(V > Vd ? V : Vd) + 2LL * L.VE - 2) / L.VE;
   const long long S = (nvec_max + kChunkVec - 1) / kChunkVec;
   // a request's decision combines each row's chunks in one workgroup pass
   if (S > kThreads) return false;
@@ -147,6 +165,8 @@ static bool make_layout(int B, int K, int V, int dtype, Layout& L) {
   L.off_dec = off;  off = align_up(off + (size_t)B * (kDecHdr + (size_t)(K + 1) * kDecRow) * 8, 256);
   L.off_rec2 = off; off = align_up(off + L.rows * L.S * kR2 * 8, 256);
   L.off_err = off;  off = align_up(off + 8, 256);
+  // cross-family: inverse map [Vd] and its duplicate flag
+  L.off_inv = off;  off = align_up(off + (Vd > 0 ? (size_t)Vd * 4 + 4 : 0), 256);
   L.total = off;
   return true;
 }
@@ -258,6 +278,12 @@ size_t asymspec_workspace_size(int B, int K, int V, int dtype) {
   return L.total;
 }
 
+size_t asymspec_workspace_size_xvocab(int B, int K, int V, int Vd, int dtype) {
+  Layout L;
+  if (Vd < 1 || !make_layout(B, K, V, dtype, L, Vd)) return 0;
+  return L.total;
+}
+
 int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stream) {
   if (workspace == nullptr || workspace_bytes % 4 != 0 || !aligned(workspace, 4)) return ASYMSPEC_E_ARG;
   if (workspace_bytes == 0) return ASYMSPEC_OK;
@@ -278,7 +304,8 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
                             void* workspace, size_t workspace_bytes, void* stream) {
   Layout L;
   if (params == nullptr) return ASYMSPEC_E_ARG;
-  if (!make_layout(B, K, V, dtype, L)) return ASYMSPEC_E_ARG;
+  if (vmap != nullptr && Vd < 1) return ASYMSPEC_E_ARG;
+  if (!make_layout(B, K, V, dtype, L, vmap != nullptr ? Vd : 0)) return ASYMSPEC_E_ARG;
   if (t == nullptr || uniforms == nullptr || temperature == nullptr || accept_len == nullptr ||
       next_token == nullptr || fused_logprobs == nullptr || workspace == nullptr)
     return ASYMSPEC_E_ARG;
@@ -332,6 +359,7 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   A.fuse_bonus = fb ? 1 : 0;
   A.vmap = vmap;
   A.Vd = vmap != nullptr ? Vd : V;
+  A.inv = vmap != nullptr ? (const int32_t*)(ws + L.off_inv) : nullptr;
   A.lam = params->gate_mode == ASYMSPEC_GATE_LAMBDA ? params->lambda : 0.0f;
   A.ln_gamma = std::log((double)params->gamma);
   A.epoch = next_epoch();
@@ -343,8 +371,20 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
 
   const unsigned long long nblk = (unsigned long long)B * (K + 1) * L.S;
   if (fused_logprobs_full != nullptr && nblk > 0x7FFFFFFFull) return ASYMSPEC_E_ARG;
+  hipError_t e = hipSuccess;
+  if (vmap != nullptr) {
+    // the drafter-to-verifier map, rebuilt for every call (the caller's map
+    // may change between calls)
+    int32_t* inv = (int32_t*)(ws + L.off_inv);
+    const int nb_d = (int)std::min<long long>((Vd + 1 + 255) / 256, 4096);
+    const int nb_v = (int)std::min<long long>((V + 255) / 256, 4096);
+    hipLaunchKernelGGL(inv_clear_kernel, dim3(nb_d), dim3(256), 0, (hipStream_t)stream, inv, Vd);
+    hipLaunchKernelGGL(inv_fill_kernel, dim3(nb_v), dim3(256), 0, (hipStream_t)stream, vmap, V, inv, Vd);
+    e = hipGetLastError();
+    if (e != hipSuccess) return ASYMSPEC_E_DEVICE;
+  }
   void* args[] = {&A};
-  hipError_t e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f, params->delta_mode), dim3(grid),
+  e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f, params->delta_mode), dim3(grid),
                                  dim3(kThreads), args, vmap != nullptr ? kXvLds : 0, (hipStream_t)stream);
   if (e == hipSuccess && fused_logprobs_full != nullptr) {
     // one workgroup per (row, chunk), after the decision kernel on the stream

@@ -115,6 +115,10 @@ struct KArgs {
   // >= Vd: not shared); null when both sides share one vocabulary
   const int32_t* vmap;
   int Vd;
+  // the drafter-to-verifier map built from vmap for this call ([Vd], then a
+  // word that is non-zero when two verifier tokens share a drafter id), or
+  // null
+  const int32_t* inv;
   double ln_gamma;
   uint32_t epoch;
   Sched sc;
@@ -629,6 +633,12 @@ DEV void map_vecs(const KArgs& A, const RowGeo& g, long long vi, u4& vt, u4& va,
   vt = t2;
   if (ab) { va = a2; vb = b2; }
 }
+// True when the drafter-to-verifier map of this call is usable (every shared
+// drafter id belongs to one verifier token).  Wave-uniform.
+DEV bool inv_ok(const KArgs& A) {
+  return A.inv != nullptr && ((cptr32)(const void*)A.inv)[A.Vd] == 0u;
+}
+
 // The three logits of verifier token x (0 <= x < V) of row g, mapped.
 template <int DT>
 DEV void mapped_tab(const KArgs& A, const RowGeo& g, int x, float& t, float& a, float& b) {

@@ -313,10 +313,69 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   return true;
 }
 
+// Cross-family vocabularies, rows with no argmax to find (sampling drafts and
+// a sampling fused bonus row): the drafter rows are read in their own order,
+// contiguously, and t is gathered through the drafter-to-verifier map, so a
+// shared token costs one gather instead of two (a and b through the
+// verifier-to-drafter map) and the gathers hit the shorter verifier row.
+// The statistics are the same sums over the shared set in another order;
+// chunk m covers drafter vectors [m * kChunkVec, (m+1) * kChunkVec).
+template <int DT, int KIND, bool kB1, int DM>
+DEV void stats_dorder(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
+  constexpr int VE = Elem<DT>::VE;
+  constexpr int ES = 16 / VE;
+  const int lane = lane_id(), w = wave_id();
+  const long long e0d = (long long)g.row * A.Vd;
+  const long long vbeg = e0d / VE, vend = (e0d + A.Vd + VE - 1) / VE;
+  const unsigned long long dbytes = (unsigned long long)A.B * (A.K + 1) * (unsigned long long)A.Vd * ES;
+  unsigned long long span = (unsigned long long)(vend - vbeg) * 16ull;
+  if (span > dbytes - (unsigned long long)vbeg * 16ull) span = dbytes - (unsigned long long)vbeg * 16ull;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc((const char*)A.a + vbeg * 16, span);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc((const char*)A.b + vbeg * 16, span);
+  const long long last_full = (long long)(dbytes / 16ull), n_el = (long long)(dbytes / ES);
+  const long long rel0 = (long long)m * kChunkVec + (long long)w * (64 * kNV) + lane;
+  StatsAcc q;
+  stats_init(q, g.c);
+  #pragma unroll 1
+  for (int kk = 0; kk < kNSub * kNV; ++kk) {
+    const long long rv = rel0 + (long long)(kk / kNV) * kTileVec + (kk % kNV) * 64;
+    const long long vi = vbeg + rv;
+    const uint32_t off = (uint32_t)(rv * 16);
+    u4 va = buf_load_nt(ra, off), vb = buf_load_nt(rb, off);
+    u4 t2 = {0, 0, 0, 0}, a2 = t2, b2 = t2;
+    #pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      const long long jg = vi * VE + e;            // flat drafter index
+      const long long jr = jg - e0d;               // drafter id in the row
+      float xt = -INFINITY, xa = -INFINITY, xb = -INFINITY;
+      const int x = (jr >= 0 && jr < A.Vd) ? A.inv[jr] : -1;
+      if (x >= 0 && x < A.V) {
+        xt = Elem<DT>::load_one(A.t, g.e0 + x);
+        if (vi >= last_full && jg < n_el) {       // the partial vector at the array end
+          xa = Elem<DT>::load_one(A.a, jg);
+          xb = Elem<DT>::load_one(A.b, jg);
+        } else {
+          xa = Elem<DT>::get(va, e);
+          xb = Elem<DT>::get(vb, e);
+        }
+      }
+      Elem<DT>::put_one(t2, e, xt);
+      Elem<DT>::put_one(a2, e, xa);
+      Elem<DT>::put_one(b2, e, xb);
+    }
+    stats_vec<DT, KIND, kB1, DM, true>(A, g.c, t2, a2, b2, kk, q);
+  }
+  publish_stats<DT, KIND, DM>(A, g, m, rel0, q, sm);
+}
+
 template <int DT, int KIND, bool kB1, int DM>
 DEV void stats_item(const KArgs& A, int row, int m, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
   const RowGeo g = row_geo<DT>(A, row);
+  if (!KindTraits<KIND>::kArg && KindTraits<KIND>::NS == 3 && A.vmap != nullptr && inv_ok(A)) {
+    stats_dorder<DT, KIND, kB1, DM>(A, g, m, sm);
+    return;
+  }
   const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
   bool done = false;
   if (A.vmap == nullptr && !has_tail(A, c0, c1)) {

@@ -128,7 +128,8 @@ def _call_xv(**over):
               B=2, K=2, V=64, acc=fake, nxt=fake, flp=fake, gate=None, full=None, ws=fake, wsb=None)
     kw.update(over)
     if kw["wsb"] is None:
-        kw["wsb"] = asp.workspace_size(max(kw["B"], 1), max(kw["K"], 0), max(kw["V"], 1), 0) or 1 << 20
+        kw["wsb"] = lib.asymspec_workspace_size_xvocab(max(kw["B"], 1), max(kw["K"], 0), max(kw["V"], 1),
+                                                       max(kw["Vd"], 1), 0) or 1 << 20
     p = asp._Params(1.0, 0.5, 0, 0, 0, 0.1, 0)
     return lib.asymspec_fuse_verify_xvocab(kw["t"], kw["a"], kw["b"], kw["dtype"], kw["vm"], kw["Vd"],
                                            kw["d"], kw["dp"], kw["u"], kw["tau"], kw["B"], kw["K"], kw["V"],
@@ -171,3 +172,16 @@ def test_kernels_do_not_spill():
     for r in rows:
         kv = dict(x.split("=") for x in r[1:])
         assert kv["scratch"] == "0", r
+
+
+def test_xvocab_workspace_size():
+    """The cross-family workspace holds the drafter-to-verifier map and rows
+    of as many chunks as the longer vocabulary needs."""
+    lib = asp.load_library()
+    plain = asp.workspace_size(128, 6, 151936, asp.BF16)
+    small = lib.asymspec_workspace_size_xvocab(128, 6, 151936, 128256, asp.BF16)
+    big = lib.asymspec_workspace_size_xvocab(128, 6, 151936, 262144, asp.BF16)
+    assert small >= plain + 128256 * 4 and big > small
+    assert lib.asymspec_workspace_size_xvocab(128, 6, 151936, 0, asp.BF16) == 0
+    assert lib.asymspec_workspace_size_xvocab(1, 1, 10, 4194298, asp.BF16) == 0   # > 256 chunks
+    assert _call_xv(wsb=asp.workspace_size(2, 2, 64, 0)) == asp.E_WORKSPACE

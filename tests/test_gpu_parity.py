@@ -558,3 +558,32 @@ def test_c_abi_example_program(gpu, tmp_path):
     flp = raw[8 * B:8 * B + 4 * B * (K + 1)].view(np.float32).reshape(B, K + 1)
     gate = raw[8 * B + 4 * B * (K + 1):].view(np.float32).reshape(B, K, 2)
     _note(compare(x, [acc, nxt, flp, gate], label="C example"))
+
+
+def test_xvocab_duplicate_map_entries(gpu):
+    """Two verifier tokens naming the same drafter id (not a string-identical
+    alignment, but a valid map): both take that drafter token's logits; the
+    drafter-order path is not usable then and the verifier-order gathers
+    give the oracle's result."""
+    from parity_util import make_xvocab
+    x = synth.generate(B=5, K=3, V=3000, dtype="bf16", rho=("uniform", 0.0, 2.0), tau=1.0, seed=17)
+    ad, bd, vm, mx = make_xvocab(x, 2500, 0.8, seed=2)
+    shared = np.nonzero(vm >= 0)[0]
+    vm = vm.copy()
+    vm[shared[1::7]] = vm[shared[0::7][:len(shared[1::7])]]     # duplicates
+    mx.t, mx.a, mx.b = O.map_to_verifier(x.t, ad, bd, vm)
+    g = run_gpu(mx, vocab=(ad, bd, vm))
+    _note(compare(mx, g, label="xvocab duplicate map entries"))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_xvocab_drafter_vocabulary_longer(gpu, dtype):
+    """A drafter vocabulary much longer than the verifier's: rows take as
+    many chunks as the drafter rows need."""
+    from parity_util import make_xvocab
+    x = synth.generate(B=4, K=3, V=3000, dtype=dtype, rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 1.0, 0.7), seed=18)
+    ad, bd, vm, mx = make_xvocab(x, 40000, 0.9, seed=3)
+    g = run_gpu(mx, vocab=(ad, bd, vm), want_full=True, fuse_bonus=True)
+    _note(compare(mx, g, fuse_bonus=True, label=f"xvocab Vd=40000 {dtype}"))
+    compare_full(mx, g[4], fuse_bonus=True, label="xvocab Vd=40000 full")
