@@ -98,10 +98,12 @@ class SpecDecoder:
 
     def __init__(self, models: TableModels, B: int, K: int, temperature, beta: float = 1.0,
                  gamma: float = 0.5, gate_mode: int = 0, seed: int = 0, backend: str = "hip",
-                 step_fn=None, device=None):
+                 step_fn=None, device=None, early_exit: int = 0, fuse_bonus: bool = False):
         self.m, self.B, self.K = models, B, K
         self.tau = np.broadcast_to(np.asarray(temperature, np.float32), (B,)).copy()
         self.beta, self.gamma, self.gate_mode = beta, gamma, gate_mode
+        self.early_exit, self.fuse_bonus = early_exit, fuse_bonus
+        self.call_seconds = []
         self.rng = np.random.default_rng(seed)
         self.h = roll(np.zeros(B, np.int64), np.arange(B))     # distinct start contexts
         self.tokens = [[] for _ in range(B)]
@@ -147,11 +149,15 @@ class SpecDecoder:
             torch = self._torch
             ii = torch.from_numpy(idx).to(self.device)
             t, a, b = (x.index_select(0, ii).view(B, K + 1, self.m.V) for x in self.m.dev)
+            dd, qq, uu = (torch.from_numpy(v).to(self.device) for v in (d, q, u))
+            torch.cuda.synchronize(self.device)
+            t0 = time.perf_counter()
             acc, nxt, _ = self._asp.fuse_verify(
-                t, a, b, torch.from_numpy(d).to(self.device), torch.from_numpy(q).to(self.device),
-                torch.from_numpy(u).to(self.device), self._tau_dev, beta=self.beta, gamma=self.gamma,
-                gate_mode=self.gate_mode, workspace=self._ws)
+                t, a, b, dd, qq, uu, self._tau_dev, beta=self.beta, gamma=self.gamma,
+                gate_mode=self.gate_mode, workspace=self._ws, early_exit=self.early_exit,
+                fuse_bonus=self.fuse_bonus)
             acc, nxt = acc.cpu().numpy(), nxt.cpu().numpy()
+            self.call_seconds.append(time.perf_counter() - t0)
         else:
             t, a, b = (x[idx].reshape(B, K + 1, self.m.V) for x in self.m.host)
             acc, nxt = self.step_fn(t, a, b, d, q, u, self.tau)
@@ -171,10 +177,16 @@ class SpecDecoder:
 
     def report(self):
         n = self.steps * self.B
-        return {"steps": self.steps, "requests": self.B, "K": self.K,
-                "AR": self.accepted / self.evaluated if self.evaluated else float("nan"),
-                "MAL": self.committed / n if n else float("nan"),
-                "tokens": self.committed}
+        rep = {"steps": self.steps, "requests": self.B, "K": self.K,
+               "AR": self.accepted / self.evaluated if self.evaluated else float("nan"),
+               "MAL": self.committed / n if n else float("nan"),
+               "tokens": self.committed}
+        if self.backend == "hip" and len(self.call_seconds) > 1:
+            # host-observed latency of the decision call (median, first call
+            # excluded): argument checks, launch, the kernel, and the copy of
+            # accept_len and next_token back
+            rep["decision_call_us"] = 1e6 * float(np.median(self.call_seconds[1:]))
+        return rep
 
 
 def main(argv=None):
@@ -190,12 +202,15 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--dtype", choices=[synth.BF16, synth.FP32], default=synth.BF16)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--gate", choices=["cda", "fixed", "kl", "lambda"], default="cda")
+    ap.add_argument("--early-exit", type=int, default=0)
     args = ap.parse_args(argv)
     import torch
     dev = torch.device("cuda")
     models = TableModels(args.V, R=args.R, rho=args.rho, dtype=args.dtype, seed=args.seed, device=dev)
+    gm = {"cda": 0, "fixed": 1, "kl": 2, "lambda": 3}[args.gate]
     dec = SpecDecoder(models, args.B, args.K, args.tau, beta=args.beta, gamma=args.gamma,
-                      seed=args.seed + 1, device=dev)
+                      gate_mode=gm, seed=args.seed + 1, device=dev, early_exit=args.early_exit)
     t0 = time.perf_counter()
     for _ in range(args.steps):
         dec.step()
@@ -203,7 +218,7 @@ def main(argv=None):
     wall = time.perf_counter() - t0
     rep = dec.report()
     rep.update({"V": args.V, "tau": args.tau, "beta": args.beta, "gamma": args.gamma,
-                "rho": args.rho, "wall_s": wall})
+                "rho": args.rho, "gate": args.gate, "early_exit": args.early_exit, "wall_s": wall})
     print(json.dumps(rep))
 
 
