@@ -114,7 +114,10 @@ typedef struct asymspec_params {
  * (0 for invalid arguments).  The workspace needs no initialisation and may be
  * reused across calls of any shape: every record the kernel exchanges between
  * workgroups is tagged with a per-call epoch.
- * Calls that may run at the same time need distinct workspaces. */
+ * Calls that may run at the same time need distinct workspaces.
+ * The epoch is a launch argument chosen on the host at each call, so a call
+ * must not be captured into a HIP graph and replayed: every replay would
+ * reuse one epoch and could take the previous replay's records for its own. */
 size_t asymspec_workspace_size(int B, int K, int V, int dtype);
 
 /* Zero-fill a workspace on `stream` with a fill kernel (never required for
