@@ -20,11 +20,13 @@ namespace asym {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+// A chunk is 2048 vectors (32 KiB of bf16).  One sub-tile of 8 vectors per
+// thread measured 2% faster than two of 4 on the bench workload.
 #ifndef ASYMSPEC_NV
-#define ASYMSPEC_NV 4
+#define ASYMSPEC_NV 8
 #endif
 #ifndef ASYMSPEC_NSUB
-#define ASYMSPEC_NSUB 2
+#define ASYMSPEC_NSUB 1
 #endif
 constexpr int kNV = ASYMSPEC_NV;                // 16-byte vectors per thread per sub-tile
 constexpr int kNSub = ASYMSPEC_NSUB;            // sub-tiles per statistics item

@@ -11,7 +11,8 @@
 // Layout: chunk m of a row covers its vectors [m * kChunkVec, (m+1) *
 // kChunkVec); sub-tile s holds kTileVec of them, wave w a run of 64 * kNV and
 // lane l every 64th from there, so each load instruction of a wave reads 1 KiB
-// of contiguous memory.  Sub-tile s + 1 is loaded while sub-tile s is reduced.
+// of contiguous memory.  A rolling window keeps the next vectors of every
+// stream in flight while the current one is reduced.
 
 #ifndef ASYMSPEC_STATS_H_
 #define ASYMSPEC_STATS_H_
