@@ -393,11 +393,6 @@ DEV int wave_min_i(int x) {
   x = min(x, dppi<0x143, 0xC>(x));
   return __builtin_amdgcn_readlane(x, 63);
 }
-DEV float wave_max_all(float x) {   // maximum over lanes, in every lane
-  #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
-  return x;
-}
 DEV double wave_sum_d(double x) {    // fp64 sum over lanes, in every lane
   #pragma unroll
   for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);

@@ -62,16 +62,6 @@ constexpr int vec_rel(int j) { return (j / kNV) * kTileVec + (j % kNV) * 64; }
 #endif
 constexpr int kWin = ASYMSPEC_WIN;   // vectors per stream in flight per thread
 
-template <int DT, int NS>
-DEV void load_tile(const __amdgpu_buffer_rsrc_t (&r)[3], uint32_t off0, u4 (&buf)[3][kNV]) {
-  #pragma unroll
-  for (int k = 0; k < kNV; ++k) {
-    const uint32_t off = off0 + (uint32_t)(k * 64 * 16);
-    #pragma unroll
-    for (int s = 0; s < NS; ++s) buf[s][k] = buf_load_nt(r[s], off);
-  }
-}
-
 // Per-slot accumulators of one thread.
 struct StatsAcc {
   Acc T, A, B, F, AT;
