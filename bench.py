@@ -29,6 +29,8 @@ sys.path.insert(0, ROOT)
 from paper_2608_26004_amd import synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+# inputs rotated per step: 4x the 256 MB Infinity Cache, so every step reads cold
+COLD_BYTES = 1 << 30
 METRIC = "fused-verify rows/s and achieved HBM GB/s (% of peak), B=128 V=151936 bf16"
 
 
@@ -45,7 +47,9 @@ def lib_digest():
     traffic figures measured on other code are not reported."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_26004_amd", "csrc")
-    paths = sorted(os.path.join(csrc, n) for n in os.listdir(csrc) if n.endswith((".hip", ".h")))
+    # every source of libasymspec.so (the read-ceiling probe is its own library)
+    paths = sorted(os.path.join(csrc, n) for n in os.listdir(csrc)
+                   if n.endswith((".hip", ".h")) and n != "probe.hip")
     for p in paths + [os.path.join(ROOT, "include", "asymspec.h")]:
         with open(p) as f:
             h.update(_code_only(f.read()).encode())
@@ -180,8 +184,12 @@ def main():
                          "`bench.py --calibrate-copy` into profiles/traffic_<workload>.json")
     ap.add_argument("--gen-workers", type=int, default=None,
                     help="processes for the input generator (1 under a profiler)")
-    ap.add_argument("--copies", type=int, default=2,
-                    help="distinct input copies rotated between steps (cold cache)")
+    ap.add_argument("--copies", type=int, default=None,
+                    help="distinct input copies rotated between steps; default: enough for "
+                         "1 GiB of inputs (at least 2), so that every step reads cold inputs "
+                         "past the 256 MB Infinity Cache")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the read-ceiling probe (plain read-reduce over 2 GiB)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "runs on one GPU only: the step shards by request with no "
@@ -229,7 +237,11 @@ def main():
         del ad, bd
     else:
         base = [dev_tensor(v) for v in (x.t, x.a, x.b)]
-    copies = [base] + [[v.clone() for v in base] for _ in range(max(0, args.copies - 1))]
+    n_copies = args.copies
+    if n_copies is None:
+        per_copy = sum(v.numel() * v.element_size() for v in base)
+        n_copies = min(1024, max(2, -(-COLD_BYTES // per_copy)))
+    copies = [base] + [[v.clone() for v in base] for _ in range(max(0, n_copies - 1))]
     d = dev_tensor(x.draft_tokens)
     q = dev_tensor(x.draft_probs)
     u = dev_tensor(x.uniforms)
@@ -285,6 +297,14 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    ceiling = None
+    if not args.no_ceiling:
+        from paper_2608_26004_amd import probe
+        ceiling = probe.read_ceiling(device=dev)
+        ceiling["kernel"] = "read_reduce_kernel (libasymspec_probe.so), 16-byte nt loads"
+        print(f"[bench] read ceiling {ceiling['GBps']:.0f} GB/s over {ceiling['bytes']} B "
+              f"({ceiling['nblocks']} workgroups)", file=sys.stderr, flush=True)
+
     acc = outs[0].cpu().numpy()
     if args.early_exit and args.early_exit <= K:
         # bytes actually read: requests with a sure rejection in their first
@@ -333,7 +353,11 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel_ms_mean": kern_ms, "kernel_ms_p10": float(np.percentile(per, 10)),
                      "kernel_ms_p90": float(np.percentile(per, 90)),
-                     "bytes_per_launch": nbytes},
+                     "bytes_per_launch": nbytes,
+                     "frac_of_read_ceiling": (achieved / ceiling["GBps"]) if ceiling else None},
+        "read_ceiling": ({"GBps": ceiling["GBps"], "frac_of_peak": ceiling["GBps"] / HBM_PEAK_GBS,
+                          "bytes": ceiling["bytes"], "nblocks": ceiling["nblocks"],
+                          "kernel": ceiling["kernel"]} if ceiling else None),
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

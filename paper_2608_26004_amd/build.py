@@ -78,7 +78,25 @@ def build_example(verbose: bool = False) -> str:
     return EXAMPLE
 
 
+PROBE_SRC = os.path.join(HERE, "csrc", "probe.hip")
+PROBE = os.path.join(HERE, "libasymspec_probe.so")
+
+
+def build_probe(verbose: bool = False) -> str:
+    """libasymspec_probe.so: the read-ceiling probe (not the decision step)."""
+    tmp = PROBE + ".tmp"
+    cmd = [HIPCC, *FLAGS, "-I", INC, PROBE_SRC, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"probe build failed ({r.returncode}):\n{r.stdout}{r.stderr}")
+    os.replace(tmp, PROBE)
+    if verbose:
+        print(f"built {PROBE}")
+    return PROBE
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
     build_example(verbose=True)
+    build_probe(verbose=True)
     sys.exit(0)
