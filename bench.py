@@ -90,10 +90,34 @@ def cpu_baseline(x, max_requests, min_seconds):
             if wall >= min_seconds:
                 break
     rows = done * (x.K + 1)
+    # one process for comparison, a quarter of the time (at least one request)
+    t1 = time.perf_counter()
+    done1 = 0
+    while True:
+        done1 += _oracle_worker([done1 % n])
+        wall1 = time.perf_counter() - t1
+        if wall1 >= min_seconds / 4:
+            break
+    per_req = x.nbytes_read() / x.B
     return dict(value=rows / wall, unit="rows/s", cores=cores, kind="oracle",
                 sample=f"{passes} pass(es) over {n} of {x.B} requests ({rows} rows) of the same "
                        f"workload, fp64 NumPy oracle, fork pool of {cores} processes, "
-                       f"wall {wall:.1f} s")
+                       f"wall {wall:.1f} s",
+                GBps=done * per_req / wall / 1e9,
+                value_1proc=done1 * (x.K + 1) / wall1,
+                sample_1proc=f"{done1} request(s) in one process, wall {wall1:.1f} s",
+                cpu_model=_cpu_model())
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 # ----------------------------------------------------------- HBM traffic --
