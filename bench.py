@@ -375,7 +375,8 @@ def main():
         "hbm_GBps": achieved,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel_ms_mean": kern_ms, "kernel_ms_p10": float(np.percentile(per, 10)),
+                     "kernel_ms_mean": kern_ms, "kernel_ms_median": float(np.median(per)),
+                     "kernel_ms_p10": float(np.percentile(per, 10)),
                      "kernel_ms_p90": float(np.percentile(per, 90)),
                      "bytes_per_launch": nbytes,
                      "frac_of_read_ceiling": (achieved / ceiling["GBps"]) if ceiling else None},
