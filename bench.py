@@ -179,9 +179,10 @@ COPY_BYTES = 1 << 30
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    # the clocks settle after a few hundred back-to-back calls (about 50 ms)
-    ap.add_argument("--warmup", type=int, default=300)
+    ap.add_argument("--steps", type=int, default=500)
+    # the clocks settle after a few hundred back-to-back calls (about 50 ms);
+    # a longer warm-up and more timed calls keep box-to-box noise out of the mean
+    ap.add_argument("--warmup", type=int, default=1000)
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--gate", action="store_true", help="also return (D, gamma_eff) per row")
     ap.add_argument("--gate-mode", choices=["cda", "fixed", "kl", "lambda"], default="cda",
