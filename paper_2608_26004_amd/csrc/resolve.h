@@ -472,11 +472,14 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
 // kKL: the divergence term is KL's (the KL gate) rather than the JSD's.
 // kNb: a and b differ somewhere in the row; otherwise b is a bitwise copy of
 // a and a's vectors stand in for it (such a row has no divergence task).
-template <int DT, int kMode, int DM, bool kKL, bool kNb>
-DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bool dr, bool db,
+template <int DT, int kMode, int DM, bool kKL, bool kNb, bool kResOnly = false>
+DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj_in, bool dr_in, bool db_in,
                     const ResidConst& rk, const JsdConst& jk, float& accj, float& seg) {
   constexpr int VE = Elem<DT>::VE;
   constexpr int kG = kMode == 2 ? 1 : 4;      // vectors per group
+  // kResOnly: the row's only task is the residual (the usual emitting row),
+  // an instance without the other tasks' code
+  const bool dj = kResOnly ? false : dj_in, dr = kResOnly ? true : dr_in, db = kResOnly ? false : db_in;
   const bool nt = dr || db, nab = dj || dr;
   const __amdgpu_buffer_rsrc_t rt = row_rsrc(A, A.t, g);
   const __amdgpu_buffer_rsrc_t ra = row_rsrc(A, nab ? A.a : A.t, g);
@@ -508,20 +511,35 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj, bo
         }
       }
       if (!kNb) vb[k] = va[k];
-      float vj[VE], vr[VE];
-      #pragma unroll
-      for (int e = 0; e < VE; ++e) {
-        const float xa = Elem<DT>::get(va[k], e), xb = Elem<DT>::get(vb[k], e);
-        const float xt = Elem<DT>::get(vt[k], e);
-        vj[e] = dj ? (kKL ? kl_elem(xa, xb, jk) : jsd_elem(xa, xb, jk)) : 0.0f;
-        vr[e] = dr ? resid_elem<DM>(xt, xa, xb, rk) : (db ? bonus_elem(xt, rk.c, rk.Rf) : 0.0f);
-      }
-      #pragma unroll
-      for (int st = 1; st < VE; st <<= 1)
+      // each task's element terms under its own (uniform) branch, so that a
+      // row without a task never evaluates that task's terms
+      if (dj) {
+        float vj[VE];
         #pragma unroll
-        for (int e = 0; e + st < VE; e += 2 * st) { vj[e] += vj[e + st]; vr[e] += vr[e + st]; }
-      accj += vj[0];
-      seg += vr[0];
+        for (int e = 0; e < VE; ++e) {
+          const float xa = Elem<DT>::get(va[k], e), xb = Elem<DT>::get(vb[k], e);
+          vj[e] = kKL ? kl_elem(xa, xb, jk) : jsd_elem(xa, xb, jk);
+        }
+        #pragma unroll
+        for (int st = 1; st < VE; st <<= 1)
+          #pragma unroll
+          for (int e = 0; e + st < VE; e += 2 * st) vj[e] += vj[e + st];
+        accj += vj[0];
+      }
+      if (dr || db) {
+        float vr[VE];
+        #pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const float xa = Elem<DT>::get(va[k], e), xb = Elem<DT>::get(vb[k], e);
+          const float xt = Elem<DT>::get(vt[k], e);
+          vr[e] = dr ? resid_elem<DM>(xt, xa, xb, rk) : bonus_elem(xt, rk.c, rk.Rf);
+        }
+        #pragma unroll
+        for (int st = 1; st < VE; st <<= 1)
+          #pragma unroll
+          for (int e = 0; e + st < VE; e += 2 * st) vr[e] += vr[e + st];
+        seg += vr[0];
+      }
     }
   }
 }
@@ -533,6 +551,10 @@ DEV void pass2_sums_any(const KArgs& A, const RowGeo& g, long long rel0, long lo
   constexpr int VE = Elem<DT>::VE;
   if (A.vmap != nullptr || has_tail(A, c0, c1))
     pass2_sums<DT, 2, DM, kKL, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+  else if (dr && !dj && !db && c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
+    pass2_sums<DT, 0, DM, false, kNb, true>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+  else if (dr && !dj && !db)
+    pass2_sums<DT, 1, DM, false, kNb, true>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
   else if (c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
     pass2_sums<DT, 0, DM, kKL, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
   else
