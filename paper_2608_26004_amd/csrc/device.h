@@ -35,6 +35,10 @@ constexpr int kChunkVec = kTileVec * kNSub;     // vectors per vocabulary chunk
 constexpr int kSegVec = kChunkVec / kWaves;     // one wave's contiguous segment (pass 2)
 constexpr int kSegPerLane = kSegVec / 64;       // vectors per lane in a segment
 constexpr int kMaxK = 63;                       // K + 1 rows of a request fit one wave
+// pass 2 reads a lane's segment in groups of 4 vectors, and the pick splits a
+// segment evenly over the workgroup's threads
+static_assert(kSegPerLane % 4 == 0 && kSegVec % kThreads == 0,
+              "the tile size must give whole pass-2 groups and pick slices");
 
 constexpr float kL2E = 1.44269504088896340736f;
 constexpr double kLn2 = 0.693147180559945309417232121458;
