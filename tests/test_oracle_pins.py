@@ -25,6 +25,34 @@ def rand_rows(V, n=1, scale=3.0, rng=rng0):
     return (scale * rng.standard_normal((n, V))).astype(np.float32)
 
 
+# ----------------------------------------------------------- bf16 decode --
+def test_bf16_decode_special_values():
+    """A bf16 value is the high half of an fp32 word: closed-form values of
+    chosen bit patterns (signed zeros, one, infinities, the smallest
+    subnormal 2^-133, the largest finite (2 - 2^-7) 2^127, 3.140625)."""
+    cases = {0x0000: 0.0, 0x8000: -0.0, 0x3F80: 1.0, 0xBF80: -1.0, 0x4049: 3.140625,
+             0x7F80: math.inf, 0xFF80: -math.inf, 0x0001: 2.0 ** -133,
+             0x7F7F: (2.0 - 2.0 ** -7) * 2.0 ** 127, 0xC2F7: -123.5, 0x3C00: 2.0 ** -7}
+    bits = np.array(list(cases), np.uint16)
+    got = O.bf16_bits_to_f32(bits).astype(np.float64)
+    for k, (b, v) in enumerate(cases.items()):
+        assert got[k] == v and math.copysign(1.0, got[k]) == math.copysign(1.0, v), (hex(b), got[k], v)
+    assert O.to_f32(bits).dtype == np.float32
+
+
+def test_bf16_decode_matches_torch():
+    """The oracle's decode against torch's bfloat16 -> float32 conversion on
+    every NaN-free bit pattern."""
+    torch = pytest.importorskip("torch")
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    exp_all = (bits >> 7) & 0xFF
+    keep = ~((exp_all == 0xFF) & ((bits & 0x7F) != 0))       # drop NaNs
+    bits = bits[keep]
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).float().numpy()
+    got = O.bf16_bits_to_f32(bits)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
 # ---------------------------------------------------------------- softmax --
 @pytest.mark.parametrize("tau", [1.0, 0.7, 2.5])
 def test_log_softmax_matches_scipy(tau):
@@ -181,6 +209,90 @@ def test_worked_example_cda_flips_decision():
         assert abs(r.rows[0].D - D_ref) < 1e-6          # fp32 inputs
     # the value behind the flip: (3/8) e^-D < .37 < 3/8
     assert (3 / 8) * math.exp(-D_ref) < 0.37 < 3 / 8
+
+
+def test_worked_example_decimals():
+    """The fp64 decimals of the two-token example (tests/golden), written
+    before any kernel existed: D, gamma_eff and the Eq. 4 threshold from the
+    oracle's JSD and gate, the fused logits of Eq. 2 in fp32 and their
+    log-softmax."""
+    g = json.load(open(os.path.join(GOLDEN, "worked_example_v2.json")))
+    dec = g["decimals"]
+    t = np.stack([_row(r) for r in g["t"]])
+    a = np.stack([_row(r) for r in g["a"]])
+    b = np.stack([_row(r) for r in g["b"]])
+    D = O.jsd(a[0], b[0])
+    assert abs(D - dec["D"]) < 1e-7                       # fp32-rounded ln 3
+    ge = O.gamma_eff(D, g["gamma"])
+    assert abs(ge - dec["gamma_eff"]) < 1e-7
+    assert abs(ge * O.softmax(b[0])[0] - dec["threshold"]) < 1e-7
+    f = O.fused_logits_f32(t[0], a[0], b[0], g["beta"])
+    np.testing.assert_allclose(f.astype(np.float64), dec["f"], atol=1e-6)
+    np.testing.assert_allclose(O.log_softmax(f), dec["log_softmax_f"], atol=1e-6)
+    assert O.argmax_first(f) == 1
+
+
+def test_worked_example_sampling_three_tokens():
+    """Sec. 3.3 Eq. 3 with the sampling acceptance on a three-token example
+    (tests/golden/worked_example_sampling_v3.json): the stored decimals
+    against their closed forms (plain math), then the oracle's fused target,
+    proposal, D, gate, acceptance probability, first-token law and sampler
+    against the decimals."""
+    g = json.load(open(os.path.join(GOLDEN, "worked_example_sampling_v3.json")))
+    e = math.e
+    # closed forms, from the definitions, independent of the oracle
+    zp = math.exp(0.5) + e + math.exp(-1.0)
+    p_cf = [math.exp(0.5) / zp, e / zp, math.exp(-1.0) / zp]
+    q_cf = [1 / (2 + e), e / (2 + e), 1 / (2 + e)]
+    Q_cf = [math.exp(0.5) / (math.exp(0.5) + 2), 1 / (math.exp(0.5) + 2), 1 / (math.exp(0.5) + 2)]
+    D_cf = sum(0.5 * P * math.log(2 * P / (P + Q)) + 0.5 * Q * math.log(2 * Q / (P + Q))
+               for P, Q in zip(q_cf, Q_cf))
+    c_cf = 0.5 * math.exp(-D_cf)
+    al_cf = sum(min(qq, pp / c_cf) for pp, qq in zip(p_cf, q_cf))
+    pi_cf = [min(q_cf[0], p_cf[0] / c_cf) + (1 - al_cf), min(q_cf[1], p_cf[1] / c_cf),
+             min(q_cf[2], p_cf[2] / c_cf)]          # the residual is all on token 0
+    np.testing.assert_allclose(p_cf, g["p_fused"], atol=1e-8)
+    np.testing.assert_allclose(q_cf, g["q"], atol=1e-8)
+    assert abs(D_cf - g["D"]) < 1e-10 and abs(c_cf - g["c"]) < 1e-10
+    assert abs(al_cf - g["alpha"]) < 1e-9
+    np.testing.assert_allclose(pi_cf, g["pi"], atol=1e-8)
+    # the oracle
+    t = np.array(g["t"], np.float32)
+    a = np.array(g["a"], np.float32)
+    b = np.array(g["b"], np.float32)
+    f = O.fused_logits_f32(t, a, b, g["beta"])
+    p = O.softmax(f, g["tau"])
+    q = O.softmax(a, g["tau"])
+    np.testing.assert_allclose(p, g["p_fused"], atol=1e-8)
+    np.testing.assert_allclose(q, g["q"], atol=1e-8)
+    D = O.jsd(a, b)
+    c = O.gamma_eff(D, g["gamma"])
+    assert abs(D - g["D"]) < 1e-9 and abs(c - g["c"]) < 1e-9
+    assert abs(O.acceptance_prob(p, q, c) - g["alpha"]) < 1e-8
+    r = np.maximum(0.0, p - q)
+    np.testing.assert_allclose(r / r.sum(), g["residual"], atol=1e-12)
+    # K = 1 request (row 1 is the bonus row)
+    T = np.stack([t, np.zeros(3, np.float32)])
+    A = np.stack([a, np.zeros(3, np.float32)])
+    Bm = np.stack([b, np.zeros(3, np.float32)])
+    np.testing.assert_allclose(O.first_token_law(T, A, Bm, 1.0, gamma=0.5), g["pi"], atol=1e-8)
+    P = O.emitted_law(T, A, Bm, 1.0, gamma=0.5)
+    np.testing.assert_allclose(P[0], [1 - g["alpha"], 0.0, 0.0], atol=1e-8)
+    g1 = g["gamma_one"]
+    c1 = O.gamma_eff(D, 1.0)
+    assert abs(c1 - g1["c"]) < 1e-9
+    assert abs(O.acceptance_prob(p, q, c1) - g1["alpha"]) < 1e-8
+    np.testing.assert_allclose(O.first_token_law(T, A, Bm, 1.0, gamma=1.0), g1["pi"], atol=1e-8)
+    # the sampler: draft 2 has ratio p~(2) / (c q(2)) ~ 0.772; u = 0.9 rejects
+    # it and the residual draw gives token 0 whatever u_K; u = 0.5 accepts it
+    for u0, acc, nxt in ((0.9, 0, 0), (0.5, 1, None)):
+        for uK in (0.01, 0.5, 0.99):
+            rr = O.verify_request(T, A, Bm, np.array([2], np.int32), None,
+                                  np.array([u0, uK], np.float32), 1.0, gamma=0.5)
+            assert rr.accept_len == acc
+            assert abs(rr.rows[0].ratio - g["p_fused"][2] / (g["c"] * g["q"][2])) < 1e-6
+            if nxt is not None:
+                assert rr.next_token == nxt
 
 
 # --------------------------------------- greedy acceptance, brute force --
