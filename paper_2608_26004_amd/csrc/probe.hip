@@ -50,9 +50,37 @@ __global__ __launch_bounds__(kThreads) void read_reduce_kernel(const v4u* src, l
   }
 }
 
+// Core-clock probe: the first lane of each workgroup spins on the 100 MHz
+// real-time counter for `ticks` ticks and records how far the shader-clock
+// counter (s_memtime) advanced meanwhile; the ratio of the two, times
+// 100 MHz, is the clock the workgroup's compute unit ran at.  The loop ends
+// once the real-time counter has moved `ticks` (bounded on the host).
+__global__ __launch_bounds__(64) void clock_kernel(uint32_t ticks, uint32_t* out) {
+  if (threadIdx.x != 0) return;
+  const uint64_t r0 = __builtin_amdgcn_s_memrealtime();
+  const uint64_t c0 = __builtin_amdgcn_s_memtime();
+  uint64_t r1 = r0;
+  while (r1 - r0 < (uint64_t)ticks) {
+    __builtin_amdgcn_s_sleep(1);
+    r1 = __builtin_amdgcn_s_memrealtime();
+  }
+  const uint64_t c1 = __builtin_amdgcn_s_memtime();
+  out[2 * blockIdx.x] = (uint32_t)(c1 - c0);
+  out[2 * blockIdx.x + 1] = (uint32_t)(r1 - r0);
+}
+
 }  // namespace
 
 extern "C" {
+
+int asymspec_probe_clock(uint32_t* out, int nblocks, uint32_t ticks, void* stream) {
+  if (out == nullptr || (reinterpret_cast<uintptr_t>(out) & 3u) != 0u) return ASYMSPEC_PROBE_E_ARG;
+  if (nblocks < 1 || nblocks > ASYMSPEC_PROBE_MAX_CLOCK_BLOCKS) return ASYMSPEC_PROBE_E_ARG;
+  if (ticks < 1u || ticks > ASYMSPEC_PROBE_MAX_CLOCK_TICKS) return ASYMSPEC_PROBE_E_ARG;
+  hipLaunchKernelGGL(clock_kernel, dim3((unsigned)nblocks), dim3(64), 0,
+                     reinterpret_cast<hipStream_t>(stream), ticks, out);
+  return hipGetLastError() == hipSuccess ? 0 : ASYMSPEC_PROBE_E_DEVICE;
+}
 
 int asymspec_probe_read(const void* src, size_t nbytes, uint32_t* out, int nblocks, void* stream) {
   if (src == nullptr || out == nullptr) return ASYMSPEC_PROBE_E_ARG;

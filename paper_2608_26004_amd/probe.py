@@ -30,6 +30,8 @@ def load_library():
     lib.asymspec_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                         ctypes.c_int, ctypes.c_void_p]
     lib.asymspec_probe_read.restype = ctypes.c_int
+    lib.asymspec_probe_clock.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_uint32, ctypes.c_void_p]
+    lib.asymspec_probe_clock.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -81,3 +83,21 @@ def read_ceiling(nbytes: int = 1 << 31, grids=(2048, 4096, 8192, 16384), reps: i
     del buf, out
     return {"GBps": best[1], "bytes": nbytes, "nblocks": best[0], "ms": best[2],
             "per_grid_GBps": per_grid}
+
+
+def clock_mhz(device=None, nblocks: int = 256, ticks: int = 2000) -> dict:
+    """Core clock in MHz, sampled by nblocks single-wave workgroups that each
+    wait `ticks` ticks (10 ns each) of the real-time counter: mean, min and
+    max over the workgroups.  Synchronises the device."""
+    import numpy as np
+    import torch
+    dev = device or torch.device("cuda")
+    out = torch.zeros(2 * nblocks, dtype=torch.int32, device=dev)
+    s = torch.cuda.current_stream(dev)
+    st = load_library().asymspec_probe_clock(ctypes.c_void_p(out.data_ptr()), int(nblocks),
+                                             int(ticks), ctypes.c_void_p(s.cuda_stream))
+    if st != 0:
+        raise RuntimeError(f"asymspec_probe_clock failed with status {st}")
+    w = out.cpu().numpy().view(np.uint32).astype(np.float64).reshape(nblocks, 2)
+    mhz = 100.0 * w[:, 0] / np.maximum(w[:, 1], 1.0)
+    return {"mean": float(mhz.mean()), "min": float(mhz.min()), "max": float(mhz.max())}

@@ -17,7 +17,7 @@ HEADER = os.path.join(ROOT, "include", "asymspec_probe.h")
 def test_probe_exports_header_symbols():
     src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
     names = sorted(set(re.findall(r"\b(asymspec_[a-z_]+)\s*\(", src)))
-    assert names == ["asymspec_probe_read"]
+    assert names == ["asymspec_probe_clock", "asymspec_probe_read"]
     lib = probe.load_library()
     for n in names:
         assert hasattr(lib, n), n
@@ -40,6 +40,31 @@ def test_probe_rejects_bad_arguments_on_host(src, nbytes, out, nblocks):
     st = probe.load_library().asymspec_probe_read(
         ctypes.c_void_p(src), nbytes, ctypes.c_void_p(out), nblocks, None)
     assert st == probe.E_ARG
+
+
+@pytest.mark.parametrize("out,nblocks,ticks", [
+    (0, 4, 100),                          # null output
+    (4098, 4, 100),                       # output not 4-byte aligned
+    (4096, 0, 100),                       # no workgroups
+    (4096, 4097, 100),                    # too many workgroups
+    (4096, 4, 0),                         # no wait
+    (4096, 4, 1000001),                   # wait beyond the stated maximum
+])
+def test_clock_probe_rejects_bad_arguments_on_host(out, nblocks, ticks):
+    st = probe.load_library().asymspec_probe_clock(ctypes.c_void_p(out), nblocks, ticks, None)
+    assert st == probe.E_ARG
+
+
+@pytest.mark.gpu
+def test_clock_probe_reads_a_plausible_clock():
+    """The sampled core clock lies between 100 MHz and the part's 2.4 GHz
+    peak (with a margin for the counters' granularity)."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    c = probe.clock_mhz(torch.device("cuda"), nblocks=64, ticks=1000)
+    print(f"[clock] {c}")
+    assert 100.0 < c["min"] <= c["max"] < 2600.0
 
 
 @pytest.mark.gpu
