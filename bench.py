@@ -287,9 +287,14 @@ def main():
         return asp.fuse_verify(*copies[i % len(copies)], d, q, u, tau, return_gate=args.gate,
                                workspace=ws, out=out_arg, **var)
 
+    from paper_2608_26004_amd import probe
+    # core clock before the warm-up, after it and after the timed calls (each
+    # sample waits 20 us on every compute unit, outside the timed region)
+    clocks = {"before_warmup": probe.clock_mhz(dev)}
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
+    clocks["after_warmup"] = probe.clock_mhz(dev)
     stream = torch.cuda.current_stream(dev)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
@@ -305,6 +310,12 @@ def main():
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
     per = np.array([a.elapsed_time(b) for a, b in ev])
+    clocks["after_timed"] = probe.clock_mhz(dev)
+    # every wait between the workgroups of every call ended in time
+    n_timeouts = ws.timeouts()
+    if n_timeouts:
+        print(f"[bench] {n_timeouts} timed-out waits: some decisions did not complete",
+              file=sys.stderr, flush=True)
     ms_step = total_ms / args.steps
     kern_ms = float(np.mean(per))
     rows = B * (K + 1)
@@ -324,7 +335,6 @@ def main():
 
     ceiling = None
     if not args.no_ceiling:
-        from paper_2608_26004_amd import probe
         ceiling = probe.read_ceiling(device=dev)
         ceiling["kernel"] = "read_reduce_kernel (libasymspec_probe.so), 16-byte nt loads"
         print(f"[bench] read ceiling {ceiling['GBps']:.0f} GB/s over {ceiling['bytes']} B "
@@ -385,8 +395,15 @@ def main():
                           "bytes": ceiling["bytes"], "nblocks": ceiling["nblocks"],
                           "kernel": ceiling["kernel"]} if ceiling else None),
         "cpu_baseline": cpu,
+        "clock_MHz": {k: round(v["mean"], 1) for k, v in clocks.items()},
+        "timeouts": n_timeouts,
     }
+    if args.steps <= 64:
+        # launch times in call order (HIP events), to see warm-up effects
+        res["per_call_ms"] = [round(float(v), 5) for v in per]
     print(json.dumps(res), flush=True)
+    if n_timeouts:
+        sys.exit(3)
 
 
 if __name__ == "__main__":

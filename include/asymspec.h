@@ -147,7 +147,9 @@ int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stre
  *                       4194297 (bf16) or 2097149 (fp32): a row spans at most
  *                       256 chunks of 32 KiB
  *   params              see asymspec_params (host pointer)
- *   accept_len          [B] int32 out: number of accepted drafts, in [0, K]
+ *   accept_len          [B] int32 out: number of accepted drafts, in [0, K]; -1
+ *                       marks a request whose decision did not complete
+ *                       (asymspec_workspace_timeouts)
  *   next_token          [B] int32 out: the token emitted after them
  *   fused_logprobs      [B][K+1] float out: [i] (i < K) = log p~_i(d_i), the
  *                       fused log-probability of draft i (temperature 1 for
@@ -173,7 +175,9 @@ int asymspec_workspace_clear(void* workspace, size_t workspace_bytes, void* stre
  *   stream              hipStream_t or NULL
  *
  * Integer and float arrays must be 4-byte aligned.  Returns ASYMSPEC_OK or a
- * negative status; on error nothing is enqueued.
+ * negative status; on error nothing is enqueued.  A request whose outputs
+ * could not be completed on the device (a wait between workgroups timed out,
+ * counted in the workspace: asymspec_workspace_timeouts) has accept_len = -1.
  */
 int asymspec_fuse_verify(const void* verifier_logits,
                          const void* drafter_full_logits,
@@ -243,6 +247,33 @@ int asymspec_fuse_verify_xvocab(const void* verifier_logits,
                                 float* fused_logprobs_full,
                                 void* workspace, size_t workspace_bytes,
                                 void* stream);
+
+/* Number of timed-out waits between workgroups recorded in `workspace`
+ * since it was last zero-filled (asymspec_workspace_clear, or a zeroed
+ * allocation), into *count (a host pointer).  The decision kernel's
+ * workgroups exchange records through the workspace; every wait for one is
+ * bounded (0.2 s by default, asymspec_set_wait_limit), and a wait that runs
+ * out is counted here.  A request whose decision could not be completed has
+ * accept_len = -1 and unspecified other outputs; every other request's
+ * outputs are valid.  A nonzero count means the device did not run the
+ * launch's workgroups as the kernel assumes (for example calls sharing one
+ * workspace overlapped) and should be treated as an error.
+ *   workspace        the workspace passed to the calls (device pointer,
+ *                    256-byte aligned, at least 256 bytes)
+ *   stream           the stream the calls were enqueued on: the count is read
+ *                    after every call enqueued before this one (the call
+ *                    synchronises the stream)
+ * Returns ASYMSPEC_OK, ASYMSPEC_E_ARG or ASYMSPEC_E_DEVICE. */
+int asymspec_workspace_timeouts(const void* workspace, size_t workspace_bytes, void* stream,
+                                uint32_t* count);
+
+/* Sets the bound of every wait between workgroups for calls enqueued after
+ * it, process-wide, in ticks of the GPU's 100 MHz clock (10 ns each); 0
+ * restores the default of 20,000,000 (0.2 s); at most 100,000,000 (1 s),
+ * else ASYMSPEC_E_ARG.  A test hook for the error path: a bound of a few
+ * ticks makes waits run out under normal operation, and every workgroup
+ * still ends. */
+int asymspec_set_wait_limit(unsigned long long ticks);
 
 /* Static text for a status code. */
 const char* asymspec_status_string(int status);

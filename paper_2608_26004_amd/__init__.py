@@ -12,6 +12,7 @@ import ctypes
 import os
 
 __all__ = ["fuse_verify", "workspace_size", "Workspace", "load_library", "status_string",
+           "workspace_timeouts", "set_wait_limit",
            "BF16", "FP32", "GATE_CDA", "GATE_FIXED", "GATE_KL", "GATE_LAMBDA",
            "DELTA_AB", "DELTA_A", "DELTA_TB", "FUSE_BONUS", "EARLY_EXIT", "AsymSpecError"]
 
@@ -78,6 +79,10 @@ def load_library(path: str | None = None):
     lib.asymspec_status_string.restype = ctypes.c_char_p
     lib.asymspec_version.argtypes = []
     lib.asymspec_version.restype = i32
+    lib.asymspec_workspace_timeouts.argtypes = [vp, sz, vp, ctypes.POINTER(ctypes.c_uint32)]
+    lib.asymspec_workspace_timeouts.restype = i32
+    lib.asymspec_set_wait_limit.argtypes = [ctypes.c_ulonglong]
+    lib.asymspec_set_wait_limit.restype = i32
     if path is None:
         _lib = lib
     return lib
@@ -111,11 +116,43 @@ class Workspace:
     def get(self, nbytes: int, device):
         import torch
         if self.buf is None or self.buf.numel() < nbytes or self.buf.device != device:
+            # a replaced buffer goes back to torch's caching allocator, which
+            # does not reuse it before the work recorded on it has finished
             self.buf = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=device)
+        self.buf.record_stream(torch.cuda.current_stream(device))
         return self.buf
 
+    def timeouts(self) -> int:
+        """Timed-out waits counted in this workspace since it was allocated
+        (synchronises the current stream); nonzero means some request's
+        decision was not completed (its accept_len is -1)."""
+        if self.buf is None:
+            return 0
+        return workspace_timeouts(self.buf)
 
+
+# one default workspace per (device, stream): calls on different streams
+# may overlap and must not share one
 _default_ws = {}
+
+
+def workspace_timeouts(buf) -> int:
+    """The timeout count of a workspace tensor (see Workspace.timeouts)."""
+    lib = load_library()
+    n = ctypes.c_uint32(0)
+    st = lib.asymspec_workspace_timeouts(_ptr(buf), buf.numel() * buf.element_size(),
+                                         _stream_handle(buf.device), ctypes.byref(n))
+    if st != OK:
+        raise AsymSpecError(st, status_string(st))
+    return int(n.value)
+
+
+def set_wait_limit(ticks: int) -> None:
+    """Bound of every wait between workgroups for later calls, in 10 ns
+    ticks (0: the default 0.2 s); a test hook for the error path."""
+    st = load_library().asymspec_set_wait_limit(int(ticks))
+    if st != OK:
+        raise AsymSpecError(st, status_string(st))
 
 
 def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
@@ -139,7 +176,8 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     early_exit: 0 reads every row; n > 0 reads the first n rows, then the
     others only if none of those is surely rejected (EARLY_EXIT); the
     per-draft outputs of rows not read are NaN.
-    Returns (accept_len [B] int32, next_token [B] int32,
+    Returns (accept_len [B] int32 (-1 marks a request whose decision did not
+             complete on the device: see Workspace.timeouts), next_token [B] int32,
              fused_logprobs [B, K+1] float32[, gate [B, K, 2] float32]
              [, full [B, K+1, V] float32])."""
     import torch
@@ -191,7 +229,8 @@ def fuse_verify(t, a, b, draft_tokens, draft_probs, uniforms, temperature,
     if ws_bytes == 0:
         raise AsymSpecError(E_ARG, "invalid shape")
     if workspace is None:
-        workspace = _default_ws.setdefault(dev, Workspace(dev))
+        key = (dev, torch.cuda.current_stream(dev).cuda_stream)
+        workspace = _default_ws.setdefault(key, Workspace(dev))
     wsbuf = workspace.get(ws_bytes, dev)
     flags = (FUSE_BONUS if fuse_bonus else 0) | (EARLY_EXIT if early_exit else 0)
     params = _Params(float(beta), float(gamma), int(gate_mode), flags, int(delta_mode), float(lam),

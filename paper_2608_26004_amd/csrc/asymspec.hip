@@ -96,13 +96,15 @@ template <int DT, bool kB1, int DM>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ASYMSPEC_WAVES)))
 void fuse_verify_kernel(KArgs A) {
   __shared__ Smem sm;
+#ifdef ASYMSPEC_TRACE
+  const uint64_t t_start = __builtin_amdgcn_s_memrealtime();
+#endif
   const Item it = sched_item(A.sc, A.K, A.S, (int)blockIdx.x);
   int type = it.type;
   if (type == kItemStats2) {
     // early exit: the rows after the first group are read unless the
     // verdict found a sure rejection among the first rows
-    if (load_verdict(A, it.req, sm) == kVerdictSkip) return;
-    type = kItemStats;
+    type = load_verdict(A, it.req, sm) == kVerdictSkip ? kItemNone : kItemStats;
   }
   // one call site per item kind keeps a single inlined copy of each
   switch (type) {
@@ -113,6 +115,19 @@ void fuse_verify_kernel(KArgs A) {
     case kItemPick: pick_item<DT, DM>(A, it.req, sm); break;
     default: break;
   }
+#ifdef ASYMSPEC_TRACE
+  // timeline of the launch (a build option for measurement): per item its
+  // start and end on the 100 MHz clock, kind, request and the unit it ran on
+  if (threadIdx.x == 0 && A.trace != nullptr) {
+    uint64_t* tr = A.trace + (size_t)blockIdx.x * 4;
+    const uint64_t hw = (uint64_t)__builtin_amdgcn_s_getreg(63492) |
+                        ((uint64_t)__builtin_amdgcn_s_getreg(6164) << 32);
+    tr[0] = t_start;
+    tr[1] = __builtin_amdgcn_s_memrealtime();
+    tr[2] = (uint64_t)(uint32_t)it.type | ((uint64_t)(uint32_t)it.req << 8) | ((uint64_t)(uint32_t)it.sub << 40);
+    tr[3] = hw;
+  }
+#endif
 }
 
 // The drafter-to-verifier map of a cross-family call: inv[j] = x for the
@@ -138,7 +153,7 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
 struct Layout {
   int S, VE;
   size_t rows;
-  size_t off_rec1, off_dec, off_rec2, off_err, off_inv, total;
+  size_t off_rec1, off_dec, off_rec2, off_err, off_inv, off_trace, total;
 };
 
 static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -161,12 +176,17 @@ static bool make_layout(int B, int K, int V, int dtype, Layout& L, int Vd = 0) {
   L.S = (int)S;
   L.rows = (size_t)B * (K + 1);
   size_t off = 0;
+  // the timeout counter first, at a place that does not depend on the shape
+  L.off_err = off;  off = align_up(off + 8, 256);
   L.off_rec1 = off; off = align_up(off + L.rows * L.S * kR1 * 8, 256);
   L.off_dec = off;  off = align_up(off + (size_t)B * (kDecHdr + (size_t)(K + 1) * kDecRow) * 8, 256);
   L.off_rec2 = off; off = align_up(off + L.rows * L.S * kR2 * 8, 256);
-  L.off_err = off;  off = align_up(off + 8, 256);
   // cross-family: inverse map [Vd] and its duplicate flag
   L.off_inv = off;  off = align_up(off + (Vd > 0 ? (size_t)Vd * 4 + 4 : 0), 256);
+#ifdef ASYMSPEC_TRACE
+  // 32 bytes per work item, for at most (K + 2) * S + 3 items per request
+  L.off_trace = off;  off = align_up(off + (size_t)B * ((size_t)(K + 2) * L.S + 3) * 32, 256);
+#endif
   L.total = off;
   return true;
 }
@@ -266,6 +286,9 @@ static uint32_t next_epoch() {
 
 static bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+// Bound of every wait between workgroups, in ticks of the 100 MHz clock.
+static std::atomic<unsigned long long> g_poll_ticks{kPollTicks};
+
 }  // namespace asym
 
 using namespace asym;
@@ -360,9 +383,13 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   A.vmap = vmap;
   A.Vd = vmap != nullptr ? Vd : V;
   A.inv = vmap != nullptr ? (const int32_t*)(ws + L.off_inv) : nullptr;
+#ifdef ASYMSPEC_TRACE
+  A.trace = (uint64_t*)(ws + L.off_trace);
+#endif
   A.lam = params->gate_mode == ASYMSPEC_GATE_LAMBDA ? params->lambda : 0.0f;
   A.ln_gamma = std::log((double)params->gamma);
   A.epoch = next_epoch();
+  A.poll_ticks = g_poll_ticks.load();
   // lags scale with the number of workgroups the chip holds at once
   const int ee_rows = ee ? (params->early_rows > 0 ? params->early_rows : 2) : 0;
   const int in_flight = vmap != nullptr ? di->max_blocks_xv[dtype] : di->max_blocks[dtype];
@@ -424,6 +451,26 @@ int asymspec_fuse_verify_xvocab(const void* t, const void* a, const void* b, int
   return fuse_verify_impl(t, a, b, dtype, vocab_map, Vd, draft_tokens, draft_probs, uniforms, temperature, B, K,
                           V, params, accept_len, next_token, fused_logprobs, gate_out, fused_logprobs_full,
                           workspace, workspace_bytes, stream);
+}
+
+int asymspec_workspace_timeouts(const void* workspace, size_t workspace_bytes, void* stream,
+                                uint32_t* count) {
+  if (workspace == nullptr || count == nullptr || workspace_bytes < 256 || !aligned(workspace, 256))
+    return ASYMSPEC_E_ARG;
+  uint32_t v = 0;
+  if (hipMemcpyAsync(&v, workspace, sizeof(v), hipMemcpyDeviceToHost, (hipStream_t)stream) != hipSuccess ||
+      hipStreamSynchronize((hipStream_t)stream) != hipSuccess) {
+    (void)hipGetLastError();
+    return ASYMSPEC_E_DEVICE;
+  }
+  *count = v;
+  return ASYMSPEC_OK;
+}
+
+int asymspec_set_wait_limit(unsigned long long ticks) {
+  if (ticks > 100000000ull) return ASYMSPEC_E_ARG;
+  g_poll_ticks.store(ticks == 0 ? kPollTicks : ticks);
+  return ASYMSPEC_OK;
 }
 
 const char* asymspec_status_string(int status) {

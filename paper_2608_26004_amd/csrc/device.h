@@ -45,7 +45,7 @@ constexpr double kLn2 = 0.693147180559945309417232121458;
 constexpr float kFloorM = -1.0e30f;             // start value of running maxima
 constexpr uint32_t kBf16NegInf = 0xFF80u;
 constexpr uint32_t kF32NegInf = 0xFF800000u;
-constexpr uint64_t kPollTicks = 20000000;      // give up a wait after 0.2 s (100 MHz clock)
+constexpr uint64_t kPollTicks = 20000000;      // give up a wait after 0.2 s (100 MHz clock): the default
 
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 typedef const __attribute__((address_space(4))) uint32_t* cptr32;
@@ -62,12 +62,14 @@ enum Kind {
 // at the row's temperature when that is not 1 (the proposal q).
 enum Slot { sT = 0, sA = 1, sB = 2, sF = 3, sAT = 4, kSlots = 5 };
 
-// Statistics record of one (row, chunk): per slot the chunk maximum M (fp32)
-// and the sum of exp2(x * c - fl(M * c)) over the chunk (fp32), the first
-// index of the chunk maximum of f (greedy drafts) or t (greedy bonus), and
-// whether a and b differ bitwise anywhere in the chunk.
-enum { R1_M = 0, R1_S = kSlots, R1_ARG = 2 * kSlots, R1_NEQ = 2 * kSlots + 1, R1_USED = 2 * kSlots + 2,
-       kR1 = 16 };
+// Statistics record of one (row, chunk): per slot a reference exponent R
+// (fp32, log2 units; at most the chunk maximum of x * c) and the sum of
+// exp2(x * c - R) over the chunk (fp32), the maximum of the argmax slot (f
+// for greedy drafts, t for the greedy bonus row) and the first index where
+// the chunk attains it, and whether a and b differ bitwise anywhere in the
+// chunk.
+enum { R1_R = 0, R1_S = kSlots, R1_ARG = 2 * kSlots, R1_NEQ = 2 * kSlots + 1, R1_MARG = 2 * kSlots + 2,
+       R1_USED = 2 * kSlots + 3, kR1 = 16 };
 
 // Decision record of one request: a header and one block per row, published
 // by the decide item; pass-2 and pick items load it into LDS (Smem::req,
@@ -76,8 +78,11 @@ enum { H_STATE = 0, H_J = 1, H_TASK_LO = 2, H_TASK_HI = 3, H_SAMP = 4, H_USED = 
 // Early exit: the verdict on a request's first rows (a sure rejection among
 // them makes the other rows unneeded).
 enum { kVerdictRead = 1, kVerdictSkip = 2 };
-enum { kStateFinal = 1, kStatePending = 2 };
-enum { R_J = 0, R_TASK_LO = 1, R_TASK_HI = 2, R_FIN = 3, R_SAMP = 4, kReqWords = 5 };
+// kStateFailed: a wait of the decide item timed out (or, as seen by a later
+// item, its own wait for the decision did); the request's outputs are marked
+// invalid (accept_len = -1).
+enum { kStateFinal = 1, kStatePending = 2, kStateFailed = 3 };
+enum { R_J = 0, R_TASK_LO = 1, R_TASK_HI = 2, R_FIN = 3, R_SAMP = 4, R_FAIL = 5, kReqWords = 6 };
 enum {
   D_TASK = 0,   // pass-2 work on the row: kTaskJsd | kTaskRes | kTaskBonus
   D_C,          // exponent scale of the row's emission distribution (log2 e / tau, or log2 e)
@@ -127,7 +132,11 @@ struct KArgs {
   const int32_t* inv;
   double ln_gamma;
   uint32_t epoch;
+  uint64_t poll_ticks;   // bound of every wait, in ticks of the 100 MHz clock
   Sched sc;
+#ifdef ASYMSPEC_TRACE
+  uint64_t* trace;    // per-item timeline (measurement builds only)
+#endif
 };
 
 // Thread coordinates for item code.  They pass through empty asm so that the
@@ -174,7 +183,8 @@ DEV void err_count(const uint32_t* e) {
 // Bounded polling with exponential backoff: the n-th retry sleeps
 // 128 * 2^min(n, kPollMaxShift) cycles, so a wave that waits long issues few
 // loads and leaves the memory system to the streaming work; a wait gives up
-// (and counts an error) after kPollTicks of the 100 MHz real-time clock.
+// (and counts an error) after A.poll_ticks of the 100 MHz real-time clock
+// (kPollTicks unless the host set another bound).
 #ifndef ASYMSPEC_POLL_SHIFT
 #define ASYMSPEC_POLL_SHIFT 3
 #endif
@@ -188,7 +198,7 @@ struct Poll {
     const int reps = 1 << (n < kPollMaxShift ? n : kPollMaxShift);
     for (int i = 0; i < reps; ++i) __builtin_amdgcn_s_sleep(2);
     ++n;
-    if (__builtin_amdgcn_s_memrealtime() - t0 > kPollTicks) {
+    if (__builtin_amdgcn_s_memrealtime() - t0 > A.poll_ticks) {
       err_count(A.err);
       return false;
     }
@@ -198,20 +208,22 @@ struct Poll {
 
 // Workgroup-wide polling step: done() is true once every thread's ok holds;
 // otherwise it sleeps with the same backoff as Poll and returns false, or
-// gives up (true, and counts an error) when thread 0 finds the wait timed
-// out.  Every thread gets the same answer.
+// gives up (true, with timed_out set, and counts an error) when thread 0
+// finds the wait timed out.  Every thread gets the same answer.
 struct BlockPoll {
   uint64_t t0;
   int n;
-  DEV BlockPoll() : t0(__builtin_amdgcn_s_memrealtime()), n(0) {}
+  bool timed_out;
+  DEV BlockPoll() : t0(__builtin_amdgcn_s_memrealtime()), n(0), timed_out(false) {}
   DEV bool done(bool ok, const KArgs& A) {
     if (__syncthreads_and(ok)) return true;
     const int reps = 1 << (n < kPollMaxShift ? n : kPollMaxShift);
     for (int i = 0; i < reps; ++i) __builtin_amdgcn_s_sleep(2);
     ++n;
-    const bool late = threadIdx.x == 0 && __builtin_amdgcn_s_memrealtime() - t0 > kPollTicks;
+    const bool late = threadIdx.x == 0 && __builtin_amdgcn_s_memrealtime() - t0 > A.poll_ticks;
     if (__syncthreads_or(late)) {
       if (threadIdx.x == 0) err_count(A.err);
+      timed_out = true;
       return true;
     }
     return false;
@@ -219,33 +231,41 @@ struct BlockPoll {
 };
 
 // Whole workgroup: wait (bounded) until slot p carries the launch epoch,
-// with one load per poll.
-DEV void wait_one(const uint64_t* p, const KArgs& A) {
+// with one load per poll.  False (in every thread) when the wait timed out.
+DEV bool wait_one(const uint64_t* p, const KArgs& A) {
   BlockPoll bp;
   while (!bp.done(threadIdx.x != 0 || tag_ok(ld_tag(p), A.epoch), A)) {
   }
+  return !bp.timed_out;
 }
 
 // Whole workgroup: load() requests a set of tagged slots and returns whether
 // this thread's share all carry the launch epoch.  When the first attempt
 // misses, the workgroup polls only the slot `sentinel` (written about last)
 // until it is in, so that a waiting workgroup adds little traffic, and then
-// loads until every share is in (bounded).
+// loads until every share is in (bounded).  False (in every thread) when a
+// wait timed out: the loaded values are then not this launch's.
 template <class F>
-DEV void load_tagged(const KArgs& A, const uint64_t* sentinel, F&& load) {
-  if (__syncthreads_and(load())) return;
-  wait_one(sentinel, A);
+DEV bool load_tagged(const KArgs& A, const uint64_t* sentinel, F&& load) {
+  if (__syncthreads_and(load())) return true;
+  if (!wait_one(sentinel, A)) return false;
   BlockPoll bp;
   while (!bp.done(load(), A)) {
   }
+  return !bp.timed_out;
 }
 
 // The fp64 value in the tagged slot pair at p (low word first); both loads
-// go out together, and the pair is polled until both carry the epoch.
-DEV double wait_pair(const uint64_t* p, const KArgs& A) {
+// go out together, and the pair is polled until both carry the epoch.  ok is
+// cleared when the wait timed out.
+DEV double wait_pair(const uint64_t* p, const KArgs& A, bool& ok) {
   uint64_t lo = ld_tag(p), hi = ld_tag(p + 1);
   Poll pl;
-  while (!(tag_ok(lo, A.epoch) && tag_ok(hi, A.epoch)) && pl.again(A)) {
+  while (!(tag_ok(lo, A.epoch) && tag_ok(hi, A.epoch))) {
+    if (!pl.again(A)) {
+      ok = false;
+      break;
+    }
     lo = ld_tag(p);
     hi = ld_tag(p + 1);
   }
@@ -404,10 +424,12 @@ DEV double wave_sum_d(double x) {    // fp64 sum over lanes, in every lane
 }
 
 // ---------------------------------------------------- online log-sum-exp
-// Running (max m, sum s of exp2(x * c - R)) with R = fl(m * c), one vector
-// of VE elements at a time.  With kTrackArg, pos = k of the first vector (in
-// this thread's order) that attains the running maximum; the element inside
-// it is found afterwards.
+// Running (reference R, sum s of exp2(x * c - R)), one vector of VE elements
+// at a time.  acc_vec keeps R = fl(m * c) for the running maximum m; with
+// kTrackArg, pos = k of the first vector (in this thread's order) that
+// attains it (the element inside it is found afterwards).  acc_vec_lazy
+// keeps R where it is while no term exceeds 2^64, which saves the maxima of
+// every vector; any R at or below the maximum gives the same normaliser.
 struct Acc { float m, R, s; int pos; };
 DEV void acc_init(Acc& q, float c) { q.m = kFloorM; q.R = kFloorM * c; q.s = 0.0f; q.pos = 0; }
 
@@ -434,6 +456,47 @@ DEV void acc_vec(Acc& q, const float (&x)[VE], float c, int k) {
   q.s = __builtin_fmaf(q.s, scale, ex[0]);
   q.m = mn;
   q.R = Rn;
+}
+
+// Lazy step: the terms at the current reference; only when some lane's
+// vector sum exceeds 2^64 (or overflows) does the wave raise those lanes'
+// references to their vector maxima and redo the vector.  A NaN sum is left
+// to the caller (the chunk is then redone on the NaN-safe path).
+template <int VE, bool kClampNaN>
+DEV void acc_vec_lazy(Acc& q, const float (&x)[VE], float c) {
+  float ex[VE];
+  #pragma unroll
+  for (int e = 0; e < VE; ++e) {
+    float arg = __builtin_fmaf(x[e], c, -q.R);
+    if (kClampNaN) arg = fmaxf(arg, -200.0f);
+    ex[e] = __builtin_amdgcn_exp2f(arg);
+  }
+  #pragma unroll
+  for (int st = 1; st < VE; st <<= 1)
+    #pragma unroll
+    for (int e = 0; e + st < VE; e += 2 * st) ex[e] += ex[e + st];
+  float v = ex[0];
+  if (__builtin_expect(__ballot(v > 0x1p64f) != 0, 0)) {
+    float vm = x[0];
+    #pragma unroll
+    for (int e = 1; e < VE; ++e) vm = fmaxf(vm, x[e]);
+    const float Rn = fmaxf(q.R, vm * c);
+    const float scale = __builtin_amdgcn_exp2f(q.R - Rn);
+    #pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      float arg = __builtin_fmaf(x[e], c, -Rn);
+      if (kClampNaN) arg = fmaxf(arg, -200.0f);
+      ex[e] = __builtin_amdgcn_exp2f(arg);
+    }
+    #pragma unroll
+    for (int st = 1; st < VE; st <<= 1)
+      #pragma unroll
+      for (int e = 0; e + st < VE; e += 2 * st) ex[e] += ex[e + st];
+    v = ex[0];
+    q.s *= scale;
+    q.R = Rn;
+  }
+  q.s += v;
 }
 
 // --------------------------------------------------- pass-2 element terms
@@ -543,7 +606,8 @@ DEV bool kind_fused(int k) { return kind_draft(k) || k == kGreedyBonusF || k == 
 DEV __amdgpu_buffer_rsrc_t row_rsrc(const KArgs& A, const void* base, const RowGeo& g) {
   const unsigned long long rbase = (unsigned long long)g.vbeg * 16ull;
   unsigned long long span = (unsigned long long)(g.vend - g.vbeg) * 16ull;
-  const unsigned long long rem = A.stream_bytes - rbase;
+  // a row past the array's end (never for a valid row index) reads nothing
+  const unsigned long long rem = rbase < A.stream_bytes ? A.stream_bytes - rbase : 0ull;
   if (span > rem) span = rem;
   // drafter rows of another vocabulary are reached through the map only:
   // a resource over them reads zeros and touches no memory
@@ -705,11 +769,13 @@ struct Smem {
   float ws[kWaves][kSlots];
   int warg[kWaves];
   int wneq[kWaves];
+  float wmarg[kWaves];
   // decision of a request: per-row blocks, request words, and the
   // per-(row, chunk) values the decide item combines into them
   uint32_t rows[kMaxK + 1][kDecRow];
   uint32_t req[kReqWords];
   float dm[kThreads][kSlots];
+  float dmarg[kThreads];
   double dt[kThreads][kSlots];
   int darg[kThreads];
   int dneq[kThreads];

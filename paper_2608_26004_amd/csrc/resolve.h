@@ -45,12 +45,12 @@ DEV JsdConst jsd_const(const uint32_t* cst) {
 }
 
 // ------------------------------------------------------------------ decide
-// Classification of one row from its combined statistics: maxima M and
-// reference exponents R = fl(M * c) per slot, sums Sp rescaled to R (fp64),
-// the first index of the argmax slot's maximum, and whether a and b differ.
-// Fills the row's decision block v (kDecRow words).
+// Classification of one row from its combined statistics: reference
+// exponents R per slot and the sums Sp of exp2(x * c - R) (fp64), the
+// maximum Marg of the argmax slot and the first index attaining it, and
+// whether a and b differ.  Fills the row's decision block v (kDecRow words).
 template <int DT>
-DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const float (&M)[kSlots],
+DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, float Marg,
                       const float (&R)[kSlots], const double (&Sp)[kSlots], int arg, bool neq,
                       uint32_t* v) {
   const int kind = g.kind;
@@ -93,7 +93,7 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const f
       if (m0 != m0) m0 = -INFINITY;
       const double lpd = ((double)fd * (double)kL2E - L2[sF]) * kLn2;
       v[D_LPD] = __float_as_uint((float)lpd);
-      v[D_LPEMIT] = __float_as_uint((float)(((double)M[sF] * (double)kL2E - L2[sF]) * kLn2));
+      v[D_LPEMIT] = __float_as_uint((float)(((double)Marg * (double)kL2E - L2[sF]) * kLn2));
       v[D_ARG] = (uint32_t)arg;
       v[D_L2E_LO] = dlo(L2[sF]);
       v[D_L2E_HI] = dhi(L2[sF]);
@@ -152,14 +152,14 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, const f
     v[D_L2E_LO] = dlo(L2[sF]);
     v[D_L2E_HI] = dhi(L2[sF]);
     v[D_ARG] = (uint32_t)arg;
-    v[D_LPEMIT] = __float_as_uint((float)(((double)M[sF] * (double)g.c - L2[sF]) * kLn2));
+    v[D_LPEMIT] = __float_as_uint((float)(((double)Marg * (double)g.c - L2[sF]) * kLn2));
   } else {
     // bonus row (Alg. 1): greedy argmax of t, or a draw from softmax(t / tau)
     v[D_RF] = __float_as_uint(R[sT]);
     v[D_L2E_LO] = dlo(L2[sT]);
     v[D_L2E_HI] = dhi(L2[sT]);
     v[D_ARG] = (uint32_t)arg;
-    v[D_LPEMIT] = __float_as_uint((float)(((double)M[sT] * (double)g.c - L2[sT]) * kLn2));
+    v[D_LPEMIT] = __float_as_uint((float)(((double)Marg * (double)g.c - L2[sT]) * kLn2));
   }
   v[D_THR_LO] = dlo(thr);
   v[D_THR_HI] = dhi(thr);
@@ -184,7 +184,8 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
   const int li = tid / S, ch = tid - li * S;
   // the last statistics item read in list order is about the last to
   // finish: a waiting workgroup polls its record only
-  const uint64_t* sentinel = A.rec1 + (((size_t)req * nrow + (nread - 1)) * S + (S - 1)) * kR1 + R1_NEQ;
+  const uint64_t* sentinel = A.rec1 + (((size_t)req * nrow + (nread - 1)) * S + (S - 1)) * kR1 + R1_MARG;
+  bool all_in = true;
   for (int r0 = 0; r0 < nread; r0 += rpg) {
     const int nr = min(rpg, nread - r0);
     const bool have = li < nr;
@@ -199,16 +200,8 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
     Gather gq{0.0f, 0.0f, 0.0f, 1.0f, 0.0f};
     if (have && ch == 0) gq = sgather<DT>(A, row_span<DT>(A, req * nrow + i));
     const RowGeo g = row_geo<DT>(A, req * nrow + i);
-    const bool draft = kind_draft(g.kind);
-    const bool fused = kind_fused(g.kind);
-    float cs[kSlots];
-    cs[sT] = draft ? kL2E : g.c;
-    cs[sA] = kL2E;
-    cs[sB] = kL2E;
-    cs[sF] = g.c;
-    cs[sAT] = g.c;
     bool first = true;
-    load_tagged(A, sentinel, [&]() {
+    all_in = load_tagged(A, sentinel, [&]() {
       if (first) {
         first = false;
         bool ok = true;
@@ -223,33 +216,32 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
         ok = ok && tag_ok(r[j], A.epoch);
       }
       return ok;
-    });
-    // row maxima: every thread of the row reads the row's records from LDS
+    }) && all_in;
+    // row references and the argmax slot's row maximum: every thread of the
+    // row reads the row's records from LDS
     if (have) {
       #pragma unroll
-      for (int s = 0; s < kSlots; ++s) sm.dm[tid][s] = payf(r[R1_M + s]);
+      for (int s = 0; s < kSlots; ++s) sm.dm[tid][s] = payf(r[R1_R + s]);
+      sm.dmarg[tid] = payf(r[R1_MARG]);
     }
     __syncthreads();
-    float M[kSlots], Rr[kSlots];
+    float Rr[kSlots], Marg = kFloorM;
     #pragma unroll
-    for (int s = 0; s < kSlots; ++s) M[s] = kFloorM;
+    for (int s = 0; s < kSlots; ++s) Rr[s] = kFloorM;
     if (have) {
       const int t0 = li * S;
       for (int c = 0; c < S; ++c) {
         #pragma unroll
-        for (int s = 0; s < kSlots; ++s) M[s] = fmaxf(M[s], sm.dm[t0 + c][s]);
+        for (int s = 0; s < kSlots; ++s) Rr[s] = fmaxf(Rr[s], sm.dm[t0 + c][s]);
+        Marg = fmaxf(Marg, sm.dmarg[t0 + c]);
       }
     }
     // this chunk's terms of the row sums, rescaled to the row's reference
-    #pragma unroll
-    for (int s = 0; s < kSlots; ++s) Rr[s] = M[s] * cs[s];
     if (have) {
-      const float Marg = fused ? M[sF] : M[sT];
       #pragma unroll
       for (int s = 0; s < kSlots; ++s)
-        sm.dt[tid][s] = (double)payf(r[R1_S + s]) * exp2((double)(payf(r[R1_M + s]) * cs[s]) - (double)Rr[s]);
-      const float mine = fused ? payf(r[R1_M + sF]) : payf(r[R1_M + sT]);
-      sm.darg[tid] = mine == Marg ? (int)pay(r[R1_ARG]) : 0x7FFFFFFF;
+        sm.dt[tid][s] = (double)payf(r[R1_S + s]) * exp2((double)payf(r[R1_R + s]) - (double)Rr[s]);
+      sm.darg[tid] = payf(r[R1_MARG]) == Marg ? (int)pay(r[R1_ARG]) : 0x7FFFFFFF;
       sm.dneq[tid] = (int)pay(r[R1_NEQ]);
     }
     __syncthreads();
@@ -264,7 +256,7 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
         arg = min(arg, sm.darg[tid + c]);
         nq |= sm.dneq[tid + c];
       }
-      classify_row<DT>(A, g, gq, M, Rr, Sp, arg, nq != 0, sm.rows[i]);
+      classify_row<DT>(A, g, gq, Marg, Rr, Sp, arg, nq != 0, sm.rows[i]);
     }
     __syncthreads();
   }
@@ -309,6 +301,7 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
       sm.req[R_TASK_HI] = (uint32_t)(tmask >> 32);
       sm.req[R_FIN] = fin ? 1u : 0u;
       sm.req[R_SAMP] = samp ? 1u : 0u;
+      sm.req[R_FAIL] = all_in ? 0u : 1u;
     }
   }
   __syncthreads();
@@ -373,10 +366,13 @@ DEV void decide_item(const KArgs& A, int req, Smem& sm, bool verdict) {
   int nread = nrow;
   if (verdict || (A.sc.ee && load_verdict(A, req, sm) == kVerdictSkip)) nread = A.sc.G;
   decide_request<DT>(A, req, sm, nread);
+  // a timed-out wait for the records: the request fails (an early-exit
+  // verdict then reads every row)
+  const bool failed = sm.req[R_FAIL] != 0u;
   if (verdict) {
     if (w == 0) {
       const uint32_t st = lane < nread ? sm.rows[lane][D_STATUS] : 0u;
-      const bool skip = __any((st & kStDecided) != 0u && (st & kStAccept) == 0u);
+      const bool skip = !failed && __any((st & kStDecided) != 0u && (st & kStAccept) == 0u);
       if (lane == 0) st_tag(dec_hdr(A, req) + H_VERDICT, skip ? kVerdictSkip : kVerdictRead, A.epoch);
     }
     return;
@@ -395,9 +391,10 @@ DEV void decide_item(const KArgs& A, int req, Smem& sm, bool verdict) {
       st_tag(hdr + H_TASK_LO, sm.req[R_TASK_LO], A.epoch);
       st_tag(hdr + H_TASK_HI, sm.req[R_TASK_HI], A.epoch);
       st_tag(hdr + H_SAMP, sm.req[R_SAMP], A.epoch);
-      st_tag(hdr + H_STATE, fin ? kStateFinal : kStatePending, A.epoch);
+      st_tag(hdr + H_STATE, failed ? kStateFailed : (fin ? kStateFinal : kStatePending), A.epoch);
+      if (failed) A.acc_out[req] = -1;
     }
-    if (fin) {
+    if (fin && !failed) {
       // greedy with no open draft: accept_len = j*, emit the fused argmax of
       // row j* (Eq. 2) or the verifier argmax of the bonus row (Alg. 1)
       const int jstar = (int)sm.req[R_J];
@@ -440,7 +437,7 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
     return ok;
   };
   // the header goes out after the rows: a waiting workgroup polls it only
-  load_tagged(A, dec_hdr(A, req) + H_STATE, load);
+  const bool in = load_tagged(A, dec_hdr(A, req) + H_STATE, load);
   #pragma unroll
   for (int q = 0; q < kPer; ++q) {
     const int k = tid + q * kThreads;
@@ -450,6 +447,7 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
         sm.rows[i][(k - H_USED) % D_USED] = pay(v[q]);
       } else if (k == H_STATE) {
         sm.req[R_FIN] = pay(v[q]) == kStateFinal ? 1u : 0u;
+        sm.req[R_FAIL] = (!in || pay(v[q]) == kStateFailed) ? 1u : 0u;
       } else if (k == H_J) {
         sm.req[R_J] = pay(v[q]);
       } else if (k == H_TASK_LO) {
@@ -461,7 +459,9 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
       }
     }
   }
+  if (!in && tid == 0) sm.req[R_FAIL] = 1u;
   __syncthreads();
+  if (sm.req[R_FAIL] != 0u) return kStateFailed;
   return sm.req[R_FIN] != 0u ? (uint32_t)kStateFinal : (uint32_t)kStatePending;
 }
 
@@ -566,6 +566,8 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
   const int lane = lane_id(), w = wave_id();
   if (load_decision(A, req, sm) != kStatePending) return;
   unsigned long long tmask = (unsigned long long)sm.req[R_TASK_LO] | ((unsigned long long)sm.req[R_TASK_HI] << 32);
+  // only rows 0..K of the request (K + 1 <= 64)
+  if (A.K + 1 < 64) tmask &= (1ull << (A.K + 1)) - 1ull;
   while (tmask != 0) {
     const int i = __builtin_ctzll(tmask);
     tmask &= tmask - 1;
@@ -615,7 +617,7 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
 // found it, sm.flags[2] = 1 and its logit (f for drafts, t for the bonus
 // row) in sm.dd[3].  Whole workgroup.
 template <int DT, int DM>
-DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm) {
+DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm, bool& ok) {
   constexpr int VE = Elem<DT>::VE;
   constexpr int kPer = kSegVec / kThreads;   // vectors per thread in a segment
   const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
@@ -631,7 +633,7 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
     double v = 0.0;
     if (sg < nseg) {
       const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
-      v = wait_pair(p, A);
+      v = wait_pair(p, A, ok);
     }
     double incl, excl;
     block_scan(v, sm, incl, excl);
@@ -653,7 +655,7 @@ DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm)
       double tot = 0.0;
       for (int sg = lane; sg < nseg; sg += 64) {
         const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
-        tot += wait_pair(p, A);
+        tot += wait_pair(p, A, ok);
       }
       tot = wave_sum_d(tot);
       if (lane == 0) sm.dd[4] = tot;
@@ -799,7 +801,13 @@ template <int DT, int DM>
 DEV void pick_item(const KArgs& A, int req, Smem& sm) {
   const int lane = lane_id(), w = wave_id();
   const int K = A.K;
-  if (load_decision(A, req, sm) != kStatePending) return;   // written by decide
+  const uint32_t state = load_decision(A, req, sm);
+  if (state != kStatePending) {
+    // final: the decide wrote the outputs; failed: mark them invalid
+    if (state == kStateFailed && threadIdx.x == 0) A.acc_out[req] = -1;
+    return;
+  }
+  bool ok = true;   // this thread's waits all ended in time
   const bool samp = sm.req[R_SAMP] != 0u;
   // requested now, used after the segment sums arrive
   const float uK = samp ? A.u[(size_t)req * (K + 1) + K] : 0.0f;
@@ -824,7 +832,7 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
     for (unsigned long long jm = __ballot((task & kTaskJsd) != 0u); jm != 0; jm &= jm - 1) {
       const int i = __builtin_ctzll(jm);
       double part = 0.0;
-      for (int c = lane; c < A.S; c += 64) part += wait_pair(p2_rec(A, req, i, c) + P2_J, A);
+      for (int c = lane; c < A.S; c += 64) part += wait_pair(p2_rec(A, req, i, c) + P2_J, A, ok);
       part = wave_sum_d(part);
       // the partials are in log2 units; JSD = half their sum, within
       // [0, ln 2]; KL = their sum, >= 0
@@ -852,7 +860,7 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
   if (samp) {
     const bool bonus = j == K && !A.fuse_bonus;   // weights from t alone
     const double u = (double)uK;
-    int pick = cdf_pick<DT, DM>(A, req, j, u, bonus, sm);
+    int pick = cdf_pick<DT, DM>(A, req, j, u, bonus, sm, ok);
     const RowGeo g = row_span<DT>(A, req * (K + 1) + j);
     const bool have_x = pick >= 0 && sm.flags[2] != 0;
     if (pick < 0) pick = row_argmax_f<DT>(A, g, sm);
@@ -869,9 +877,12 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
     const double l2 = u2d(sm.rows[j][D_L2E_LO], sm.rows[j][D_L2E_HI]);
     lpn = (float)(((double)x * c - l2) * kLn2);
   }
+  // a wait that timed out leaves the decision incomplete: invalid outputs
+  const bool failed = __syncthreads_or(!ok);
   if (w == 0) {
     const bool skip = lane <= K && (sm.rows[lane][D_STATUS] & kStSkip) != 0u;
     write_outputs(A, req, j, next, lpn, lpd, Dl, skip);
+    if (failed && lane == 0) A.acc_out[req] = -1;
   }
 }
 

@@ -66,40 +66,46 @@ constexpr int kWin = ASYMSPEC_WIN;   // vectors per stream in flight per thread
 struct StatsAcc {
   Acc T, A, B, F, AT;
   uint64_t neq;   // lanes that saw a != b (wave-uniform mask)
+  // wave-uniform: a and b have been equal bitwise in every lane so far, so B
+  // would have received exactly A's updates; B is not updated then and takes
+  // A's state when the first difference comes (or at the end)
+  bool bsame;
 };
 
 // Wave partials, cross-wave combine and the tagged chunk record.
 template <int DT, int KIND, int DM>
-DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, const StatsAcc& q,
+DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, const StatsAcc& q0,
                        Smem& sm) {
   using TR = KindTraits<KIND>;
   constexpr int VE = Elem<DT>::VE;
   constexpr bool kDraft = TR::NS == 3;
   const int lane = lane_id(), w = wave_id();
-  const float c = g.c;
-  // wave partials: max, sum rescaled to the wave max
-  #define ASYM_WAVE_SLOT(S_, Q_, C_, USED_)                                  \
+  StatsAcc q = q0;
+  if (TR::kB && q.bsame) q.B = q.A;
+  // wave partials: the largest reference, the sums rescaled to it
+  #define ASYM_WAVE_SLOT(S_, Q_, USED_)                                      \
     {                                                                       \
-      float mw = kFloorM, sw = 0.0f;                                        \
+      float rw = kFloorM, sw = 0.0f;                                        \
       if (USED_) {                                                          \
-        mw = wave_max(Q_.m);                                                \
-        sw = wave_sum(Q_.s * __builtin_amdgcn_exp2f(Q_.R - mw * (C_)));     \
+        rw = wave_max(Q_.R);                                                \
+        sw = wave_sum(Q_.s * __builtin_amdgcn_exp2f(Q_.R - rw));            \
       }                                                                     \
-      if (lane == 0) { sm.wm[w][S_] = mw; sm.ws[w][S_] = sw; }              \
+      if (lane == 0) { sm.wm[w][S_] = rw; sm.ws[w][S_] = sw; }              \
     }
-  ASYM_WAVE_SLOT(sT, q.T, (kDraft ? kL2E : c), TR::kT)
-  ASYM_WAVE_SLOT(sA, q.A, kL2E, TR::kA)
-  ASYM_WAVE_SLOT(sB, q.B, kL2E, TR::kB)
-  ASYM_WAVE_SLOT(sF, q.F, c, TR::kF)
-  ASYM_WAVE_SLOT(sAT, q.AT, c, TR::kAT)
+  ASYM_WAVE_SLOT(sT, q.T, TR::kT)
+  ASYM_WAVE_SLOT(sA, q.A, TR::kA)
+  ASYM_WAVE_SLOT(sB, q.B, TR::kB)
+  ASYM_WAVE_SLOT(sF, q.F, TR::kF)
+  ASYM_WAVE_SLOT(sAT, q.AT, TR::kAT)
   #undef ASYM_WAVE_SLOT
   {
     int cand = 0x7FFFFFFF;
+    float mw = kFloorM;
     if (TR::kArg) {
       // the lanes holding the wave maximum re-read the vector where their
       // running maximum first reached it and take its first such element
       const Acc& qa = TR::argslot == sF ? q.F : q.T;
-      const float mw = wave_max(qa.m);
+      mw = wave_max(qa.m);
       if (qa.m == mw && mw > kFloorM) {
         const long long rv = rel0 + vec_rel(qa.pos);
         const long long vi = g.vbeg + rv;
@@ -127,37 +133,36 @@ DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, c
       cand = wave_min_i(cand);
     }
     const int wn = q.neq != 0 ? 1 : 0;
-    if (lane == 0) { sm.warg[w] = cand; sm.wneq[w] = wn; }
+    if (lane == 0) { sm.warg[w] = cand; sm.wneq[w] = wn; sm.wmarg[w] = mw; }
   }
   __syncthreads();
   // wave 0: lane s < kSlots combines slot s over the waves; lane kSlots the
-  // argmax and the a-vs-b flag; then the lanes publish the record
+  // argmax slot's maximum and index and the a-vs-b flag; then the lanes
+  // publish the record
   if (w == 0) {
     uint64_t* rec = A.rec1 + ((size_t)g.row * A.S + m) * kR1;
     if (lane < kSlots) {
-      const float cs = (lane == sA || lane == sB || (lane == sT && kDraft)) ? kL2E : c;
-      float M = kFloorM;
+      float R = kFloorM;
       #pragma unroll
-      for (int i = 0; i < kWaves; ++i) M = fmaxf(M, sm.wm[i][lane]);
-      const float R = M * cs;
+      for (int i = 0; i < kWaves; ++i) R = fmaxf(R, sm.wm[i][lane]);
       float S = 0.0f;
       #pragma unroll
-      for (int i = 0; i < kWaves; ++i) S += sm.ws[i][lane] * __builtin_amdgcn_exp2f(sm.wm[i][lane] * cs - R);
-      st_tag(rec + R1_M + lane, __float_as_uint(M), A.epoch);
+      for (int i = 0; i < kWaves; ++i) S += sm.ws[i][lane] * __builtin_amdgcn_exp2f(sm.wm[i][lane] - R);
+      st_tag(rec + R1_R + lane, __float_as_uint(R), A.epoch);
       st_tag(rec + R1_S + lane, __float_as_uint(S), A.epoch);
     } else if (lane == kSlots) {
-      constexpr int asl = TR::argslot;
       float Mall = kFloorM;
       #pragma unroll
-      for (int i = 0; i < kWaves; ++i) Mall = fmaxf(Mall, sm.wm[i][asl]);
+      for (int i = 0; i < kWaves; ++i) Mall = fmaxf(Mall, sm.wmarg[i]);
       int arg = 0x7FFFFFFF, nq = 0;
       #pragma unroll
       for (int i = 0; i < kWaves; ++i) {
-        if (sm.wm[i][asl] == Mall) arg = min(arg, sm.warg[i]);
+        if (sm.wmarg[i] == Mall) arg = min(arg, sm.warg[i]);
         nq |= sm.wneq[i];
       }
       st_tag(rec + R1_ARG, (uint32_t)arg, A.epoch);
       st_tag(rec + R1_NEQ, (uint32_t)nq, A.epoch);
+      st_tag(rec + R1_MARG, __float_as_uint(Mall), A.epoch);
     }
   }
 }
@@ -166,9 +171,18 @@ DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, c
 // compiler sinks the arithmetic of later vectors to the end of the chunk and
 // keeps all their loaded data live at once.
 DEV void pin(Acc& q) { asm volatile("" : "+v"(q.m), "+v"(q.R), "+v"(q.s)); }
+DEV void pin_lazy(Acc& q) { asm volatile("" : "+v"(q.R), "+v"(q.s)); }
+
+// One vector into a slot that needs no maximum: the full step on a thread's
+// first vector (kFirst), the lazy step after it.
+template <int VE, bool kClamp, bool kFirst>
+DEV void acc_sum(Acc& q, const float (&x)[VE], float c) {
+  if (kFirst) acc_vec<VE, kClamp, false>(q, x, c, 0);
+  else acc_vec_lazy<VE, kClamp>(q, x, c);
+}
 
 // One vector of each stream into the accumulators.
-template <int DT, int KIND, bool kB1, int DM, bool kClamp>
+template <int DT, int KIND, bool kB1, int DM, bool kClamp, bool kFirst>
 DEV void stats_vec(const KArgs& A, float c, const u4& vt, const u4& va, const u4& vb, int kk, StatsAcc& q) {
   using TR = KindTraits<KIND>;
   constexpr int VE = Elem<DT>::VE;
@@ -190,25 +204,40 @@ DEV void stats_vec(const KArgs& A, float c, const u4& vt, const u4& va, const u4
     uint64_t nm = __ballot((pa.x != pb.x) | (pa.y != pb.y));
     asm volatile("" : "+s"(nm));
     q.neq |= nm;
-    if (TR::kT) acc_vec<VE, false, false>(q.T, xt, kL2E, kk);
-    acc_vec<VE, kClamp, TR::kArg>(q.F, xf, c, kk);
-    if (TR::kA) acc_vec<VE, false, false>(q.A, xa, kL2E, kk);
-    if (TR::kB) acc_vec<VE, false, false>(q.B, xb, kL2E, kk);
-    if (TR::kAT) acc_vec<VE, false, false>(q.AT, xa, c, kk);
-    if (TR::kT) pin(q.T);
-    pin(q.F);
-    if (TR::kA) pin(q.A);
-    if (TR::kB) pin(q.B);
-    if (TR::kAT) pin(q.AT);
+    // B before A: while the views agree in every lane B is A (bsame)
+    if (TR::kB && !(q.bsame && nm == 0)) {
+      if (q.bsame) {
+        q.B = q.A;
+        q.bsame = false;
+      }
+      acc_sum<VE, false, kFirst>(q.B, xb, kL2E);
+    }
+    if (TR::kT) acc_sum<VE, false, kFirst>(q.T, xt, kL2E);
+    if (TR::kArg) acc_vec<VE, kClamp, true>(q.F, xf, c, kk);
+    else acc_sum<VE, kClamp, kFirst>(q.F, xf, c);
+    if (TR::kA) acc_sum<VE, false, kFirst>(q.A, xa, kL2E);
+    if (TR::kAT) acc_sum<VE, false, kFirst>(q.AT, xa, c);
+    if (TR::kT) pin_lazy(q.T);
+    if (TR::kArg) pin(q.F);
+    else pin_lazy(q.F);
+    if (TR::kA) pin_lazy(q.A);
+    if (TR::kB) pin_lazy(q.B);
+    if (TR::kAT) pin_lazy(q.AT);
   } else {
-    acc_vec<VE, false, TR::kArg>(q.T, xt, c, kk);
-    pin(q.T);
+    if (TR::kArg) {
+      acc_vec<VE, false, true>(q.T, xt, c, kk);
+      pin(q.T);
+    } else {
+      acc_sum<VE, false, kFirst>(q.T, xt, c);
+      pin_lazy(q.T);
+    }
   }
 }
 
 DEV void stats_init(StatsAcc& q, float c) {
   acc_init(q.T, c); acc_init(q.A, kL2E); acc_init(q.B, kL2E); acc_init(q.F, c); acc_init(q.AT, c);
   q.neq = 0;
+  q.bsame = true;
 }
 
 // Generic path: one vector at a time, every vector repaired (row boundary,
@@ -241,7 +270,7 @@ DEV void stats_slow(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
       fix_vec<DT>(A, g, A.a, vi, va);
       fix_vec<DT>(A, g, A.b, vi, vb);
     }
-    stats_vec<DT, KIND, kB1, DM, true>(A, g.c, vt, va, vb, kk, q);
+    stats_vec<DT, KIND, kB1, DM, true, true>(A, g.c, vt, va, vb, kk, q);
   }
   publish_stats<DT, KIND, DM>(A, g, m, rel0, q, sm);
 }
@@ -287,7 +316,12 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
     }
     // masked elements have a = b = -inf, so f is NaN there: the boundary
     // chunks clamp the exponent of f
-    stats_vec<DT, KIND, kB1, DM, kMask>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl], buf[NS == 3 ? 2 : 0][sl], j, q);
+    if (j == 0)
+      stats_vec<DT, KIND, kB1, DM, kMask, true>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl],
+                                                buf[NS == 3 ? 2 : 0][sl], j, q);
+    else
+      stats_vec<DT, KIND, kB1, DM, kMask, false>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl],
+                                                 buf[NS == 3 ? 2 : 0][sl], j, q);
     if (j + kWin < kVecs) {
       #pragma unroll
       for (int s = 0; s < NS; ++s) buf[s][sl] = buf_load_nt(r[s], off0 + (uint32_t)(vec_rel(j + kWin) * 16));
@@ -354,7 +388,7 @@ DEV void stats_dorder(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
       Elem<DT>::put_one(a2, e, xa);
       Elem<DT>::put_one(b2, e, xb);
     }
-    stats_vec<DT, KIND, kB1, DM, true>(A, g.c, t2, a2, b2, kk, q);
+    stats_vec<DT, KIND, kB1, DM, true, true>(A, g.c, t2, a2, b2, kk, q);
   }
   publish_stats<DT, KIND, DM>(A, g, m, rel0, q, sm);
 }

@@ -264,6 +264,30 @@ def workload_inputs(index: int, workers: int | None = None, **override) -> Input
     return generate(workers=workers, **kw)
 
 
+def workload_requests(index: int, lo: int, hi: int) -> Inputs:
+    """Requests lo..hi-1 of benchmark workload ``index``, identical to the
+    same requests of ``workload_inputs(index)`` (each request has its own
+    seeded stream), so that a subset can be regenerated in another process."""
+    wl = WORKLOADS[index]
+    if not (0 <= lo < hi <= wl.B):
+        raise ValueError("need 0 <= lo < hi <= B")
+    children = np.random.SeedSequence(wl.seed).spawn(wl.B)
+    wl_args = (wl.K, wl.V, wl.dtype, wl.prior, wl.rho, wl.tau)
+    n = hi - lo
+    np_dtype = np.uint16 if wl.dtype == BF16 else np.float32
+    t = np.empty((n, wl.K + 1, wl.V), np_dtype)
+    a = np.empty_like(t)
+    bb = np.empty_like(t)
+    d = np.zeros((n, wl.K), np.int32)
+    p = np.zeros((n, wl.K), np.float32)
+    u = np.zeros((n, wl.K + 1), np.float32)
+    tau = np.zeros(n, np.float32)
+    rho = np.zeros(n, np.float64)
+    for k, b in enumerate(range(lo, hi)):
+        t[k], a[k], bb[k], d[k], p[k], u[k], tau[k], rho[k] = _gen_request(wl_args, b, children[b], 0.0)
+    return Inputs(t, a, bb, d, p, u, tau, rho, wl.dtype)
+
+
 def replicate_for_mc(t_rows: np.ndarray, a_rows: np.ndarray, b_rows: np.ndarray,
                      tau: float, n: int, seed: int):
     """n copies of one request (rows [K+1][V], stored dtype) with fresh drafts

@@ -185,3 +185,20 @@ def test_xvocab_workspace_size():
     assert lib.asymspec_workspace_size_xvocab(128, 6, 151936, 0, asp.BF16) == 0
     assert lib.asymspec_workspace_size_xvocab(1, 1, 10, 4194298, asp.BF16) == 0   # > 256 chunks
     assert _call_xv(wsb=asp.workspace_size(2, 2, 64, 0)) == asp.E_WORKSPACE
+
+
+def test_timeout_count_and_wait_limit_host_checks():
+    """The timeout read-back and the wait-bound hook refuse invalid
+    arguments on the host (no device access: nothing is enqueued)."""
+    lib = asp.load_library()
+    n = ctypes.c_uint32(7)
+    fake = ctypes.c_void_p(1 << 20)
+    assert lib.asymspec_workspace_timeouts(None, 4096, None, ctypes.byref(n)) == asp.E_ARG
+    assert lib.asymspec_workspace_timeouts(fake, 4096, None, None) == asp.E_ARG
+    assert lib.asymspec_workspace_timeouts(fake, 128, None, ctypes.byref(n)) == asp.E_ARG
+    assert lib.asymspec_workspace_timeouts(ctypes.c_void_p((1 << 20) + 64), 4096, None,
+                                           ctypes.byref(n)) == asp.E_ARG
+    assert n.value == 7
+    assert lib.asymspec_set_wait_limit(100000001) == asp.E_ARG
+    assert lib.asymspec_set_wait_limit(5) == asp.OK
+    assert lib.asymspec_set_wait_limit(0) == asp.OK      # back to the default
