@@ -248,6 +248,51 @@ int asymspec_fuse_verify_xvocab(const void* verifier_logits,
                                 void* workspace, size_t workspace_bytes,
                                 void* stream);
 
+/* ---- the same step without a caller workspace ------------------------- */
+#define ASYMSPEC_NOALLOC_MAX_WORKSPACE (32u << 20)  /* bytes of static scratch per device */
+
+/*
+ * For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): asymspec_fuse_verify with
+ * every argument but the workspace, which is instead a static device array
+ * of ASYMSPEC_NOALLOC_MAX_WORKSPACE bytes that the library holds on each
+ * device it runs on, for the life of the process.  No device memory is
+ * allocated or freed by this call.
+ *   - Shapes whose asymspec_workspace_size exceeds the array return
+ *     ASYMSPEC_E_WORKSPACE with nothing enqueued (B = 512, K = 8, V = 256000
+ *     bf16 needs 16.6 MiB and fits).
+ *   - Every call on one device uses that device's array: calls that may
+ *     overlap on one device (other streams, other host threads) race and
+ *     must not be issued; calls in one stream are ordered and safe.
+ *   - Nothing in the array must start at zero: every record the kernel
+ *     exchanges carries the call's epoch.  Its timeout counter is read with
+ *     asymspec_noalloc_timeouts (cumulative over the process).
+ *   - The epoch is still a launch argument chosen here at each call, so a
+ *     captured call must not be replayed (see asymspec_workspace_size).
+ * Returns the status codes of asymspec_fuse_verify, or ASYMSPEC_E_DEVICE
+ * when the array's device address cannot be found.
+ */
+int asymspec_fuse_verify_noalloc(const void* verifier_logits,
+                                 const void* drafter_full_logits,
+                                 const void* drafter_comp_logits,
+                                 int dtype,
+                                 const int32_t* draft_tokens,
+                                 const float* draft_probs,
+                                 const float* uniforms,
+                                 const float* temperature,
+                                 int B, int K, int V,
+                                 const asymspec_params* params,
+                                 int32_t* accept_len,
+                                 int32_t* next_token,
+                                 float* fused_logprobs,
+                                 float* gate_out,
+                                 float* fused_logprobs_full,
+                                 void* stream);
+
+/* Timed-out waits counted in the current device's static array (see
+ * asymspec_workspace_timeouts; synchronises `stream`). */
+int asymspec_noalloc_timeouts(void* stream, uint32_t* count);
+
 /* Number of timed-out waits between workgroups recorded in `workspace`
  * since it was last zero-filled (asymspec_workspace_clear, or a zeroed
  * allocation), into *count (a host pointer).  The decision kernel's

@@ -83,6 +83,11 @@ def load_library(path: str | None = None):
     lib.asymspec_workspace_timeouts.restype = i32
     lib.asymspec_set_wait_limit.argtypes = [ctypes.c_ulonglong]
     lib.asymspec_set_wait_limit.restype = i32
+    lib.asymspec_fuse_verify_noalloc.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, i32, i32, i32,
+                                                 ctypes.POINTER(_Params), vp, vp, vp, vp, vp, vp]
+    lib.asymspec_fuse_verify_noalloc.restype = i32
+    lib.asymspec_noalloc_timeouts.argtypes = [vp, ctypes.POINTER(ctypes.c_uint32)]
+    lib.asymspec_noalloc_timeouts.restype = i32
     if path is None:
         _lib = lib
     return lib

@@ -270,6 +270,33 @@ static const DevInfo* device_info() {
   return &di;
 }
 
+// Static scratch of the non-allocating entry point: the workspace of calls
+// whose callers cannot allocate.  Each device that loads the library holds
+// its own copy until the process ends; its address on a device comes from
+// hipGetSymbolAddress with that device current (the array's name in host
+// code is not a device address).
+constexpr size_t kScratchBytes = (size_t)ASYMSPEC_NOALLOC_MAX_WORKSPACE;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+static void* g_scratch[64];
+static std::mutex g_scratch_mu;
+
+// The device address of the current device's scratch, looked up once per
+// device; null when the lookup fails.
+static void* scratch_ptr() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch[dev] = p;
+  }
+  return g_scratch[dev];
+}
+
 static uint32_t next_epoch() {
   static std::atomic<uint32_t> ctr{0};
   static std::once_flag once;
@@ -451,6 +478,29 @@ int asymspec_fuse_verify_xvocab(const void* t, const void* a, const void* b, int
   return fuse_verify_impl(t, a, b, dtype, vocab_map, Vd, draft_tokens, draft_probs, uniforms, temperature, B, K,
                           V, params, accept_len, next_token, fused_logprobs, gate_out, fused_logprobs_full,
                           workspace, workspace_bytes, stream);
+}
+
+int asymspec_fuse_verify_noalloc(const void* t, const void* a, const void* b, int dtype,
+                                 const int32_t* draft_tokens, const float* draft_probs,
+                                 const float* uniforms, const float* temperature,
+                                 int B, int K, int V, const asymspec_params* params,
+                                 int32_t* accept_len, int32_t* next_token, float* fused_logprobs,
+                                 float* gate_out, float* fused_logprobs_full, void* stream) {
+  Layout L;
+  if (!make_layout(B, K, V, dtype, L)) return ASYMSPEC_E_ARG;
+  if (L.total > kScratchBytes) return ASYMSPEC_E_WORKSPACE;
+  void* ws = scratch_ptr();
+  if (ws == nullptr) return ASYMSPEC_E_DEVICE;
+  return fuse_verify_impl(t, a, b, dtype, nullptr, 0, draft_tokens, draft_probs, uniforms, temperature, B, K, V,
+                          params, accept_len, next_token, fused_logprobs, gate_out, fused_logprobs_full, ws,
+                          kScratchBytes, stream);
+}
+
+int asymspec_noalloc_timeouts(void* stream, uint32_t* count) {
+  if (count == nullptr) return ASYMSPEC_E_ARG;
+  void* ws = scratch_ptr();
+  if (ws == nullptr) return ASYMSPEC_E_DEVICE;
+  return asymspec_workspace_timeouts(ws, kScratchBytes, stream, count);
 }
 
 int asymspec_workspace_timeouts(const void* workspace, size_t workspace_bytes, void* stream,

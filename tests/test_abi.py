@@ -202,3 +202,23 @@ def test_timeout_count_and_wait_limit_host_checks():
     assert lib.asymspec_set_wait_limit(100000001) == asp.E_ARG
     assert lib.asymspec_set_wait_limit(5) == asp.OK
     assert lib.asymspec_set_wait_limit(0) == asp.OK      # back to the default
+
+
+def test_noalloc_refuses_shapes_beyond_the_array():
+    """The non-allocating entry point refuses, on the host with nothing
+    enqueued, a shape whose workspace exceeds its static array, and invalid
+    shapes (the fake pointers are never dereferenced)."""
+    lib = asp.load_library()
+    fake = ctypes.c_void_p(1 << 20)
+    params = asp._Params(1.0, 0.5, 0, 0, 0, 0.1, 0)
+    B, K, V = 2048, 8, 256000
+    assert asp.workspace_size(B, K, V, asp.BF16) > 32 << 20
+    assert asp.workspace_size(512, 8, 256000, asp.BF16) <= 32 << 20
+    st = lib.asymspec_fuse_verify_noalloc(fake, fake, fake, asp.BF16, fake, None, fake, fake, B, K, V,
+                                          ctypes.byref(params), fake, fake, fake, None, None, None)
+    assert st == asp.E_WORKSPACE
+    st = lib.asymspec_fuse_verify_noalloc(fake, fake, fake, asp.BF16, fake, None, fake, fake, 0, K, V,
+                                          ctypes.byref(params), fake, fake, fake, None, None, None)
+    assert st == asp.E_ARG
+    n = ctypes.c_uint32(0)
+    assert lib.asymspec_noalloc_timeouts(None, None) == asp.E_ARG
