@@ -42,7 +42,7 @@
 
 namespace asym {
 
-template <int DT, bool kB1, int DM>
+template <int DT, bool kB1, int DM, bool kKL>
 DEV void stats_chunk(const KArgs& A, int req, int i, int m, Smem& sm) {
   const int row = req * (A.K + 1) + i;
   const float tau = sload_f32(A.tau, req);
@@ -56,11 +56,11 @@ DEV void stats_chunk(const KArgs& A, int req, int i, int m, Smem& sm) {
       stats_item<DT, kGreedyBonus, kB1, DM>(A, row, m, sm);
     }
   } else if (!(tau > 0.0f)) {
-    stats_item<DT, kGreedyDraft, kB1, DM>(A, row, m, sm);
+    stats_item<DT, kGreedyDraft, kB1, DM, kKL>(A, row, m, sm);
   } else if (tau == 1.0f) {
-    stats_item<DT, kSampleDraft1, kB1, DM>(A, row, m, sm);
+    stats_item<DT, kSampleDraft1, kB1, DM, kKL>(A, row, m, sm);
   } else {
-    stats_item<DT, kSampleDraftT, kB1, DM>(A, row, m, sm);
+    stats_item<DT, kSampleDraftT, kB1, DM, kKL>(A, row, m, sm);
   }
 }
 
@@ -69,7 +69,7 @@ DEV void stats_chunk(const KArgs& A, int req, int i, int m, Smem& sm) {
 // gathers from the whole of the row's drafter logits; the items of a request
 // are then renumbered so that those sharing an XCD take consecutive chunks
 // of the same rows, and each XCD's L2 holds few drafter rows at a time.
-template <int DT, bool kB1, int DM>
+template <int DT, bool kB1, int DM, bool kKL>
 DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
   int p = sub;
   if (A.vmap != nullptr) {
@@ -78,7 +78,7 @@ DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
     p = sub < n1 ? xcd_grouped(sub, n1) : n1 + xcd_grouped(sub - n1, n - n1);
   }
   const int i = p / A.S, m = p - i * A.S;
-  stats_chunk<DT, kB1, DM>(A, req, i, m, sm);
+  stats_chunk<DT, kB1, DM, kKL>(A, req, i, m, sm);
 }
 
 
@@ -92,7 +92,10 @@ DEV void stats_dispatch(const KArgs& A, int req, int sub, Smem& sm) {
 // running or queued behind workgroups that never wait: the list drains
 // whether or not every workgroup fits on the chip at once.  The waits are
 // bounded besides (Poll), and a timeout is counted in the workspace.
-template <int DT, bool kB1, int DM>
+// kKL: calls with the KL gate, whose draft rows also sum the divergence
+// beside the A slot (a kernel of its own, so that the extra registers of
+// those items do not weigh on the other gates' kernels).
+template <int DT, bool kB1, int DM, bool kKL>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ASYMSPEC_WAVES)))
 void fuse_verify_kernel(KArgs A) {
   __shared__ Smem sm;
@@ -108,7 +111,7 @@ void fuse_verify_kernel(KArgs A) {
   }
   // one call site per item kind keeps a single inlined copy of each
   switch (type) {
-    case kItemStats: stats_dispatch<DT, kB1, DM>(A, it.req, it.sub, sm); break;
+    case kItemStats: stats_dispatch<DT, kB1, DM, kKL>(A, it.req, it.sub, sm); break;
     case kItemVerdict:
     case kItemDecide: decide_item<DT>(A, it.req, sm, type == kItemVerdict); break;
     case kItemPass2: pass2_item<DT, DM>(A, it.req, it.sub, sm); break;
@@ -213,21 +216,28 @@ static std::mutex g_dev_mu;
 static_assert(kDeltaAB == ASYMSPEC_DELTA_AB && kDeltaA == ASYMSPEC_DELTA_A && kDeltaTB == ASYMSPEC_DELTA_TB,
               "delta sources");
 
-// One kernel per storage type, beta == 1 or not, and source of delta.
+// One kernel per storage type, beta == 1 or not, and source of delta; the
+// KL gate has its own kernels (beta taken at run time: fl(1 * x) = x, so a
+// call with beta = 1 computes the same values).
 template <int DT>
-static const void* kernel_ptr_dt(bool beta1, int dm) {
-  if (beta1) {
-    if (dm == kDeltaA) return (const void*)fuse_verify_kernel<DT, true, kDeltaA>;
-    if (dm == kDeltaTB) return (const void*)fuse_verify_kernel<DT, true, kDeltaTB>;
-    return (const void*)fuse_verify_kernel<DT, true, kDeltaAB>;
+static const void* kernel_ptr_dt(bool beta1, int dm, bool kl) {
+  if (kl) {
+    if (dm == kDeltaA) return (const void*)fuse_verify_kernel<DT, false, kDeltaA, true>;
+    if (dm == kDeltaTB) return (const void*)fuse_verify_kernel<DT, false, kDeltaTB, true>;
+    return (const void*)fuse_verify_kernel<DT, false, kDeltaAB, true>;
   }
-  if (dm == kDeltaA) return (const void*)fuse_verify_kernel<DT, false, kDeltaA>;
-  if (dm == kDeltaTB) return (const void*)fuse_verify_kernel<DT, false, kDeltaTB>;
-  return (const void*)fuse_verify_kernel<DT, false, kDeltaAB>;
+  if (beta1) {
+    if (dm == kDeltaA) return (const void*)fuse_verify_kernel<DT, true, kDeltaA, false>;
+    if (dm == kDeltaTB) return (const void*)fuse_verify_kernel<DT, true, kDeltaTB, false>;
+    return (const void*)fuse_verify_kernel<DT, true, kDeltaAB, false>;
+  }
+  if (dm == kDeltaA) return (const void*)fuse_verify_kernel<DT, false, kDeltaA, false>;
+  if (dm == kDeltaTB) return (const void*)fuse_verify_kernel<DT, false, kDeltaTB, false>;
+  return (const void*)fuse_verify_kernel<DT, false, kDeltaAB, false>;
 }
-static const void* kernel_ptr(int dtype, bool beta1, int dm) {
-  return dtype == ASYMSPEC_BF16 ? kernel_ptr_dt<ASYMSPEC_BF16>(beta1, dm)
-                                : kernel_ptr_dt<ASYMSPEC_FP32>(beta1, dm);
+static const void* kernel_ptr(int dtype, bool beta1, int dm, bool kl) {
+  return dtype == ASYMSPEC_BF16 ? kernel_ptr_dt<ASYMSPEC_BF16>(beta1, dm, kl)
+                                : kernel_ptr_dt<ASYMSPEC_FP32>(beta1, dm, kl);
 }
 template <int DT>
 static const void* dump_ptr_dt(int dm) {
@@ -251,13 +261,12 @@ static const DevInfo* device_info() {
   di.n_cu = pr.multiProcessorCount;
   for (int dt = 0; dt < 2; ++dt) {
     int nb = 1 << 30, nx = 1 << 30;
-    for (int b1 = 0; b1 < 2; ++b1)
+    for (int v = 0; v < 3; ++v)
       for (int dm = 0; dm < 3; ++dm) {
         int x = 0, y = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&x, kernel_ptr(dt, b1 != 0, dm), kThreads, 0) !=
-                hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&y, kernel_ptr(dt, b1 != 0, dm), kThreads, kXvLds) !=
-                hipSuccess)
+        const void* k = kernel_ptr(dt, v == 0, dm, v == 2);
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&x, k, kThreads, 0) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&y, k, kThreads, kXvLds) != hipSuccess)
           return nullptr;
         nb = std::min(nb, x);
         nx = std::min(nx, y);
@@ -438,7 +447,8 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
     if (e != hipSuccess) return ASYMSPEC_E_DEVICE;
   }
   void* args[] = {&A};
-  e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f, params->delta_mode), dim3(grid),
+  e = hipLaunchKernel(kernel_ptr(dtype, params->beta == 1.0f, params->delta_mode,
+                                 params->gate_mode == ASYMSPEC_GATE_KL), dim3(grid),
                                  dim3(kThreads), args, vmap != nullptr ? kXvLds : 0, (hipStream_t)stream);
   if (e == hipSuccess && fused_logprobs_full != nullptr) {
     // one workgroup per (row, chunk), after the decision kernel on the stream

@@ -8,6 +8,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cfloat>
 #include <cstdint>
 
 #include "asymspec.h"
@@ -68,8 +69,11 @@ enum Slot { sT = 0, sA = 1, sB = 2, sF = 3, sAT = 4, kSlots = 5 };
 // for greedy drafts, t for the greedy bonus row) and the first index where
 // the chunk attains it, and whether a and b differ bitwise anywhere in the
 // chunk.
+// Calls with the KL gate also carry W, the sum of exp2(a * log2 e - R_A) (a -
+// b) relative to the A slot's reference: KL(P || Q) = W / S_A - (LA - LB) in
+// nats, with no second pass.
 enum { R1_R = 0, R1_S = kSlots, R1_ARG = 2 * kSlots, R1_NEQ = 2 * kSlots + 1, R1_MARG = 2 * kSlots + 2,
-       R1_USED = 2 * kSlots + 3, kR1 = 16 };
+       R1_W = 2 * kSlots + 3, R1_USED = 2 * kSlots + 4, kR1 = 16 };
 
 // Decision record of one request: a header and one block per row, published
 // by the decide item; pass-2 and pick items load it into LDS (Smem::req,
@@ -97,7 +101,7 @@ enum {
   D_L2E_LO, D_L2E_HI,   // log2 normaliser (fp64) of the emission distribution
   D_ARG,        // greedy: argmax of f (drafts) or t (bonus)
   D_LPEMIT,     // greedy: log-probability of that argmax
-  D_GD_LO, D_GD_HI,     // lambda gate: D = lambda * Delta(d) (fp64)
+  D_GD_LO, D_GD_HI,     // D known at the decide (lambda and KL gates; fp64)
   D_USED,
   kDecRow = 24
 };
@@ -499,6 +503,53 @@ DEV void acc_vec_lazy(Acc& q, const float (&x)[VE], float c) {
   q.s += v;
 }
 
+// The same two steps for the A slot of calls with the KL gate, which also
+// keep W = sum of exp2(x * c - R) d, d = a - b with -inf (a token the full
+// view masks, whose term is 0) raised to -FLT_MAX so that 0 * d stays 0.
+template <int VE, bool kFirst>
+DEV void acc_vec_w(Acc& q, float& W, const float (&x)[VE], const float (&d)[VE], float c) {
+  float ex[VE];
+  float R = q.R;
+  if (kFirst) {
+    float vm = x[0];
+    #pragma unroll
+    for (int e = 1; e < VE; ++e) vm = fmaxf(vm, x[e]);
+    q.m = fmaxf(q.m, vm);
+    R = q.m * c;
+  }
+  #pragma unroll
+  for (int e = 0; e < VE; ++e) ex[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[e], c, -R));
+  float v = ex[0], w = ex[0] * fmaxf(d[0], -FLT_MAX);
+  #pragma unroll
+  for (int e = 1; e < VE; ++e) {
+    v += ex[e];
+    w = __builtin_fmaf(ex[e], fmaxf(d[e], -FLT_MAX), w);
+  }
+  if (!kFirst && __builtin_expect(__ballot(v > 0x1p64f) != 0, 0)) {
+    float vm = x[0];
+    #pragma unroll
+    for (int e = 1; e < VE; ++e) vm = fmaxf(vm, x[e]);
+    R = fmaxf(q.R, vm * c);
+    #pragma unroll
+    for (int e = 0; e < VE; ++e) ex[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[e], c, -R));
+    v = ex[0];
+    w = ex[0] * fmaxf(d[0], -FLT_MAX);
+    #pragma unroll
+    for (int e = 1; e < VE; ++e) {
+      v += ex[e];
+      w = __builtin_fmaf(ex[e], fmaxf(d[e], -FLT_MAX), w);
+    }
+  }
+  if (R != q.R) {
+    const float scale = __builtin_amdgcn_exp2f(q.R - R);
+    q.s *= scale;
+    W *= scale;
+    q.R = R;
+  }
+  q.s += v;
+  W += w;
+}
+
 // --------------------------------------------------- pass-2 element terms
 // Shared by pass 2 and the emission scan so that both see identical values.
 struct ResidConst { float beta, c, Rf, isf, Rq, isq; };
@@ -526,15 +577,6 @@ DEV float jsd_elem(float a, float b, const JsdConst& k) {
   const float g = 1.0f - __builtin_amdgcn_logf(fmaxf(P + Q, 1e-37f));
   return __builtin_fmaf(P, lp + g, Q * (lq + g));
 }
-// KL term P log2(P/Q) of KL(softmax(a) || softmax(b)) (the gate of App. G),
-// 0 where P = 0.
-DEV float kl_elem(float a, float b, const JsdConst& k) {
-  const float lp = (fmaxf(__builtin_fmaf(a, kL2E, -k.Ra), kFloorM) - k.kahi) - k.kalo;
-  const float lq = (fmaxf(__builtin_fmaf(b, kL2E, -k.Rb), kFloorM) - k.kbhi) - k.kblo;
-  const float P = __builtin_amdgcn_exp2f(lp);
-  return P > 0.0f ? P * (lp - lq) : 0.0f;
-}
-
 // log2 of a positive double to ~1e-7 absolute: exact exponent split plus the
 // hardware log2 of the mantissa.
 DEV double log2_dbl(double x) {
@@ -770,12 +812,14 @@ struct Smem {
   int warg[kWaves];
   int wneq[kWaves];
   float wmarg[kWaves];
+  float wkl[kWaves];
   // decision of a request: per-row blocks, request words, and the
   // per-(row, chunk) values the decide item combines into them
   uint32_t rows[kMaxK + 1][kDecRow];
   uint32_t req[kReqWords];
   float dm[kThreads][kSlots];
   float dmarg[kThreads];
+  double dw[kThreads];
   double dt[kThreads][kSlots];
   int darg[kThreads];
   int dneq[kThreads];

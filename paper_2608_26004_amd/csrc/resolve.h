@@ -51,7 +51,7 @@ DEV JsdConst jsd_const(const uint32_t* cst) {
 // whether a and b differ.  Fills the row's decision block v (kDecRow words).
 template <int DT>
 DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, float Marg,
-                      const float (&R)[kSlots], const double (&Sp)[kSlots], int arg, bool neq,
+                      const float (&R)[kSlots], const double (&Sp)[kSlots], double Wkl, int arg, bool neq,
                       uint32_t* v) {
   const int kind = g.kind;
   const bool draft = kind_draft(kind);
@@ -75,13 +75,23 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, float M
     v[D_KBHI] = __float_as_uint(kbhi);
     v[D_KBLO] = __float_as_uint((float)(kb - (double)kbhi));
     const float fd = fuse_masked(gq.t, gq.a, gq.b, A.beta, A.delta_mode);
-    // lambda gate (App. B): D = lambda * Delta(d), Delta the drafter views'
-    // log-probability difference at the draft token; decided here
+    // gates whose D is known here, so that the row is decided at once:
+    // lambda (App. B), D = lambda * Delta(d), Delta the drafter views'
+    // log-probability difference at the draft token; KL (App. G),
+    // D = KL(P || Q) = E_P[a - b] - (LA - LB) from the statistics (a
+    // negative rounding residue is 0; an undefined sum, only from an input
+    // with b = -inf under a finite a, is +inf)
     double Dl = 0.0;
+    const bool dknown = gm == ASYMSPEC_GATE_LAMBDA || gm == ASYMSPEC_GATE_KL;
     if (gm == ASYMSPEC_GATE_LAMBDA) {
       const double lpa = ((double)gq.a * (double)kL2E - L2[sA]) * kLn2;
       const double lpb1 = ((double)gq.b * (double)kL2E - L2[sB]) * kLn2;
       Dl = (double)A.lam * (lpa - lpb1);
+    } else if (gm == ASYMSPEC_GATE_KL) {
+      Dl = neq ? Wkl / Sp[sA] - (L2[sA] - L2[sB]) * kLn2 : 0.0;
+      Dl = Dl != Dl ? INFINITY : (Dl < 0.0 ? 0.0 : Dl);
+    }
+    if (dknown) {
       v[D_GD_LO] = dlo(Dl);
       v[D_GD_HI] = dhi(Dl);
     }
@@ -99,7 +109,7 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, float M
       v[D_L2E_HI] = dhi(L2[sF]);
       // D >= 0 for the divergence gates (and D = 0 when a == b bitwise),
       // D <= ln 2 for the JSD; outside those bounds the row stays open
-      if (gm == ASYMSPEC_GATE_LAMBDA) accept = m0 + Dl > 0.0;
+      if (dknown) accept = m0 + Dl > 0.0;
       else if (gm == ASYMSPEC_GATE_FIXED || !neq) accept = m0 > 0.0;
       else if (m0 > 0.0) accept = 1;
       else if (gm == ASYMSPEC_GATE_CDA && m0 + kLn2 <= 0.0) accept = 0;
@@ -120,7 +130,7 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, float M
       else if (lq == -INFINITY) x = INFINITY;
       else x = lpd - lq - A.ln_gamma;
       const double lnu = gq.u > 0.0f ? ln_f(gq.u) : -INFINITY;
-      if (gm == ASYMSPEC_GATE_LAMBDA) {
+      if (dknown) {
         if (lpd == -INFINITY) accept = 0;          // p~(d) = 0 rejects
         else if (lq == -INFINITY) accept = 1;      // q(d) = 0 accepts
         else accept = lnu < x + Dl;
@@ -241,6 +251,7 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
       #pragma unroll
       for (int s = 0; s < kSlots; ++s)
         sm.dt[tid][s] = (double)payf(r[R1_S + s]) * exp2((double)payf(r[R1_R + s]) - (double)Rr[s]);
+      sm.dw[tid] = (double)payf(r[R1_W]) * exp2((double)payf(r[R1_R + sA]) - (double)Rr[sA]);
       sm.darg[tid] = payf(r[R1_MARG]) == Marg ? (int)pay(r[R1_ARG]) : 0x7FFFFFFF;
       sm.dneq[tid] = (int)pay(r[R1_NEQ]);
     }
@@ -250,13 +261,15 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
       #pragma unroll
       for (int s = 0; s < kSlots; ++s) Sp[s] = 0.0;
       int arg = 0x7FFFFFFF, nq = 0;
+      double Wkl = 0.0;
       for (int c = 0; c < S; ++c) {
         #pragma unroll
         for (int s = 0; s < kSlots; ++s) Sp[s] += sm.dt[tid + c][s];
+        Wkl += sm.dw[tid + c];
         arg = min(arg, sm.darg[tid + c]);
         nq |= sm.dneq[tid + c];
       }
-      classify_row<DT>(A, g, gq, Marg, Rr, Sp, arg, nq != 0, sm.rows[i]);
+      classify_row<DT>(A, g, gq, Marg, Rr, Sp, Wkl, arg, nq != 0, sm.rows[i]);
     }
     __syncthreads();
   }
@@ -288,7 +301,8 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
     // pass 2 computes D (JSD, or KL for that gate) for the open rows and,
     // when the gate output is wanted, for every row whose views differ; the
     // lambda gate's D is known here
-    if (is_draft && A.gate_mode != ASYMSPEC_GATE_LAMBDA && (open || (A.want_gate && neq))) task |= kTaskJsd;
+    const bool dknown = A.gate_mode == ASYMSPEC_GATE_LAMBDA || A.gate_mode == ASYMSPEC_GATE_KL;
+    if (is_draft && !dknown && (open || (A.want_gate && neq))) task |= kTaskJsd;
     if (samp && is_draft && (open || lane == jstar)) task |= kTaskRes;
     // the bonus draw: softmax(t / tau), or the fused row's p~ as a residual
     if (samp && lane == K && jstar == K) task |= A.fuse_bonus ? kTaskRes : kTaskBonus;
@@ -403,7 +417,7 @@ DEV void decide_item(const KArgs& A, int req, Smem& sm, bool verdict) {
       const float lpd = lane < K ? __uint_as_float(sm.rows[lane][D_LPD]) : 0.0f;
       // D of the rows: 0 (no view difference, or no D wanted) or the
       // lambda gate's, known here
-      const double dl = (lane < K && A.gate_mode == ASYMSPEC_GATE_LAMBDA)
+      const double dl = (lane < K && (A.gate_mode == ASYMSPEC_GATE_LAMBDA || A.gate_mode == ASYMSPEC_GATE_KL))
                             ? u2d(sm.rows[lane][D_GD_LO], sm.rows[lane][D_GD_HI])
                             : 0.0;
       const bool skip = lane <= K && (sm.rows[lane][D_STATUS] & kStSkip) != 0u;
@@ -469,10 +483,9 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
 // Pass-2 sums of one thread over its kSegPerLane vectors of a chunk.
 // kMode 0: interior chunk (no masking); 1: masked, branch-free; 2: generic
 // (one vector at a time, array-end repair).
-// kKL: the divergence term is KL's (the KL gate) rather than the JSD's.
 // kNb: a and b differ somewhere in the row; otherwise b is a bitwise copy of
 // a and a's vectors stand in for it (such a row has no divergence task).
-template <int DT, int kMode, int DM, bool kKL, bool kNb, bool kResOnly = false>
+template <int DT, int kMode, int DM, bool kNb, bool kResOnly = false>
 DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj_in, bool dr_in, bool db_in,
                     const ResidConst& rk, const JsdConst& jk, float& accj, float& seg) {
   constexpr int VE = Elem<DT>::VE;
@@ -518,7 +531,7 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj_in,
         #pragma unroll
         for (int e = 0; e < VE; ++e) {
           const float xa = Elem<DT>::get(va[k], e), xb = Elem<DT>::get(vb[k], e);
-          vj[e] = kKL ? kl_elem(xa, xb, jk) : jsd_elem(xa, xb, jk);
+          vj[e] = jsd_elem(xa, xb, jk);
         }
         #pragma unroll
         for (int st = 1; st < VE; st <<= 1)
@@ -544,21 +557,21 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj_in,
   }
 }
 
-template <int DT, int DM, bool kKL, bool kNb>
+template <int DT, int DM, bool kNb>
 DEV void pass2_sums_any(const KArgs& A, const RowGeo& g, long long rel0, long long c0, long long c1,
                         bool dj, bool dr, bool db, const ResidConst& rk, const JsdConst& jk, float& accj,
                         float& seg) {
   constexpr int VE = Elem<DT>::VE;
   if (A.vmap != nullptr || has_tail(A, c0, c1))
-    pass2_sums<DT, 2, DM, kKL, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 2, DM, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
   else if (dr && !dj && !db && c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
-    pass2_sums<DT, 0, DM, false, kNb, true>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 0, DM, kNb, true>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
   else if (dr && !dj && !db)
-    pass2_sums<DT, 1, DM, false, kNb, true>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 1, DM, kNb, true>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
   else if (c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
-    pass2_sums<DT, 0, DM, kKL, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 0, DM, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
   else
-    pass2_sums<DT, 1, DM, kKL, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 1, DM, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
 }
 
 template <int DT, int DM>
@@ -581,14 +594,11 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
     const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
     float accj = 0.0f, seg = 0.0f;
     if (task != 0) {
-      // JSD rows of the KL gate take the KL term (a rare, separate instance);
       // a row with a == b bitwise has no divergence task and skips b
-      if (dj && A.gate_mode == ASYMSPEC_GATE_KL)
-        pass2_sums_any<DT, DM, true, true>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
-      else if ((cst[D_STATUS] & kStNeq) != 0u || A.vmap != nullptr)
-        pass2_sums_any<DT, DM, false, true>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
+      if ((cst[D_STATUS] & kStNeq) != 0u || A.vmap != nullptr)
+        pass2_sums_any<DT, DM, true>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
       else
-        pass2_sums_any<DT, DM, false, false>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
+        pass2_sums_any<DT, DM, false>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
     }
     const float wj = wave_sum(accj);
     const float wseg = wave_sum(seg);
@@ -834,17 +844,12 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
       double part = 0.0;
       for (int c = lane; c < A.S; c += 64) part += wait_pair(p2_rec(A, req, i, c) + P2_J, A, ok);
       part = wave_sum_d(part);
-      // the partials are in log2 units; JSD = half their sum, within
-      // [0, ln 2]; KL = their sum, >= 0
-      if (A.gate_mode == ASYMSPEC_GATE_KL) {
-        const double D = kLn2 * part;
-        if (lane == i) Dl = D < 0.0 ? 0.0 : D;
-      } else {
-        const double D = 0.5 * kLn2 * part;
-        if (lane == i) Dl = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
-      }
+      // the partials are in log2 units; JSD = half their sum, within [0, ln 2]
+      const double D = 0.5 * kLn2 * part;
+      if (lane == i) Dl = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
     }
-    if (A.gate_mode == ASYMSPEC_GATE_LAMBDA && lane < K) Dl = u2d(sm.rows[lane][D_GD_LO], sm.rows[lane][D_GD_HI]);
+    if ((A.gate_mode == ASYMSPEC_GATE_LAMBDA || A.gate_mode == ASYMSPEC_GATE_KL) && lane < K)
+      Dl = u2d(sm.rows[lane][D_GD_LO], sm.rows[lane][D_GD_HI]);
     const bool decided = st & kStDecided;
     const bool acc = decided ? (st & kStAccept) != 0 : (Dl > thr);
     const int jr = wave_min_i(is_draft && !acc ? lane : 0x7FFFFFFF);

@@ -158,15 +158,23 @@ inline bool sched_build(int B, int K, int S, int items_in_flight, Sched& sc, int
 ASYM_HD inline Item sched_item(const Sched& sc, int K, int S, int idx) {
   Item it{kItemNone, 0, 0};
   if (idx < 0 || idx >= sc.total) return it;
-  int r = 0;
-  for (int k = 1; k < sc.n_runs; ++k)
-    if (idx >= sc.i0[k]) r = k;
-  const int off = idx - sc.i0[r];
-  const int blk = sc.blk[r];
+  // the run holding idx, found with constant indices only (in a kernel the
+  // schedule is part of a by-value argument, which a variable index would
+  // force into private memory)
+  int i0 = sc.i0[0], blk = sc.blk[0], q0 = sc.q0[0], parts = sc.parts[0];
+  #pragma unroll
+  for (int k = 1; k < kMaxRuns; ++k) {
+    if (k < sc.n_runs && idx >= sc.i0[k]) {
+      i0 = sc.i0[k];
+      blk = sc.blk[k];
+      q0 = sc.q0[k];
+      parts = sc.parts[k];
+    }
+  }
+  const int off = idx - i0;
   const int qs = off / blk;
   int o = off - qs * blk;
-  const int q = sc.q0[r] + qs;
-  const int parts = sc.parts[r];
+  const int q = q0 + qs;
   const int n1 = sc.G * S, n2 = (K + 1 - sc.G) * S;
   if (parts & kPartStats) {
     if (o < n1) { it.type = kItemStats; it.req = q; it.sub = o; return it; }

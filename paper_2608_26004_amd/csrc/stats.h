@@ -70,10 +70,11 @@ struct StatsAcc {
   // would have received exactly A's updates; B is not updated then and takes
   // A's state when the first difference comes (or at the end)
   bool bsame;
+  float W;        // KL gate: the A-weighted sum of a - b (see R1_W)
 };
 
 // Wave partials, cross-wave combine and the tagged chunk record.
-template <int DT, int KIND, int DM>
+template <int DT, int KIND, int DM, bool kKL>
 DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, const StatsAcc& q0,
                        Smem& sm) {
   using TR = KindTraits<KIND>;
@@ -98,6 +99,11 @@ DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, c
   ASYM_WAVE_SLOT(sF, q.F, TR::kF)
   ASYM_WAVE_SLOT(sAT, q.AT, TR::kAT)
   #undef ASYM_WAVE_SLOT
+  if (kKL && TR::kA) {
+    const float rw = wave_max(q.A.R);
+    const float ww = wave_sum(q.W * __builtin_amdgcn_exp2f(q.A.R - rw));
+    if (lane == 0) sm.wkl[w] = ww;
+  }
   {
     int cand = 0x7FFFFFFF;
     float mw = kFloorM;
@@ -163,6 +169,17 @@ DEV void publish_stats(const KArgs& A, const RowGeo& g, int m, long long rel0, c
       st_tag(rec + R1_ARG, (uint32_t)arg, A.epoch);
       st_tag(rec + R1_NEQ, (uint32_t)nq, A.epoch);
       st_tag(rec + R1_MARG, __float_as_uint(Mall), A.epoch);
+    } else if (lane == kSlots + 1) {
+      // the KL sum, relative to the A slot's chunk reference (0 without it)
+      float W = 0.0f;
+      if (kKL && TR::kA) {
+        float R = kFloorM;
+        #pragma unroll
+        for (int i = 0; i < kWaves; ++i) R = fmaxf(R, sm.wm[i][sA]);
+        #pragma unroll
+        for (int i = 0; i < kWaves; ++i) W += sm.wkl[i] * __builtin_amdgcn_exp2f(sm.wm[i][sA] - R);
+      }
+      st_tag(rec + R1_W, __float_as_uint(W), A.epoch);
     }
   }
 }
@@ -182,7 +199,7 @@ DEV void acc_sum(Acc& q, const float (&x)[VE], float c) {
 }
 
 // One vector of each stream into the accumulators.
-template <int DT, int KIND, bool kB1, int DM, bool kClamp, bool kFirst>
+template <int DT, int KIND, bool kB1, int DM, bool kKL, bool kClamp, bool kFirst>
 DEV void stats_vec(const KArgs& A, float c, const u4& vt, const u4& va, const u4& vb, int kk, StatsAcc& q) {
   using TR = KindTraits<KIND>;
   constexpr int VE = Elem<DT>::VE;
@@ -215,7 +232,14 @@ DEV void stats_vec(const KArgs& A, float c, const u4& vt, const u4& va, const u4
     if (TR::kT) acc_sum<VE, false, kFirst>(q.T, xt, kL2E);
     if (TR::kArg) acc_vec<VE, kClamp, true>(q.F, xf, c, kk);
     else acc_sum<VE, kClamp, kFirst>(q.F, xf, c);
-    if (TR::kA) acc_sum<VE, false, kFirst>(q.A, xa, kL2E);
+    if (kKL && TR::kA) {
+      float dab[VE];
+      #pragma unroll
+      for (int e = 0; e < VE; ++e) dab[e] = __fsub_rn(xa[e], xb[e]);
+      acc_vec_w<VE, kFirst>(q.A, q.W, xa, dab, kL2E);
+    } else if (TR::kA) {
+      acc_sum<VE, false, kFirst>(q.A, xa, kL2E);
+    }
     if (TR::kAT) acc_sum<VE, false, kFirst>(q.AT, xa, c);
     if (TR::kT) pin_lazy(q.T);
     if (TR::kArg) pin(q.F);
@@ -238,13 +262,14 @@ DEV void stats_init(StatsAcc& q, float c) {
   acc_init(q.T, c); acc_init(q.A, kL2E); acc_init(q.B, kL2E); acc_init(q.F, c); acc_init(q.AT, c);
   q.neq = 0;
   q.bsame = true;
+  q.W = 0.0f;
 }
 
 // Generic path: one vector at a time, every vector repaired (row boundary,
 // array end), NaN-safe exponent for f.  Used for the chunk that holds a
 // ragged array end, to redo a chunk whose f sum came out NaN, and for every
 // chunk when the drafter rows are reached through a vocabulary map.
-template <int DT, int KIND, bool kB1, int DM>
+template <int DT, int KIND, bool kB1, int DM, bool kKL>
 DEV void stats_slow(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   using TR = KindTraits<KIND>;
   constexpr bool kDraft = TR::NS == 3;
@@ -270,15 +295,15 @@ DEV void stats_slow(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
       fix_vec<DT>(A, g, A.a, vi, va);
       fix_vec<DT>(A, g, A.b, vi, vb);
     }
-    stats_vec<DT, KIND, kB1, DM, true, true>(A, g.c, vt, va, vb, kk, q);
+    stats_vec<DT, KIND, kB1, DM, kKL, true, true>(A, g.c, vt, va, vb, kk, q);
   }
-  publish_stats<DT, KIND, DM>(A, g, m, rel0, q, sm);
+  publish_stats<DT, KIND, DM, kKL>(A, g, m, rel0, q, sm);
 }
 
 // Fast path; kMask for the first and last chunk of a row (elements outside
 // the row are masked, without branches).  Returns false, without publishing,
 // when the chunk must be redone on the generic path.
-template <int DT, int KIND, bool kB1, int DM, bool kMask>
+template <int DT, int KIND, bool kB1, int DM, bool kKL, bool kMask>
 DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   using TR = KindTraits<KIND>;
   constexpr int VE = Elem<DT>::VE;
@@ -296,17 +321,19 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
 
   StatsAcc q;
   stats_init(q, c);
-  // rolling prefetch: slot j % kWin holds vector j; it is refilled with
-  // vector j + kWin as soon as vector j is reduced
+  // rolling prefetch: slot j % W holds vector j; it is refilled with vector
+  // j + W as soon as vector j is reduced (one vector less in flight with the
+  // KL sum, which needs the registers)
   constexpr int kVecs = kNSub * kNV;
-  u4 buf[3][kWin];
+  constexpr int W = kKL ? kWin - 1 : kWin;
+  u4 buf[3][W];
   #pragma unroll
-  for (int j = 0; j < kWin; ++j)
+  for (int j = 0; j < W; ++j)
     #pragma unroll
     for (int s = 0; s < NS; ++s) buf[s][j] = buf_load_nt(r[s], off0 + (uint32_t)(vec_rel(j) * 16));
   #pragma unroll
   for (int j = 0; j < kVecs; ++j) {
-    const int sl = j % kWin;
+    const int sl = j % W;
     if (kMask) {
       // elements outside the row become -inf (selects, no branches)
       const int e_lo = lo_e - (rel0 + vec_rel(j)) * VE;
@@ -317,14 +344,14 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
     // masked elements have a = b = -inf, so f is NaN there: the boundary
     // chunks clamp the exponent of f
     if (j == 0)
-      stats_vec<DT, KIND, kB1, DM, kMask, true>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl],
-                                                buf[NS == 3 ? 2 : 0][sl], j, q);
+      stats_vec<DT, KIND, kB1, DM, kKL, kMask, true>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl],
+                                                     buf[NS == 3 ? 2 : 0][sl], j, q);
     else
-      stats_vec<DT, KIND, kB1, DM, kMask, false>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl],
-                                                 buf[NS == 3 ? 2 : 0][sl], j, q);
-    if (j + kWin < kVecs) {
+      stats_vec<DT, KIND, kB1, DM, kKL, kMask, false>(A, c, buf[0][sl], buf[NS == 3 ? 1 : 0][sl],
+                                                      buf[NS == 3 ? 2 : 0][sl], j, q);
+    if (j + W < kVecs) {
       #pragma unroll
-      for (int s = 0; s < NS; ++s) buf[s][sl] = buf_load_nt(r[s], off0 + (uint32_t)(vec_rel(j + kWin) * 16));
+      for (int s = 0; s < NS; ++s) buf[s][sl] = buf_load_nt(r[s], off0 + (uint32_t)(vec_rel(j + W) * 16));
     }
     // one vector's temporaries at a time
     __builtin_amdgcn_sched_barrier(0);
@@ -334,7 +361,7 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   // chunk redone on the NaN-safe path.  The test is workgroup-wide, so every
   // thread takes the same path.
   if (kDraft && !kMask && __syncthreads_or(q.F.s != q.F.s)) return false;
-  publish_stats<DT, KIND, DM>(A, g, m, rel0, q, sm);
+  publish_stats<DT, KIND, DM, kKL>(A, g, m, rel0, q, sm);
   return true;
 }
 
@@ -345,7 +372,7 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
 // verifier-to-drafter map) and the gathers hit the shorter verifier row.
 // The statistics are the same sums over the shared set in another order;
 // chunk m covers drafter vectors [m * kChunkVec, (m+1) * kChunkVec).
-template <int DT, int KIND, bool kB1, int DM>
+template <int DT, int KIND, bool kB1, int DM, bool kKL>
 DEV void stats_dorder(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
   constexpr int ES = 16 / VE;
@@ -388,17 +415,17 @@ DEV void stats_dorder(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
       Elem<DT>::put_one(a2, e, xa);
       Elem<DT>::put_one(b2, e, xb);
     }
-    stats_vec<DT, KIND, kB1, DM, true, true>(A, g.c, t2, a2, b2, kk, q);
+    stats_vec<DT, KIND, kB1, DM, kKL, true, true>(A, g.c, t2, a2, b2, kk, q);
   }
-  publish_stats<DT, KIND, DM>(A, g, m, rel0, q, sm);
+  publish_stats<DT, KIND, DM, kKL>(A, g, m, rel0, q, sm);
 }
 
-template <int DT, int KIND, bool kB1, int DM>
+template <int DT, int KIND, bool kB1, int DM, bool kKL = false>
 DEV void stats_item(const KArgs& A, int row, int m, Smem& sm) {
   constexpr int VE = Elem<DT>::VE;
   const RowGeo g = row_geo<DT>(A, row);
   if (!KindTraits<KIND>::kArg && KindTraits<KIND>::NS == 3 && A.vmap != nullptr && inv_ok(A)) {
-    stats_dorder<DT, KIND, kB1, DM>(A, g, m, sm);
+    stats_dorder<DT, KIND, kB1, DM, kKL>(A, g, m, sm);
     return;
   }
   const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
@@ -406,10 +433,10 @@ DEV void stats_item(const KArgs& A, int row, int m, Smem& sm) {
   if (A.vmap == nullptr && !has_tail(A, c0, c1)) {
     // a chunk whose vectors lie wholly inside the row needs no masking
     const bool interior = c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V;
-    done = interior ? stats_fast<DT, KIND, kB1, DM, false>(A, g, m, sm)
-                    : stats_fast<DT, KIND, kB1, DM, true>(A, g, m, sm);
+    done = interior ? stats_fast<DT, KIND, kB1, DM, kKL, false>(A, g, m, sm)
+                    : stats_fast<DT, KIND, kB1, DM, kKL, true>(A, g, m, sm);
   }
-  if (!done) stats_slow<DT, KIND, kB1, DM>(A, g, m, sm);
+  if (!done) stats_slow<DT, KIND, kB1, DM, kKL>(A, g, m, sm);
 }
 
 }  // namespace asym

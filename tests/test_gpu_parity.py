@@ -184,6 +184,27 @@ def test_variants_workload_1(gpu, gate, delta):
     _note(compare(x, g, gate_mode=gate, delta_mode=delta, label=f"variant workload 1 g={gate} d={delta}"))
 
 
+def test_kl_gate_single_pass_infinite_and_zero_divergence(gpu):
+    """KL gate (App. G) from the statistics items alone: a request whose
+    compressed view masks tokens the full view keeps has D = +inf and
+    gamma_eff = 0 (delta = a keeps the fused logits finite), requests with
+    identical views have D = 0 exactly, the rest match the oracle; greedy
+    and sampling requests, bf16 and fp32."""
+    for dtype in ("fp32", "bf16"):
+        x = synth.generate(B=8, K=3, V=4099, dtype=dtype, rho=("alternate", 0.0, 1.5),
+                           tau=("alternate", 0.0, 1.0), seed=2 if dtype == "fp32" else 3)
+        neg = np.float32(-np.inf) if dtype == "fp32" else np.uint16(0xFF80)
+        x.b[1, :, 100:110] = neg
+        x.b[5, :, 4000:4099] = neg
+        g = run_gpu(x, gate_mode=2, delta_mode=1)
+        _note(compare(x, g, gate_mode=2, delta_mode=1, label=f"KL +inf {dtype}"))
+        gate = g[3]
+        for r in (1, 5):
+            assert np.isinf(gate[r, :, 0]).all() and (gate[r, :, 1] == 0.0).all()
+        for r in (0, 2, 4, 6):
+            assert (gate[r, :, 0] == 0.0).all() and (gate[r, :, 1] == np.float32(0.5)).all()
+
+
 # ------------------------------------------------------ fused bonus row --
 def _reach_bonus(x, reqs):
     """Requests `reqs` get identical views and verifier on their draft rows
