@@ -184,6 +184,10 @@ def main():
     # a longer warm-up and more timed calls keep box-to-box noise out of the mean
     ap.add_argument("--warmup", type=int, default=1000)
     ap.add_argument("--workload", type=int, default=3)
+    ap.add_argument("--shape", type=str, default=None, metavar="B:K:V:TAU",
+                    help="another shape instead of a workload: bf16 logits from the workloads' "
+                         "Gaussian generator with divergence scale 1, e.g. 8:2:151936:0 (the "
+                         "paper's operating point: K = 2, greedy)")
     ap.add_argument("--gate", action="store_true", help="also return (D, gamma_eff) per row")
     ap.add_argument("--gate-mode", choices=["cda", "fixed", "kl", "lambda"], default="cda",
                     help="acceptance gate (cda: the paper's; the others are its baselines)")
@@ -223,11 +227,20 @@ def main():
         sys.exit(2)
 
     wl = synth.WORKLOADS[args.workload]
+    if args.shape:
+        sB, sK, sV, stau = args.shape.split(":")
+        kind = "greedy" if float(stau) <= 0 else f"tau{float(stau):g}"
+        wl = synth.Workload(f"B{sB}_K{sK}_V{sV}_bf16_{kind}", int(sB), int(sK), int(sV), "bf16",
+                            "gauss", 1.0, float(stau), 26104)
     if args.write_traffic:
         write_traffic(args.write_traffic[0], args.write_traffic[1], wl.name, COPY_BYTES)
         return
     t_gen = time.perf_counter()
-    x = synth.workload_inputs(args.workload, workers=args.gen_workers)
+    if args.shape:
+        x = synth.generate(B=wl.B, K=wl.K, V=wl.V, dtype=wl.dtype, prior=wl.prior, rho=wl.rho,
+                           tau=wl.tau, seed=wl.seed, workers=args.gen_workers)
+    else:
+        x = synth.workload_inputs(args.workload, workers=args.gen_workers)
     t_gen = time.perf_counter() - t_gen
     print(f"[bench] generated {wl.name} in {t_gen:.1f} s", file=sys.stderr, flush=True)
 

@@ -101,6 +101,7 @@ void fuse_verify_kernel(KArgs A) {
   __shared__ Smem sm;
 #ifdef ASYMSPEC_TRACE
   const uint64_t t_start = __builtin_amdgcn_s_memrealtime();
+  if (threadIdx.x == 0) sm.t_mark[0] = sm.t_mark[1] = t_start;
 #endif
   const Item it = sched_item(A.sc, A.K, A.S, (int)blockIdx.x);
   int type = it.type;
@@ -120,15 +121,14 @@ void fuse_verify_kernel(KArgs A) {
   }
 #ifdef ASYMSPEC_TRACE
   // timeline of the launch (a build option for measurement): per item its
-  // start and end on the 100 MHz clock, kind, request and the unit it ran on
-  if (threadIdx.x == 0 && A.trace != nullptr) {
+  // start and end on the 100 MHz clock, kind and request, and for statistics
+  // items when the first streaming load went out and when the stream ended
+  if (threadIdx.x == 0 && A.trace != nullptr && blockIdx.x < A.trace_items) {
     uint64_t* tr = A.trace + (size_t)blockIdx.x * 4;
-    const uint64_t hw = (uint64_t)__builtin_amdgcn_s_getreg(63492) |
-                        ((uint64_t)__builtin_amdgcn_s_getreg(6164) << 32);
     tr[0] = t_start;
     tr[1] = __builtin_amdgcn_s_memrealtime();
     tr[2] = (uint64_t)(uint32_t)it.type | ((uint64_t)(uint32_t)it.req << 8) | ((uint64_t)(uint32_t)it.sub << 40);
-    tr[3] = hw;
+    tr[3] = (sm.t_mark[0] - t_start) | ((sm.t_mark[1] - t_start) << 32);
   }
 #endif
 }
@@ -187,7 +187,8 @@ static bool make_layout(int B, int K, int V, int dtype, Layout& L, int Vd = 0) {
   // cross-family: inverse map [Vd] and its duplicate flag
   L.off_inv = off;  off = align_up(off + (Vd > 0 ? (size_t)Vd * 4 + 4 : 0), 256);
 #ifdef ASYMSPEC_TRACE
-  // 32 bytes per work item, for at most (K + 2) * S + 3 items per request
+  // 32 bytes per work item, for at most (K + 2) S + 3 items per request
+  // (statistics, pass 2, decide, pick, verdict)
   L.off_trace = off;  off = align_up(off + (size_t)B * ((size_t)(K + 2) * L.S + 3) * 32, 256);
 #endif
   L.total = off;
@@ -421,6 +422,7 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   A.inv = vmap != nullptr ? (const int32_t*)(ws + L.off_inv) : nullptr;
 #ifdef ASYMSPEC_TRACE
   A.trace = (uint64_t*)(ws + L.off_trace);
+  A.trace_items = (unsigned)((size_t)B * ((size_t)(K + 2) * L.S + 3));
 #endif
   A.lam = params->gate_mode == ASYMSPEC_GATE_LAMBDA ? params->lambda : 0.0f;
   A.ln_gamma = std::log((double)params->gamma);

@@ -140,6 +140,7 @@ struct KArgs {
   Sched sc;
 #ifdef ASYMSPEC_TRACE
   uint64_t* trace;    // per-item timeline (measurement builds only)
+  unsigned trace_items;   // items the timeline holds
 #endif
 };
 
@@ -828,8 +829,12 @@ struct Smem {
   float wseg[kWaves];
   int flags[8];
   double dd[8];
+  double djsd[kMaxK + 1];   // pick: D of the rows with a JSD task
   double scan[kWaves];
   int imin[kWaves];
+#ifdef ASYMSPEC_TRACE
+  uint64_t t_mark[2];   // measurement builds: first streaming load, end of the stream
+#endif
 };
 
 // Inclusive and exclusive prefix sums over the workgroup, in thread order.

@@ -821,7 +821,24 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
   const bool samp = sm.req[R_SAMP] != 0u;
   // requested now, used after the segment sums arrive
   const float uK = samp ? A.u[(size_t)req * (K + 1) + K] : 0.0f;
-  // wave 0: D of the rows that have it, final decisions, the emitting row
+  // D of each row with a JSD task, the rows dealt out over the waves (the
+  // k-th such row to wave k mod 4, its chunk partials over the lanes)
+  {
+    const uint32_t tk = lane <= K ? sm.rows[lane][D_TASK] : 0u;
+    unsigned long long jm = __ballot((tk & kTaskJsd) != 0u);
+    for (int k = 0; jm != 0; jm &= jm - 1, ++k) {
+      if (k % kWaves != w) continue;
+      const int i = __builtin_ctzll(jm);
+      double part = 0.0;
+      for (int c = lane; c < A.S; c += 64) part += wait_pair(p2_rec(A, req, i, c) + P2_J, A, ok);
+      part = wave_sum_d(part);
+      // the partials are in log2 units; JSD = half their sum, within [0, ln 2]
+      const double D = 0.5 * kLn2 * part;
+      if (lane == 0) sm.djsd[i] = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
+    }
+  }
+  __syncthreads();
+  // wave 0: final decisions, the emitting row
   float lpd = 0.0f;
   double Dl = 0.0;
   if (w == 0) {
@@ -838,16 +855,7 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
       arg = v[D_ARG];
       lpe = __uint_as_float(v[D_LPEMIT]);
     }
-    // D of each row that has a JSD task: lane c takes chunk c's partial
-    for (unsigned long long jm = __ballot((task & kTaskJsd) != 0u); jm != 0; jm &= jm - 1) {
-      const int i = __builtin_ctzll(jm);
-      double part = 0.0;
-      for (int c = lane; c < A.S; c += 64) part += wait_pair(p2_rec(A, req, i, c) + P2_J, A, ok);
-      part = wave_sum_d(part);
-      // the partials are in log2 units; JSD = half their sum, within [0, ln 2]
-      const double D = 0.5 * kLn2 * part;
-      if (lane == i) Dl = D < 0.0 ? 0.0 : (D > kLn2 ? kLn2 : D);
-    }
+    if (task & kTaskJsd) Dl = sm.djsd[lane];
     if ((A.gate_mode == ASYMSPEC_GATE_LAMBDA || A.gate_mode == ASYMSPEC_GATE_KL) && lane < K)
       Dl = u2d(sm.rows[lane][D_GD_LO], sm.rows[lane][D_GD_HI]);
     const bool decided = st & kStDecided;

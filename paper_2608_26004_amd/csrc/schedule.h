@@ -158,18 +158,19 @@ inline bool sched_build(int B, int K, int S, int items_in_flight, Sched& sc, int
 ASYM_HD inline Item sched_item(const Sched& sc, int K, int S, int idx) {
   Item it{kItemNone, 0, 0};
   if (idx < 0 || idx >= sc.total) return it;
-  // the run holding idx, found with constant indices only (in a kernel the
-  // schedule is part of a by-value argument, which a variable index would
-  // force into private memory)
+  // the run holding idx, found with constant indices and selects only: in a
+  // kernel the schedule is part of a by-value argument, which a variable
+  // index would force into private memory, and loads under a condition would
+  // each wait for the one before
   int i0 = sc.i0[0], blk = sc.blk[0], q0 = sc.q0[0], parts = sc.parts[0];
   #pragma unroll
   for (int k = 1; k < kMaxRuns; ++k) {
-    if (k < sc.n_runs && idx >= sc.i0[k]) {
-      i0 = sc.i0[k];
-      blk = sc.blk[k];
-      q0 = sc.q0[k];
-      parts = sc.parts[k];
-    }
+    const int ik = sc.i0[k], bk = sc.blk[k], qk = sc.q0[k], pk = sc.parts[k];
+    const bool take = k < sc.n_runs && idx >= ik;
+    i0 = take ? ik : i0;
+    blk = take ? bk : blk;
+    q0 = take ? qk : q0;
+    parts = take ? pk : parts;
   }
   const int off = idx - i0;
   const int qs = off / blk;

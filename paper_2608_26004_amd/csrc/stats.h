@@ -326,6 +326,9 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   // KL sum, which needs the registers)
   constexpr int kVecs = kNSub * kNV;
   constexpr int W = kKL ? kWin - 1 : kWin;
+#ifdef ASYMSPEC_TRACE
+  if (threadIdx.x == 0) sm.t_mark[0] = __builtin_amdgcn_s_memrealtime();
+#endif
   u4 buf[3][W];
   #pragma unroll
   for (int j = 0; j < W; ++j)
@@ -360,6 +363,9 @@ DEV bool stats_fast(const KArgs& A, const RowGeo& g, int m, Smem& sm) {
   // a token both views mask) makes some thread's f sum NaN; only then is the
   // chunk redone on the NaN-safe path.  The test is workgroup-wide, so every
   // thread takes the same path.
+#ifdef ASYMSPEC_TRACE
+  if (threadIdx.x == 0) sm.t_mark[1] = __builtin_amdgcn_s_memrealtime();
+#endif
   if (kDraft && !kMask && __syncthreads_or(q.F.s != q.F.s)) return false;
   publish_stats<DT, KIND, DM, kKL>(A, g, m, rel0, q, sm);
   return true;
