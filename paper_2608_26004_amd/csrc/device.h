@@ -35,11 +35,12 @@ constexpr int kTileVec = kThreads * kNV;        // vectors per sub-tile
 constexpr int kChunkVec = kTileVec * kNSub;     // vectors per vocabulary chunk
 constexpr int kSegVec = kChunkVec / kWaves;     // one wave's contiguous segment (pass 2)
 constexpr int kSegPerLane = kSegVec / 64;       // vectors per lane in a segment
+// Pass 2 sums the weights of a chunk per sub-block of 64 consecutive vectors
+// (one vector per lane of a wave): kSegPerLane sub-blocks per wave segment.
+constexpr int kSubPerChunk = kWaves * kSegPerLane;
 constexpr int kMaxK = 63;                       // K + 1 rows of a request fit one wave
-// pass 2 reads a lane's segment in groups of 4 vectors, and the pick splits a
-// segment evenly over the workgroup's threads
-static_assert(kSegPerLane % 4 == 0 && kSegVec % kThreads == 0,
-              "the tile size must give whole pass-2 groups and pick slices");
+// pass 2 reads a lane's segment in groups of 4 vectors
+static_assert(kSegPerLane % 4 == 0, "the tile size must give whole pass-2 groups");
 
 constexpr float kL2E = 1.44269504088896340736f;
 constexpr double kLn2 = 0.693147180559945309417232121458;
@@ -110,8 +111,9 @@ enum { kTaskJsd = 1, kTaskRes = 2, kTaskBonus = 4 };
 enum { kStDecided = 1, kStAccept = 2, kStDraft = 4, kStNeq = 8, kStSkip = 16 };
 
 // Pass-2 record of one (request, row, chunk): the chunk's JSD partial (fp64,
-// in log2 units) and the four wave-segment weight sums (fp64).
-enum { P2_J = 0, P2_SEG = 2, P2_USED = 10, kR2 = 12 };
+// in log2 units, two slots) and the weight sums of its sub-blocks (fp32, one
+// slot each, in vocabulary order).
+enum { P2_J = 0, P2_SEG = 2, P2_USED = P2_SEG + kSubPerChunk, kR2 = P2_USED };
 
 struct KArgs {
   const void* t; const void* a; const void* b;
@@ -421,6 +423,37 @@ DEV int wave_min_i(int x) {
   x = min(x, dppi<0x142, 0xA>(x));
   x = min(x, dppi<0x143, 0xC>(x));
   return __builtin_amdgcn_readlane(x, 63);
+}
+// DPP move of both halves of an fp64 value; lanes whose source is outside
+// the pattern (or in a row that ROWMASK leaves out) read 0.
+template <int CTRL, int ROWMASK = 0xF>
+DEV double dpp_d0(double x) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, x);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, ROWMASK, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, ROWMASK, 0xF, false);
+  return __builtin_bit_cast(double, (uint64_t)(uint32_t)lo | ((uint64_t)(uint32_t)hi << 32));
+}
+// An fp64 value of one lane, in every lane.
+DEV double readlane_d(double x, int lane) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, x);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), lane);
+  return __builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32));
+}
+// Inclusive and exclusive prefix sums of an fp64 value over the lanes of a
+// wave, in lane order: row shifts by 1, 2, 4 and 8 within each row of 16
+// lanes, then row 0's total into row 1 and row 2's into row 3 (row_bcast15),
+// then rows 0-1 into rows 2-3 (row_bcast31); the exclusive sum is the
+// inclusive one shifted by a lane (wave_shr1).  All 64 lanes must be active.
+DEV void wave_scan_d(double x, double& incl, double& excl) {
+  x += dpp_d0<0x111>(x);
+  x += dpp_d0<0x112>(x);
+  x += dpp_d0<0x114>(x);
+  x += dpp_d0<0x118>(x);
+  x += dpp_d0<0x142, 0xA>(x);
+  x += dpp_d0<0x143, 0xC>(x);
+  incl = x;
+  excl = dpp_d0<0x138>(x);
 }
 DEV double wave_sum_d(double x) {    // fp64 sum over lanes, in every lane
   #pragma unroll
@@ -826,7 +859,6 @@ struct Smem {
   int dneq[kThreads];
   // pass 2 / pick: partials, scans
   float wj[kWaves];
-  float wseg[kWaves];
   int flags[8];
   double dd[8];
   double djsd[kMaxK + 1];   // pick: D of the rows with a JSD task

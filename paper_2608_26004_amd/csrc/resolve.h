@@ -247,11 +247,13 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
       }
     }
     // this chunk's terms of the row sums, rescaled to the row's reference
+    // (the factor 2^(R_chunk - R_row) <= 1 in fp32: its error is far below
+    // that of the fp32 chunk sums it scales)
     if (have) {
       #pragma unroll
       for (int s = 0; s < kSlots; ++s)
-        sm.dt[tid][s] = (double)payf(r[R1_S + s]) * exp2((double)payf(r[R1_R + s]) - (double)Rr[s]);
-      sm.dw[tid] = (double)payf(r[R1_W]) * exp2((double)payf(r[R1_R + sA]) - (double)Rr[sA]);
+        sm.dt[tid][s] = (double)(payf(r[R1_S + s]) * __builtin_amdgcn_exp2f(payf(r[R1_R + s]) - Rr[s]));
+      sm.dw[tid] = (double)(payf(r[R1_W]) * __builtin_amdgcn_exp2f(payf(r[R1_R + sA]) - Rr[sA]));
       sm.darg[tid] = payf(r[R1_MARG]) == Marg ? (int)pay(r[R1_ARG]) : 0x7FFFFFFF;
       sm.dneq[tid] = (int)pay(r[R1_NEQ]);
     }
@@ -487,7 +489,7 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
 // a and a's vectors stand in for it (such a row has no divergence task).
 template <int DT, int kMode, int DM, bool kNb, bool kResOnly = false>
 DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj_in, bool dr_in, bool db_in,
-                    const ResidConst& rk, const JsdConst& jk, float& accj, float& seg) {
+                    const ResidConst& rk, const JsdConst& jk, float& accj, float (&seg)[kSegPerLane]) {
   constexpr int VE = Elem<DT>::VE;
   constexpr int kG = kMode == 2 ? 1 : 4;      // vectors per group
   // kResOnly: the row's only task is the residual (the usual emitting row),
@@ -551,7 +553,10 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj_in,
         for (int st = 1; st < VE; st <<= 1)
           #pragma unroll
           for (int e = 0; e + st < VE; e += 2 * st) vr[e] += vr[e + st];
-        seg += vr[0];
+        // vector k0 + k: selects on the run-time group start keep every
+        // sum in its own register
+        #pragma unroll
+        for (int q = 0; q < kSegPerLane; q += kG) seg[q + k] += (q == k0) ? vr[0] : 0.0f;
       }
     }
   }
@@ -560,7 +565,7 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj_in,
 template <int DT, int DM, bool kNb>
 DEV void pass2_sums_any(const KArgs& A, const RowGeo& g, long long rel0, long long c0, long long c1,
                         bool dj, bool dr, bool db, const ResidConst& rk, const JsdConst& jk, float& accj,
-                        float& seg) {
+                        float (&seg)[kSegPerLane]) {
   constexpr int VE = Elem<DT>::VE;
   if (A.vmap != nullptr || has_tail(A, c0, c1))
     pass2_sums<DT, 2, DM, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
@@ -592,7 +597,9 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
     const JsdConst jk = jsd_const(cst);
     const long long rel0 = (long long)m * kChunkVec + (long long)w * kSegVec + lane;
     const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
-    float accj = 0.0f, seg = 0.0f;
+    float accj = 0.0f, seg[kSegPerLane];
+    #pragma unroll
+    for (int k = 0; k < kSegPerLane; ++k) seg[k] = 0.0f;
     if (task != 0) {
       // a row with a == b bitwise has no divergence task and skips b
       if ((cst[D_STATUS] & kStNeq) != 0u || A.vmap != nullptr)
@@ -600,188 +607,203 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
       else
         pass2_sums_any<DT, DM, false>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
     }
+    // this wave's sub-block sums: lane k publishes sub-block k of the wave's
+    // segment; the JSD partial goes through LDS
+    float mine = 0.0f;
+    #pragma unroll
+    for (int k = 0; k < kSegPerLane; ++k) {
+      const float sk = wave_sum(seg[k]);
+      mine = lane == k ? sk : mine;
+    }
+    uint64_t* rec = p2_rec(A, req, i, m);
+    if (lane < kSegPerLane) st_tag(rec + P2_SEG + w * kSegPerLane + lane, __float_as_uint(mine), A.epoch);
     const float wj = wave_sum(accj);
-    const float wseg = wave_sum(seg);
-    if (lane == 0) { sm.wj[w] = wj; sm.wseg[w] = wseg; }
+    if (lane == 0) sm.wj[w] = wj;
     __syncthreads();
-    if (w == 0 && lane < P2_USED) {
+    if (w == 0 && lane < 2) {
       double v = 0.0;
-      if (lane < 2) {
-        #pragma unroll
-        for (int q = 0; q < kWaves; ++q) v += (double)sm.wj[q];
-      } else {
-        v = (double)sm.wseg[(lane - P2_SEG) >> 1];
-      }
-      st_tag(p2_rec(A, req, i, m) + lane, (lane & 1) ? dhi(v) : dlo(v), A.epoch);
+      #pragma unroll
+      for (int q = 0; q < kWaves; ++q) v += (double)sm.wj[q];
+      st_tag(rec + P2_J + lane, lane ? dhi(v) : dlo(v), A.epoch);
     }
     __syncthreads();
   }
 }
 
 // -------------------------------------------------------------------- pick
+// Sub-block sums a lane of the pick holds at once.
+constexpr int kPickRun = 8;
+
+// The tagged slots of sub-blocks [s0, s0 + n) (n <= kPickRun) of pass-2
+// record area rec, requested at once and polled until all are in (bounded;
+// ok cleared on a timeout); the other entries of v are zero.
+DEV void load_sub_run(const KArgs& A, const uint64_t* rec, int s0, int n, float (&v)[kPickRun], bool& ok) {
+  auto slot = [&](int sb) { return rec + (size_t)(sb / kSubPerChunk) * kR2 + P2_SEG + sb % kSubPerChunk; };
+  const uint64_t zero = (uint64_t)A.epoch << 32;
+  uint64_t r[kPickRun];
+  #pragma unroll
+  for (int j = 0; j < kPickRun; ++j) r[j] = j < n ? ld_tag(slot(s0 + j)) : zero;
+  Poll pl;
+  for (;;) {
+    bool in = true;
+    #pragma unroll
+    for (int j = 0; j < kPickRun; ++j) in = in && tag_ok(r[j], A.epoch);
+    if (in) break;
+    if (!pl.again(A)) {
+      ok = false;
+      break;
+    }
+    #pragma unroll
+    for (int j = 0; j < kPickRun; ++j) r[j] = j < n ? ld_tag(slot(s0 + j)) : zero;
+  }
+  #pragma unroll
+  for (int j = 0; j < kPickRun; ++j) v[j] = payf(r[j]);
+}
+
 // Inverse-CDF draw over row i of request req: the first element x whose
 // cumulative weight exceeds u * total, with the weights of pass 2 (residual
 // for drafts, bonus weights for the bonus row) recomputed by the same element
-// functions.  Row constants are in sm.rows[i].  Returns -1 when no element
-// carries weight; otherwise the element's index, and, when the scan itself
-// found it, sm.flags[2] = 1 and its logit (f for drafts, t for the bonus
-// row) in sm.dd[3].  Whole workgroup.
+// functions.  Pass 2's sums locate the 64-vector sub-block that holds it and
+// a scan of that sub-block the element; wave 0 does both, without barriers.
+// Row constants are in sm.rows[i].  Returns -1 when no element carries
+// weight; otherwise the element's index, and, when the scan itself found it,
+// sm.flags[2] = 1 and its logit (f for drafts, t for the bonus row) in
+// sm.dd[3].  Whole workgroup.
 template <int DT, int DM>
 DEV int cdf_pick(const KArgs& A, int req, int i, double u, bool bonus, Smem& sm, bool& ok) {
   constexpr int VE = Elem<DT>::VE;
-  constexpr int kPer = kSegVec / kThreads;   // vectors per thread in a segment
-  const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
-  const RowGeo g = row_span<DT>(A, req * (A.K + 1) + i);
-  const int nseg = A.S * kWaves;
-  if (tid == 0) sm.flags[2] = 0;
-  double target;
-  int sel = 0x7FFFFFFF, last_nz = -1;
-  if (nseg <= kThreads) {
-    // 1. one pass: thread sg holds segment sum sg; the scan gives the total
-    // and the segment holding the target
-    const int sg = tid;
-    double v = 0.0;
-    if (sg < nseg) {
-      const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
-      v = wait_pair(p, A, ok);
+  const int lane = lane_id(), w = wave_id();
+  if (w == 0) {
+    const RowGeo g = row_span<DT>(A, req * (A.K + 1) + i);
+    const int nsub = A.S * kSubPerChunk;
+    // lane l holds sub-blocks [l * per, l * per + per) in runs of kPickRun
+    const int per = (nsub + 63) / 64;
+    const int nrun = (per + kPickRun - 1) / kPickRun;
+    const int s0 = min(lane * per, nsub), s1 = min(s0 + per, nsub);
+    const uint64_t* rec = p2_rec(A, req, i, 0);
+    float v[kPickRun];
+    double lsum = 0.0;
+    for (int q = 0; q < nrun; ++q) {
+      const int a = min(s0 + q * kPickRun, s1);
+      load_sub_run(A, rec, a, min(kPickRun, s1 - a), v, ok);
+      #pragma unroll
+      for (int j = 0; j < kPickRun; ++j) lsum += (double)v[j];
     }
     double incl, excl;
-    block_scan(v, sm, incl, excl);
-    if (tid == kThreads - 1) sm.dd[4] = incl;
-    __syncthreads();
-    const double total = sm.dd[4];
-    if (!(total > 0.0)) return -1;
-    target = u * total;
-    const int cand = block_min_i((v > 0.0 && incl > target) ? sg : 0x7FFFFFFF, sm);
-    const int lnz = block_min_i(v > 0.0 ? -sg : 0x7FFFFFFF, sm);
-    if (lnz != 0x7FFFFFFF) last_nz = -lnz;
-    if (sg == cand) sm.dd[6] = excl;
-    if (sg == last_nz) sm.dd[7] = excl;
-    __syncthreads();
-    sel = cand;
-  } else {
-    // total weight (wave 0 waits for every segment sum)
-    if (w == 0) {
-      double tot = 0.0;
-      for (int sg = lane; sg < nseg; sg += 64) {
-        const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
-        tot += wait_pair(p, A, ok);
+    wave_scan_d(lsum, incl, excl);
+    const double total = readlane_d(incl, 63);
+    int pick = -1;
+    if (total > 0.0) {
+      const double target = u * total;
+      // the sub-block: the first with weight whose cumulative sum passes the
+      // target, else (rounding left the target at the total) the last one
+      // with weight; only the lane whose run holds it walks its run again
+      int cand = 0x7FFFFFFF, last = -1;
+      double cb = 0.0, lb = 0.0;
+      const bool mine = incl > target && excl <= target;
+      const bool any_w = lsum > 0.0;
+      if (mine || any_w) {
+        double run = excl;
+        for (int q = 0; q < nrun; ++q) {
+          const int a = min(s0 + q * kPickRun, s1);
+          if (nrun > 1) load_sub_run(A, rec, a, min(kPickRun, s1 - a), v, ok);
+          #pragma unroll
+          for (int j = 0; j < kPickRun; ++j) {
+            const double nx = run + (double)v[j];
+            if (v[j] > 0.0f && nx > target && cand == 0x7FFFFFFF) { cand = a + j; cb = run; }
+            if (v[j] > 0.0f) { last = a + j; lb = run; }
+            run = nx;
+          }
+        }
       }
-      tot = wave_sum_d(tot);
-      if (lane == 0) sm.dd[4] = tot;
-    }
-    __syncthreads();
-    const double total = sm.dd[4];
-    if (!(total > 0.0)) return -1;
-    target = u * total;
-    // 1. the segment holding the target: scan of segment sums in index order
-    double carry = 0.0;
-    for (int s0 = 0; s0 < nseg && sel == 0x7FFFFFFF; s0 += kThreads) {
-      const int sg = s0 + tid;
-      double v = 0.0;
-      if (sg < nseg) {
-        const uint64_t* p = p2_rec(A, req, i, sg / kWaves) + P2_SEG + 2 * (sg % kWaves);
-        v = payd(ld_tag(p), ld_tag(p + 1));
+      int sel = wave_min_i(cand);
+      double before;
+      if (sel == 0x7FFFFFFF) {
+        const int neg = wave_min_i(last >= 0 ? -last : 0x7FFFFFFF);
+        sel = neg == 0x7FFFFFFF ? -1 : -neg;
+        const unsigned long long src = __ballot(last == sel);
+        before = __shfl(lb, src ? (int)__builtin_ctzll(src) : 0, 64);
+      } else {
+        const unsigned long long src = __ballot(cand == sel);
+        before = __shfl(cb, (int)__builtin_ctzll(src), 64);
       }
-      double incl, excl;
-      block_scan(v, sm, incl, excl);
-      incl += carry;
-      excl += carry;
-      const int cand = block_min_i((v > 0.0 && incl > target) ? sg : 0x7FFFFFFF, sm);
-      const int lnz = block_min_i(v > 0.0 ? -sg : 0x7FFFFFFF, sm);
-      if (lnz != 0x7FFFFFFF) last_nz = -lnz;
-      __syncthreads();
-      if (sg == cand) sm.dd[6] = excl;
-      if (sg == last_nz) sm.dd[7] = excl;
-      if (tid == kThreads - 1) sm.dd[5] = incl;
-      __syncthreads();
-      carry = sm.dd[5];
-      sel = cand;
+      if (sel >= 0) {
+        // lane l scans vector l of the sub-block
+        const int ch = sel / kSubPerChunk, sub = sel % kSubPerChunk;
+        const long long sv0 = g.vbeg + (long long)ch * kChunkVec + (long long)sub * 64;
+        const long long vi = sv0 + lane;
+        const uint32_t* cst = sm.rows[i];
+        const ResidConst rk = resid_const(A, cst);
+        const __amdgpu_buffer_rsrc_t rt = row_rsrc(A, A.t, g);
+        const __amdgpu_buffer_rsrc_t ra = row_rsrc(A, bonus ? A.t : A.a, g);
+        // a row whose a and b are equal bitwise reads a for b (same weights)
+        const bool nb = !bonus && (cst[D_STATUS] & kStNeq) != 0u;
+        const __amdgpu_buffer_rsrc_t rb = row_rsrc(A, nb ? A.b : A.t, g);
+        const uint32_t off = (uint32_t)((vi - g.vbeg) * 16);
+        u4 vt = buf_load(rt, off);
+        u4 va = bonus ? vt : buf_load(ra, off);
+        u4 vb = nb ? buf_load(rb, off) : u4{0, 0, 0, 0};
+        if (A.vmap != nullptr) {
+          fix_vec<DT>(A, g, A.t, vi, vt);
+          map_vecs<DT>(A, g, vi, vt, va, vb, !bonus);
+          if (bonus) va = vt;
+        } else if (has_tail(A, sv0, sv0 + 64)) {
+          fix_vec<DT>(A, g, A.t, vi, vt);
+          if (!bonus) fix_vec<DT>(A, g, A.a, vi, va);
+          if (nb) fix_vec<DT>(A, g, A.b, vi, vb);
+        } else {
+          mask_vec<DT>(A, g, vi, vt);
+          mask_vec<DT>(A, g, vi, va);
+          mask_vec<DT>(A, g, vi, vb);
+        }
+        if (!nb) vb = va;
+        float x[VE];
+        double vsum = 0.0;
+        #pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const float xt = Elem<DT>::get(vt, e);
+          x[e] = bonus ? bonus_elem(xt, rk.c, rk.Rf)
+                       : resid_elem<DM>(xt, Elem<DT>::get(va, e), Elem<DT>::get(vb, e), rk);
+          vsum += (double)x[e];
+        }
+        double vin, vex;
+        wave_scan_d(vsum, vin, vex);
+        double run = before + vex;
+        int first_ok = 0x7FFFFFFF, last_pos = -1;
+        float fx = 0.0f;
+        #pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          run += (double)x[e];
+          const int idx = (int)(vi * VE + e - g.e0);
+          if (x[e] > 0.0f && run > target && first_ok == 0x7FFFFFFF) {
+            first_ok = idx;
+            const float xt = Elem<DT>::get(vt, e);
+            fx = bonus ? xt
+                       : fuse_masked(xt, Elem<DT>::get(va, e), Elem<DT>::get(vb, e), A.beta, A.delta_mode);
+          }
+          if (x[e] > 0.0f) last_pos = idx;
+        }
+        pick = wave_min_i(first_ok);
+        if (pick == 0x7FFFFFFF) {
+          // rounding left the target past the sub-block's own sum: its
+          // last element with weight
+          const int neg = wave_min_i(last_pos >= 0 ? -last_pos : 0x7FFFFFFF);
+          pick = neg == 0x7FFFFFFF ? -1 : -neg;
+          if (lane == 0) sm.flags[2] = 0;
+        } else {
+          if (first_ok == pick) sm.dd[3] = (double)fx;
+          if (lane == 0) sm.flags[2] = 1;
+        }
+      } else if (lane == 0) {
+        sm.flags[2] = 0;
+      }
+    } else if (lane == 0) {
+      sm.flags[2] = 0;
     }
-  }
-  if (sel == 0x7FFFFFFF) {
-    if (last_nz < 0) return -1;
-    sel = last_nz;
-    if (tid == 0) sm.dd[6] = sm.dd[7];
+    if (lane == 0) sm.flags[3] = pick;
   }
   __syncthreads();
-  const double before = sm.dd[6];
-  // 2. scan inside the segment: thread tid takes vectors kPer * tid ...
-  const int ch = sel / kWaves, ww = sel % kWaves;
-  const uint32_t* cst = sm.rows[i];
-  const ResidConst rk = resid_const(A, cst);
-  const __amdgpu_buffer_rsrc_t rt = row_rsrc(A, A.t, g);
-  const __amdgpu_buffer_rsrc_t ra = row_rsrc(A, bonus ? A.t : A.a, g);
-  // a row whose a and b are equal bitwise reads a for b (same weights)
-  const bool nb = !bonus && (cst[D_STATUS] & kStNeq) != 0u;
-  const __amdgpu_buffer_rsrc_t rb = row_rsrc(A, nb ? A.b : A.t, g);
-  const long long rel = (long long)ch * kChunkVec + (long long)ww * kSegVec + (long long)kPer * tid;
-  const long long sv0 = g.vbeg + (long long)ch * kChunkVec + (long long)ww * kSegVec;
-  const bool tail = has_tail(A, sv0, sv0 + kSegVec);
-  u4 vt[kPer], va[kPer], vb[kPer];
-  double tsum = 0.0;
-  int last_pos = -1;
-  #pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const uint32_t off = (uint32_t)((rel + k) * 16);
-    const long long vi = g.vbeg + rel + k;
-    vt[k] = buf_load(rt, off);
-    va[k] = bonus ? vt[k] : buf_load(ra, off);
-    vb[k] = nb ? buf_load(rb, off) : u4{0, 0, 0, 0};
-    if (A.vmap != nullptr) {
-      fix_vec<DT>(A, g, A.t, vi, vt[k]);
-      map_vecs<DT>(A, g, vi, vt[k], va[k], vb[k], !bonus);
-      if (bonus) va[k] = vt[k];
-    } else if (tail) {
-      fix_vec<DT>(A, g, A.t, vi, vt[k]);
-      if (!bonus) fix_vec<DT>(A, g, A.a, vi, va[k]);
-      if (nb) fix_vec<DT>(A, g, A.b, vi, vb[k]);
-    } else {
-      mask_vec<DT>(A, g, vi, vt[k]);
-      mask_vec<DT>(A, g, vi, va[k]);
-      mask_vec<DT>(A, g, vi, vb[k]);
-    }
-    if (!nb) vb[k] = va[k];
-    #pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      const float xt = Elem<DT>::get(vt[k], e);
-      const float x = bonus ? bonus_elem(xt, rk.c, rk.Rf)
-                            : resid_elem<DM>(xt, Elem<DT>::get(va[k], e), Elem<DT>::get(vb[k], e), rk);
-      tsum += (double)x;
-      if (x > 0.0f) last_pos = (int)((vi * VE + e) - g.e0);
-    }
-  }
-  double incl, excl;
-  block_scan(tsum, sm, incl, excl);
-  double run = before + excl;
-  int first_ok = 0x7FFFFFFF;
-  float fx = 0.0f;
-  #pragma unroll
-  for (int k = 0; k < kPer; ++k)
-    #pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      const float xt = Elem<DT>::get(vt[k], e);
-      const float xa = Elem<DT>::get(va[k], e), xb = Elem<DT>::get(vb[k], e);
-      const float x = bonus ? bonus_elem(xt, rk.c, rk.Rf) : resid_elem<DM>(xt, xa, xb, rk);
-      run += (double)x;
-      if (x > 0.0f && run > target && first_ok == 0x7FFFFFFF) {
-        first_ok = (int)((g.vbeg + rel + k) * VE + e - g.e0);
-        fx = bonus ? xt : fuse_masked(xt, xa, xb, A.beta, A.delta_mode);
-      }
-    }
-  int pick = block_min_i(first_ok, sm);
-  if (pick == 0x7FFFFFFF) {
-    // rounding left the target past the segment's own sum: its last nonzero
-    const int neg = block_min_i(last_pos >= 0 ? -last_pos : 0x7FFFFFFF, sm);
-    pick = (neg == 0x7FFFFFFF) ? -1 : -neg;
-  } else {
-    if (first_ok == pick) {
-      sm.flags[2] = 1;
-      sm.dd[3] = (double)fx;
-    }
-    __syncthreads();
-  }
-  return pick;
+  return sm.flags[3];
 }
 
 // Argmax of the fused logits of a row by a full scan (whole workgroup); only
