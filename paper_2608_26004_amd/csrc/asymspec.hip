@@ -187,9 +187,9 @@ static bool make_layout(int B, int K, int V, int dtype, Layout& L, int Vd = 0) {
   // cross-family: inverse map [Vd] and its duplicate flag
   L.off_inv = off;  off = align_up(off + (Vd > 0 ? (size_t)Vd * 4 + 4 : 0), 256);
 #ifdef ASYMSPEC_TRACE
-  // 32 bytes per work item, for at most (K + 2) S + 3 items per request
-  // (statistics, pass 2, decide, pick, verdict)
-  L.off_trace = off;  off = align_up(off + (size_t)B * ((size_t)(K + 2) * L.S + 3) * 32, 256);
+  // 32 bytes per work item, for at most (K + 1 + kMaxP2) S + 3 items per
+  // request (statistics, pass 2, decide, pick, verdict)
+  L.off_trace = off;  off = align_up(off + (size_t)B * ((size_t)(K + 1 + kMaxP2) * L.S + 3) * 32, 256);
 #endif
   L.total = off;
   return true;
@@ -422,7 +422,7 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   A.inv = vmap != nullptr ? (const int32_t*)(ws + L.off_inv) : nullptr;
 #ifdef ASYMSPEC_TRACE
   A.trace = (uint64_t*)(ws + L.off_trace);
-  A.trace_items = (unsigned)((size_t)B * ((size_t)(K + 2) * L.S + 3));
+  A.trace_items = (unsigned)((size_t)B * ((size_t)(K + 1 + kMaxP2) * L.S + 3));
 #endif
   A.lam = params->gate_mode == ASYMSPEC_GATE_LAMBDA ? params->lambda : 0.0f;
   A.ln_gamma = std::log((double)params->gamma);
@@ -431,7 +431,12 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   // lags scale with the number of workgroups the chip holds at once
   const int ee_rows = ee ? (params->early_rows > 0 ? params->early_rows : 2) : 0;
   const int in_flight = vmap != nullptr ? di->max_blocks_xv[dtype] : di->max_blocks[dtype];
-  if (!sched_build(B, K, L.S, in_flight, A.sc, ee_rows)) return ASYMSPEC_E_ARG;
+  // pass 2 in 4 or 2 items per chunk while that many still fit on the chip
+  // at once: a small batch leaves most of it idle, and pass 2's divergence
+  // terms are arithmetic-bound within one workgroup
+  const long long p2_items = (long long)B * L.S;
+  A.P2 = p2_items * 4 <= in_flight ? 4 : (p2_items * 2 <= in_flight ? 2 : 1);
+  if (!sched_build(B, K, L.S, in_flight, A.sc, ee_rows, A.P2)) return ASYMSPEC_E_ARG;
   const int grid = A.sc.total;
 
   const unsigned long long nblk = (unsigned long long)B * (K + 1) * L.S;

@@ -110,10 +110,12 @@ enum { kTaskJsd = 1, kTaskRes = 2, kTaskBonus = 4 };
 // kStSkip: a row after a sure rejection that early exit did not read.
 enum { kStDecided = 1, kStAccept = 2, kStDraft = 4, kStNeq = 8, kStSkip = 16 };
 
-// Pass-2 record of one (request, row, chunk): the chunk's JSD partial (fp64,
-// in log2 units, two slots) and the weight sums of its sub-blocks (fp32, one
-// slot each, in vocabulary order).
-enum { P2_J = 0, P2_SEG = 2, P2_USED = P2_SEG + kSubPerChunk, kR2 = P2_USED };
+// Pass 2 splits each chunk into P2 in {1, 2, 4} contiguous parts, one item
+// each.  Pass-2 record of one (request, row, chunk): the JSD partial of each
+// part (fp32, in log2 units) and the weight sums of the chunk's sub-blocks
+// (fp32, in vocabulary order), one slot each.
+constexpr int kMaxP2 = 4;
+enum { P2_J = 0, P2_SEG = kMaxP2, P2_USED = P2_SEG + kSubPerChunk, kR2 = P2_USED };
 
 struct KArgs {
   const void* t; const void* a; const void* b;
@@ -123,6 +125,7 @@ struct KArgs {
   uint32_t* err;
   unsigned long long stream_bytes;   // bytes of each logit array
   int B, K, V, S;
+  int P2;             // pass-2 items per chunk
   float beta, gamma; int gate_mode; int want_gate;
   int delta_mode;     // source of delta in f = t + beta * delta
   int fuse_bonus;     // the bonus row emits from f rather than t
@@ -277,6 +280,21 @@ DEV double wait_pair(const uint64_t* p, const KArgs& A, bool& ok) {
     hi = ld_tag(p + 1);
   }
   return payd(lo, hi);
+}
+
+// The fp32 value in the tagged slot at p, polled until it carries the
+// epoch; ok is cleared when the wait timed out.
+DEV float wait_f32(const uint64_t* p, const KArgs& A, bool& ok) {
+  uint64_t v = ld_tag(p);
+  Poll pl;
+  while (!tag_ok(v, A.epoch)) {
+    if (!pl.again(A)) {
+      ok = false;
+      break;
+    }
+    v = ld_tag(p);
+  }
+  return payf(v);
 }
 
 // Poll a tagged slot until it carries the launch epoch (bounded).

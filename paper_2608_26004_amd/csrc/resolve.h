@@ -482,16 +482,18 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
 }
 
 // ------------------------------------------------------------------ pass 2
-// Pass-2 sums of one thread over its kSegPerLane vectors of a chunk.
-// kMode 0: interior chunk (no masking); 1: masked, branch-free; 2: generic
-// (one vector at a time, array-end repair).
+// Pass-2 sums of one thread over its nk vectors (64 apart) of a chunk part;
+// the weight sum of vector k goes to seg[k].
+// kMode 0: interior part (no masking); 1: masked, branch-free; 2: generic
+// (one vector at a time, array-end repair).  kGF vectors per group (4, or 2
+// when a lane has only 2).
 // kNb: a and b differ somewhere in the row; otherwise b is a bitwise copy of
 // a and a's vectors stand in for it (such a row has no divergence task).
-template <int DT, int kMode, int DM, bool kNb, bool kResOnly = false>
-DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj_in, bool dr_in, bool db_in,
+template <int DT, int kMode, int DM, bool kNb, bool kResOnly = false, int kGF = 4>
+DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, int nk, bool dj_in, bool dr_in, bool db_in,
                     const ResidConst& rk, const JsdConst& jk, float& accj, float (&seg)[kSegPerLane]) {
   constexpr int VE = Elem<DT>::VE;
-  constexpr int kG = kMode == 2 ? 1 : 4;      // vectors per group
+  constexpr int kG = kMode == 2 ? 1 : kGF;    // vectors per group
   // kResOnly: the row's only task is the residual (the usual emitting row),
   // an instance without the other tasks' code
   const bool dj = kResOnly ? false : dj_in, dr = kResOnly ? true : dr_in, db = kResOnly ? false : db_in;
@@ -500,7 +502,7 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj_in,
   const __amdgpu_buffer_rsrc_t ra = row_rsrc(A, nab ? A.a : A.t, g);
   const __amdgpu_buffer_rsrc_t rb = row_rsrc(A, nab ? A.b : A.t, g);
   #pragma unroll 1
-  for (int k0 = 0; k0 < kSegPerLane; k0 += kG) {
+  for (int k0 = 0; k0 < nk; k0 += kG) {
     u4 vt[kG], va[kG], vb[kG];
     #pragma unroll
     for (int k = 0; k < kG; ++k) {
@@ -562,26 +564,31 @@ DEV void pass2_sums(const KArgs& A, const RowGeo& g, long long rel0, bool dj_in,
   }
 }
 
-template <int DT, int DM, bool kNb>
-DEV void pass2_sums_any(const KArgs& A, const RowGeo& g, long long rel0, long long c0, long long c1,
+template <int DT, int DM, bool kNb, int kGF>
+DEV void pass2_sums_any(const KArgs& A, const RowGeo& g, long long rel0, int nk, long long c0, long long c1,
                         bool dj, bool dr, bool db, const ResidConst& rk, const JsdConst& jk, float& accj,
                         float (&seg)[kSegPerLane]) {
   constexpr int VE = Elem<DT>::VE;
   if (A.vmap != nullptr || has_tail(A, c0, c1))
-    pass2_sums<DT, 2, DM, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 2, DM, kNb>(A, g, rel0, nk, dj, dr, db, rk, jk, accj, seg);
   else if (dr && !dj && !db && c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
-    pass2_sums<DT, 0, DM, kNb, true>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 0, DM, kNb, true, kGF>(A, g, rel0, nk, dj, dr, db, rk, jk, accj, seg);
   else if (dr && !dj && !db)
-    pass2_sums<DT, 1, DM, kNb, true>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 1, DM, kNb, true, kGF>(A, g, rel0, nk, dj, dr, db, rk, jk, accj, seg);
   else if (c0 * VE >= g.e0 && c1 * VE <= g.e0 + A.V)
-    pass2_sums<DT, 0, DM, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 0, DM, kNb, false, kGF>(A, g, rel0, nk, dj, dr, db, rk, jk, accj, seg);
   else
-    pass2_sums<DT, 1, DM, kNb>(A, g, rel0, dj, dr, db, rk, jk, accj, seg);
+    pass2_sums<DT, 1, DM, kNb, false, kGF>(A, g, rel0, nk, dj, dr, db, rk, jk, accj, seg);
 }
 
 template <int DT, int DM>
-DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
+DEV void pass2_item(const KArgs& A, int req, int sub, Smem& sm) {
   const int lane = lane_id(), w = wave_id();
+  // part `part` of chunk m: kChunkVec / P2 vectors, wave w's nk * 64 of
+  // them from pbase + w * 64 * nk, lane l every 64th from there
+  const int m = sub / A.P2, part = sub - m * A.P2;
+  const int nk = kSegPerLane / A.P2;
+  const long long pbase = (long long)m * kChunkVec + (long long)part * (kChunkVec / A.P2);
   if (load_decision(A, req, sm) != kStatePending) return;
   unsigned long long tmask = (unsigned long long)sm.req[R_TASK_LO] | ((unsigned long long)sm.req[R_TASK_HI] << 32);
   // only rows 0..K of the request (K + 1 <= 64)
@@ -595,36 +602,43 @@ DEV void pass2_item(const KArgs& A, int req, int m, Smem& sm) {
     const bool dj = task & kTaskJsd, dr = task & kTaskRes, db = task & kTaskBonus;
     const ResidConst rk = resid_const(A, cst);
     const JsdConst jk = jsd_const(cst);
-    const long long rel0 = (long long)m * kChunkVec + (long long)w * kSegVec + lane;
-    const long long c0 = g.vbeg + (long long)m * kChunkVec, c1 = c0 + kChunkVec;
+    const long long rel0 = pbase + (long long)w * 64 * nk + lane;
+    const long long c0 = g.vbeg + pbase, c1 = c0 + kChunkVec / A.P2;
     float accj = 0.0f, seg[kSegPerLane];
     #pragma unroll
     for (int k = 0; k < kSegPerLane; ++k) seg[k] = 0.0f;
     if (task != 0) {
       // a row with a == b bitwise has no divergence task and skips b
-      if ((cst[D_STATUS] & kStNeq) != 0u || A.vmap != nullptr)
-        pass2_sums_any<DT, DM, true>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
-      else
-        pass2_sums_any<DT, DM, false>(A, g, rel0, c0, c1, dj, dr, db, rk, jk, accj, seg);
+      const bool nbr = (cst[D_STATUS] & kStNeq) != 0u || A.vmap != nullptr;
+      if (nk >= 4) {
+        if (nbr) pass2_sums_any<DT, DM, true, 4>(A, g, rel0, nk, c0, c1, dj, dr, db, rk, jk, accj, seg);
+        else pass2_sums_any<DT, DM, false, 4>(A, g, rel0, nk, c0, c1, dj, dr, db, rk, jk, accj, seg);
+      } else {
+        if (nbr) pass2_sums_any<DT, DM, true, 2>(A, g, rel0, nk, c0, c1, dj, dr, db, rk, jk, accj, seg);
+        else pass2_sums_any<DT, DM, false, 2>(A, g, rel0, nk, c0, c1, dj, dr, db, rk, jk, accj, seg);
+      }
     }
-    // this wave's sub-block sums: lane k publishes sub-block k of the wave's
-    // segment; the JSD partial goes through LDS
+    // this wave's sub-block sums: lane k < nk publishes the wave's k-th
+    // sub-block; the part's JSD partial goes through LDS
     float mine = 0.0f;
     #pragma unroll
     for (int k = 0; k < kSegPerLane; ++k) {
-      const float sk = wave_sum(seg[k]);
-      mine = lane == k ? sk : mine;
+      if (k < nk) {
+        const float sk = wave_sum(seg[k]);
+        mine = lane == k ? sk : mine;
+      }
     }
     uint64_t* rec = p2_rec(A, req, i, m);
-    if (lane < kSegPerLane) st_tag(rec + P2_SEG + w * kSegPerLane + lane, __float_as_uint(mine), A.epoch);
+    if (lane < nk)
+      st_tag(rec + P2_SEG + part * (kSubPerChunk / A.P2) + w * nk + lane, __float_as_uint(mine), A.epoch);
     const float wj = wave_sum(accj);
     if (lane == 0) sm.wj[w] = wj;
     __syncthreads();
-    if (w == 0 && lane < 2) {
-      double v = 0.0;
+    if (threadIdx.x == 0) {
+      float v = 0.0f;
       #pragma unroll
-      for (int q = 0; q < kWaves; ++q) v += (double)sm.wj[q];
-      st_tag(rec + P2_J + lane, lane ? dhi(v) : dlo(v), A.epoch);
+      for (int q = 0; q < kWaves; ++q) v += sm.wj[q];
+      st_tag(rec + P2_J + part, __float_as_uint(v), A.epoch);
     }
     __syncthreads();
   }
@@ -852,7 +866,8 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
       if (k % kWaves != w) continue;
       const int i = __builtin_ctzll(jm);
       double part = 0.0;
-      for (int c = lane; c < A.S; c += 64) part += wait_pair(p2_rec(A, req, i, c) + P2_J, A, ok);
+      for (int c = lane; c < A.S * A.P2; c += 64)
+        part += (double)wait_f32(p2_rec(A, req, i, c / A.P2) + P2_J + c % A.P2, A, ok);
       part = wave_sum_d(part);
       // the partials are in log2 units; JSD = half their sum, within [0, ln 2]
       const double D = 0.5 * kLn2 * part;

@@ -13,7 +13,8 @@
 //                                             ((K+1-G) * S items; early exit
 //                                             only),
 //   * the decide item of request q - L1       (1 item),
-//   * the pass-2 items of request q - L2      (S items, one per chunk),
+//   * the pass-2 items of request q - L2      (S2 = P2 * S items: P2 parts
+//                                             of each chunk),
 //   * the pick item of request q - L3         (1 item),
 // each present only when its request index lies in [0, B).  Without early
 // exit G = K + 1 and Lv = Ls = 0.  An item only ever waits for items earlier
@@ -48,6 +49,7 @@ struct Sched {
   int n_runs;
   int total;              // number of items
   int G;                  // rows in the first group (K + 1 without early exit)
+  int S2;                 // pass-2 items per request (P2 parts of each of S chunks)
   int ee;                 // early exit: verdict and second-group items present
   int Lv, Ls, L1, L2, L3;
   int q0[kMaxRuns];       // first step of the run
@@ -59,7 +61,7 @@ struct Sched {
 struct Item {
   int type;   // ItemType
   int req;    // request index
-  int sub;    // statistics: row-in-request * S + chunk; pass 2: chunk; else 0
+  int sub;    // statistics: row-in-request * S + chunk; pass 2: chunk * P2 + part; else 0
 };
 
 ASYM_HD inline bool sched_in(int q, int lag, int B) { return q - lag >= 0 && q - lag < B; }
@@ -78,7 +80,7 @@ ASYM_HD inline int sched_parts(const Sched& sc, int q, int B) {
 ASYM_HD inline int sched_block(const Sched& sc, int parts, int K, int S) {
   return ((parts & kPartStats) ? sc.G * S : 0) + ((parts & kPartVerdict) ? 1 : 0) +
          ((parts & kPartStats2) ? (K + 1 - sc.G) * S : 0) + ((parts & kPartDecide) ? 1 : 0) +
-         ((parts & kPartPass2) ? S : 0) + ((parts & kPartPick) ? 1 : 0);
+         ((parts & kPartPass2) ? sc.S2 : 0) + ((parts & kPartPick) ? 1 : 0);
 }
 
 #ifndef ASYMSPEC_LAG_PCT
@@ -104,12 +106,15 @@ ASYM_HD inline int sched_block(const Sched& sc, int parts, int K, int S) {
 // and the pass-2 and pick lags add lag2_pct and lag3_pct percent to the lag
 // before them.  With early exit (ee_rows in [1, K]) the first ee_rows rows of
 // a request are read first, its verdict follows LAGV_PCT later and the other
-// rows LAGS_PCT after that; the decide lag then counts from those.  Returns
-// false when the schedule would not fit in 31-bit indices.
-inline bool sched_build(int B, int K, int S, int items_in_flight, Sched& sc, int ee_rows = 0,
+// rows LAGS_PCT after that; the decide lag then counts from those.  Pass 2
+// takes p2 items per chunk.  Returns false when the schedule would not fit in
+// 31-bit indices.
+inline bool sched_build(int B, int K, int S, int items_in_flight, Sched& sc, int ee_rows = 0, int p2 = 1,
                         int lag_pct = ASYMSPEC_LAG_PCT, int lag2_pct = ASYMSPEC_LAG2_PCT,
                         int lag3_pct = ASYMSPEC_LAG3_PCT) {
-  if (B < 1 || K < 0 || S < 1 || items_in_flight < 1 || ee_rows < 0) return false;
+  if (B < 1 || K < 0 || S < 1 || items_in_flight < 1 || ee_rows < 0 || p2 < 1) return false;
+  if ((long long)S * p2 > (1LL << 24)) return false;
+  sc.S2 = S * p2;
   // steps hold at least the (K+1) * S statistics items of their request
   const long long per_step = (long long)(K + 1) * S;
   auto window = [&](int pct) {
@@ -194,8 +199,8 @@ ASYM_HD inline Item sched_item(const Sched& sc, int K, int S, int idx) {
     o -= 1;
   }
   if (parts & kPartPass2) {
-    if (o < S) { it.type = kItemPass2; it.req = q - sc.L2; it.sub = o; return it; }
-    o -= S;
+    if (o < sc.S2) { it.type = kItemPass2; it.req = q - sc.L2; it.sub = o; return it; }
+    o -= sc.S2;
   }
   it.type = kItemPick;
   it.req = q - sc.L3;

@@ -23,8 +23,9 @@ using namespace asym;
 int main(int argc, char** argv) {
   const int B = atoi(argv[1]), K = atoi(argv[2]), S = atoi(argv[3]), G = atoi(argv[4]);
   const int ee = argc > 5 ? atoi(argv[5]) : 0;
+  const int p2 = argc > 6 ? atoi(argv[6]) : 1;
   Sched sc;
-  if (!sched_build(B, K, S, G, sc, ee)) { printf("FAIL build\n"); return 1; }
+  if (!sched_build(B, K, S, G, sc, ee, p2)) { printf("FAIL build\n"); return 1; }
   printf("T %d %d %d %d\n", sc.total, sc.L1, sc.L2, sc.L3);
   for (int i = 0; i < sc.total; ++i) {
     const Item it = sched_item(sc, K, S, i);
@@ -48,8 +49,8 @@ def driver():
     return exe
 
 
-def enumerate_items(exe, B, K, S, G, ee=0):
-    out = subprocess.run([exe, str(B), str(K), str(S), str(G), str(ee)], check=True,
+def enumerate_items(exe, B, K, S, G, ee=0, p2=1):
+    out = subprocess.run([exe, str(B), str(K), str(S), str(G), str(ee), str(p2)], check=True,
                          capture_output=True, text=True).stdout.split("\n")
     head = out[0].split()
     assert head[0] == "T"
@@ -64,9 +65,12 @@ SHAPES = [(1, 0, 1, 1), (1, 4, 4, 512), (8, 5, 8, 1024), (32, 8, 10, 1024),
           (7, 2, 30, 2048), (128, 6, 19, 256)]
 
 
+@pytest.mark.parametrize("p2", [1, 2, 4])
 @pytest.mark.parametrize("B,K,S,G", SHAPES)
-def test_every_item_once_and_dependencies_first(driver, B, K, S, G):
-    items = enumerate_items(driver, B, K, S, G)
+def test_every_item_once_and_dependencies_first(driver, B, K, S, G, p2):
+    """Pass 2 runs as p2 items per chunk (sub = chunk * p2 + part)."""
+    items = enumerate_items(driver, B, K, S, G, 0, p2)
+    S2 = S * p2
     stats, decide, pass2, pick = {}, {}, {}, {}
     for idx, (ty, req, sub) in enumerate(items):
         assert 0 <= req < B
@@ -78,7 +82,7 @@ def test_every_item_once_and_dependencies_first(driver, B, K, S, G):
             assert req not in decide
             decide[req] = idx
         elif ty == 2:
-            assert 0 <= sub < S and (req, sub) not in pass2
+            assert 0 <= sub < S2 and (req, sub) not in pass2
             pass2[(req, sub)] = idx
         elif ty == 3:
             assert req not in pick
@@ -86,13 +90,13 @@ def test_every_item_once_and_dependencies_first(driver, B, K, S, G):
         else:
             pytest.fail(f"unknown item type {ty}")
     assert len(stats) == B * (K + 1) * S
-    assert len(decide) == len(pick) == B and len(pass2) == B * S
+    assert len(decide) == len(pick) == B and len(pass2) == B * S2
     for r in range(B):
         last_stat = max(stats[(r, s)] for s in range((K + 1) * S))
         assert decide[r] > last_stat
-        for m in range(S):
+        for m in range(S2):
             assert pass2[(r, m)] > decide[r]
-        assert pick[r] > max(pass2[(r, m)] for m in range(S))
+        assert pick[r] > max(pass2[(r, m)] for m in range(S2))
 
 
 def test_lags_cover_the_items_in_flight(driver):
@@ -143,12 +147,14 @@ EE_SHAPES = [(1, 1, 1, 1, 1), (128, 6, 10, 1024, 2), (128, 6, 10, 1024, 1), (32,
              (512, 8, 16, 1024, 2), (7, 2, 30, 2048, 2), (200, 3, 1, 3, 1), (5, 63, 2, 7, 60)]
 
 
+@pytest.mark.parametrize("p2", [1, 4])
 @pytest.mark.parametrize("B,K,S,G,ee", EE_SHAPES)
-def test_early_exit_order(driver, B, K, S, G, ee):
+def test_early_exit_order(driver, B, K, S, G, ee, p2):
     """With early exit the first ee rows of a request are read, then its
     verdict, then the other rows (skipped after a sure rejection); every
     item appears once and each comes after all items it waits for."""
-    items = enumerate_items(driver, B, K, S, G, ee)
+    items = enumerate_items(driver, B, K, S, G, ee, p2)
+    S2 = S * p2
     n1 = ee * S
     stats, verdict, decide, pass2, pick = {}, {}, {}, {}, {}
     for idx, (ty, req, sub) in enumerate(items):
@@ -173,8 +179,9 @@ def test_early_exit_order(driver, B, K, S, G, ee):
         assert verdict[r] > max(stats[(r, s)] for s in range(n1))
         assert min(stats[(r, s)] for s in range(n1, (K + 1) * S)) > verdict[r]
         assert decide[r] > max(stats[(r, s)] for s in range((K + 1) * S))
-        assert min(pass2[(r, m)] for m in range(S)) > decide[r]
-        assert pick[r] > max(pass2[(r, m)] for m in range(S))
+        assert len([m for m in range(S2) if (r, m) in pass2]) == S2
+        assert min(pass2[(r, m)] for m in range(S2)) > decide[r]
+        assert pick[r] > max(pass2[(r, m)] for m in range(S2))
 
 
 def test_early_exit_off_when_no_second_group(driver):
