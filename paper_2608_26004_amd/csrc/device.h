@@ -451,6 +451,43 @@ DEV double dpp_d0(double x) {
   const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, ROWMASK, 0xF, false);
   return __builtin_bit_cast(double, (uint64_t)(uint32_t)lo | ((uint64_t)(uint32_t)hi << 32));
 }
+// Reductions over the 16 lanes of each DPP row (lanes 16r .. 16r + 15),
+// the result in every lane of the row: rotations by 8, 4, 2 and 1 lanes
+// within the row.
+template <int N>
+DEV int ror16_i(int x) { return __builtin_amdgcn_update_dpp(x, x, 0x120 + N, 0xF, 0xF, false); }
+template <int N>
+DEV double ror16_d(double x) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, x);
+  const uint32_t lo = (uint32_t)ror16_i<N>((int)(uint32_t)b);
+  const uint32_t hi = (uint32_t)ror16_i<N>((int)(uint32_t)(b >> 32));
+  return __builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32));
+}
+DEV float row16_max(float x) {
+  x = fmaxf(x, __int_as_float(ror16_i<8>(__float_as_int(x))));
+  x = fmaxf(x, __int_as_float(ror16_i<4>(__float_as_int(x))));
+  x = fmaxf(x, __int_as_float(ror16_i<2>(__float_as_int(x))));
+  return fmaxf(x, __int_as_float(ror16_i<1>(__float_as_int(x))));
+}
+DEV int row16_min(int x) {
+  x = min(x, ror16_i<8>(x));
+  x = min(x, ror16_i<4>(x));
+  x = min(x, ror16_i<2>(x));
+  return min(x, ror16_i<1>(x));
+}
+DEV int row16_or(int x) {
+  x |= ror16_i<8>(x);
+  x |= ror16_i<4>(x);
+  x |= ror16_i<2>(x);
+  return x | ror16_i<1>(x);
+}
+DEV double row16_sum(double x) {
+  x += ror16_d<8>(x);
+  x += ror16_d<4>(x);
+  x += ror16_d<2>(x);
+  return x + ror16_d<1>(x);
+}
+
 // An fp64 value of one lane, in every lane.
 DEV double readlane_d(double x, int lane) {
   const uint64_t b = __builtin_bit_cast(uint64_t, x);

@@ -183,22 +183,25 @@ DEV void classify_row(const KArgs& A, const RowGeo& g, const Gather& gq, float M
 // without pass 2).  Rows from nread on (early exit: they follow a sure
 // rejection and were not read) get placeholder blocks.  Thread (i, ch) of a
 // group of rows takes record ch of row i, so all records arrive in one round
-// trip; the row's maxima, sums, argmax and a-vs-b flag are combined through
-// LDS in chunk order and the row's first thread classifies it.  Whole
+// trip; the row's maxima, sums, argmax and a-vs-b flag are combined (for
+// S <= 16 within the 16 lanes of a DPP row given to each row, else through
+// LDS in chunk order) and the row's first thread classifies it.  Whole
 // workgroup; S must not exceed kThreads.
 template <int DT>
 DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
   const int lane = lane_id(), w = wave_id(), tid = w * 64 + lane;
   const int K = A.K, S = A.S, nrow = K + 1;
-  const int rpg = kThreads / S;                 // rows per group
-  const int li = tid / S, ch = tid - li * S;
+  const bool dpp = S <= 16;                     // a row's chunks in one DPP row
+  const int stride = dpp ? 16 : S;              // lanes per row
+  const int rpg = kThreads / stride;            // rows per group
+  const int li = tid / stride, ch = tid - li * stride;
   // the last statistics item read in list order is about the last to
   // finish: a waiting workgroup polls its record only
   const uint64_t* sentinel = A.rec1 + (((size_t)req * nrow + (nread - 1)) * S + (S - 1)) * kR1 + R1_MARG;
   bool all_in = true;
   for (int r0 = 0; r0 < nread; r0 += rpg) {
     const int nr = min(rpg, nread - r0);
-    const bool have = li < nr;
+    const bool have = li < nr && ch < S;
     const int i = r0 + (have ? li : 0);
     // first requests: the records, the draft token and its logits (row
     // leaders), then the temperature; none waits for another but the
@@ -227,6 +230,27 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
       }
       return ok;
     }) && all_in;
+    if (dpp) {
+      // the row's lanes: maxima, then the rescaled sums (fp64), the argmax
+      // among the chunks holding the maximum, and the a-vs-b flag; lanes
+      // without a chunk contribute nothing
+      float Rr[kSlots];
+      #pragma unroll
+      for (int s = 0; s < kSlots; ++s) Rr[s] = row16_max(have ? payf(r[R1_R + s]) : kFloorM);
+      const float Marg = row16_max(have ? payf(r[R1_MARG]) : kFloorM);
+      double Sp[kSlots];
+      #pragma unroll
+      for (int s = 0; s < kSlots; ++s)
+        Sp[s] = row16_sum(have ? (double)(payf(r[R1_S + s]) * __builtin_amdgcn_exp2f(payf(r[R1_R + s]) - Rr[s]))
+                               : 0.0);
+      const double Wkl =
+          row16_sum(have ? (double)(payf(r[R1_W]) * __builtin_amdgcn_exp2f(payf(r[R1_R + sA]) - Rr[sA])) : 0.0);
+      const int arg = row16_min(have && payf(r[R1_MARG]) == Marg ? (int)pay(r[R1_ARG]) : 0x7FFFFFFF);
+      const int nq = row16_or(have ? (int)pay(r[R1_NEQ]) : 0);
+      if (have && ch == 0) classify_row<DT>(A, g, gq, Marg, Rr, Sp, Wkl, arg, nq != 0, sm.rows[i]);
+      __syncthreads();
+      continue;
+    }
     // row references and the argmax slot's row maximum: every thread of the
     // row reads the row's records from LDS
     if (have) {
