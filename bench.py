@@ -176,6 +176,45 @@ COPY_BYTES = 1 << 30
 
 
 # ------------------------------------------------------------------- main --
+def clock_series(step, n, dev, every=20):
+    """n calls of step(i) after 2 s of idle, with the core clock sampled every
+    `every` calls by the clock probe enqueued between calls; per window of
+    `every` calls: the clock (MHz) and the mean and minimum call time (us,
+    HIP events)."""
+    import ctypes
+    import torch
+    from paper_2608_26004_amd import probe
+    torch.cuda.synchronize()
+    time.sleep(2.0)
+    nb = 64
+    nprobe = (n + every - 1) // every
+    cbuf = torch.zeros(nprobe * 2 * nb, dtype=torch.int32, device=dev)
+    lib = probe.load_library()
+    stream = torch.cuda.current_stream(dev)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for i in range(n):
+        if i % every == 0:
+            st = lib.asymspec_probe_clock(ctypes.c_void_p(cbuf.data_ptr() + (i // every) * 2 * nb * 4), nb, 500,
+                                          ctypes.c_void_p(stream.cuda_stream))
+            if st != 0:
+                raise RuntimeError(f"asymspec_probe_clock failed with status {st}")
+        ev[i][0].record(stream)
+        step(i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    per = np.array([a.elapsed_time(b) for a, b in ev]) * 1e3
+    w = cbuf.cpu().numpy().view(np.uint32).astype(np.float64).reshape(nprobe, nb, 2)
+    mhz = (100.0 * w[:, :, 0] / np.maximum(w[:, :, 1], 1.0)).mean(axis=1)
+    out = []
+    for j in range(nprobe):
+        seg = per[j * every:(j + 1) * every]
+        out.append({"calls": [j * every, j * every + len(seg) - 1], "MHz": round(float(mhz[j]), 1),
+                    "us_mean": round(float(seg.mean()), 1), "us_min": round(float(seg.min()), 1)})
+        print(f"[bench] calls {j * every:5d}-{j * every + len(seg) - 1:5d}: clock {mhz[j]:7.1f} MHz, "
+              f"call {seg.mean():6.1f} us (min {seg.min():6.1f})", file=sys.stderr, flush=True)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -219,6 +258,10 @@ def main():
                          "past the 256 MB Infinity Cache")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the read-ceiling probe (plain read-reduce over 2 GiB)")
+    ap.add_argument("--clock-series", type=int, default=0, metavar="N",
+                    help="after everything else, 2 s idle and then N more calls with the core clock "
+                         "sampled every 20 calls (clock probe enqueued between calls): how the clock "
+                         "and the call time move after a load step; reported as clock_series")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "runs on one GPU only: the step shards by request with no "
@@ -353,6 +396,10 @@ def main():
         print(f"[bench] read ceiling {ceiling['GBps']:.0f} GB/s over {ceiling['bytes']} B "
               f"({ceiling['nblocks']} workgroups)", file=sys.stderr, flush=True)
 
+    series = None
+    if args.clock_series > 0:
+        series = clock_series(step, args.clock_series, dev)
+
     acc = outs[0].cpu().numpy()
     if args.early_exit and args.early_exit <= K:
         # bytes actually read: requests with a sure rejection in their first
@@ -411,6 +458,8 @@ def main():
         "clock_MHz": {k: round(v["mean"], 1) for k, v in clocks.items()},
         "timeouts": n_timeouts,
     }
+    if series is not None:
+        res["clock_series"] = series
     if args.steps <= 64:
         # launch times in call order (HIP events), to see warm-up effects
         res["per_call_ms"] = [round(float(v), 5) for v in per]

@@ -249,7 +249,7 @@ int asymspec_fuse_verify_xvocab(const void* verifier_logits,
                                 void* stream);
 
 /* ---- the same step without a caller workspace ------------------------- */
-#define ASYMSPEC_NOALLOC_MAX_WORKSPACE (32u << 20)  /* bytes of static scratch per device */
+#define ASYMSPEC_NOALLOC_MAX_WORKSPACE (48u << 20)  /* bytes of static scratch per device */
 
 /*
  * For callers that cannot allocate (code under HIP graph capture, tight

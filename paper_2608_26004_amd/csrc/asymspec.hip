@@ -431,11 +431,12 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   // lags scale with the number of workgroups the chip holds at once
   const int ee_rows = ee ? (params->early_rows > 0 ? params->early_rows : 2) : 0;
   const int in_flight = vmap != nullptr ? di->max_blocks_xv[dtype] : di->max_blocks[dtype];
-  // pass 2 in 4 or 2 items per chunk while that many still fit on the chip
-  // at once: a small batch leaves most of it idle, and pass 2's divergence
-  // terms are arithmetic-bound within one workgroup
+  // pass 2 in 8, 4 or 2 items per chunk while that many still fit on the
+  // chip at once: a small batch leaves most of it idle, and pass 2's
+  // divergence terms are arithmetic-bound within one workgroup
   const long long p2_items = (long long)B * L.S;
-  A.P2 = p2_items * 4 <= in_flight ? 4 : (p2_items * 2 <= in_flight ? 2 : 1);
+  A.P2 = 1;
+  while (A.P2 < kMaxP2 && p2_items * 2 * A.P2 <= in_flight) A.P2 *= 2;
   if (!sched_build(B, K, L.S, in_flight, A.sc, ee_rows, A.P2)) return ASYMSPEC_E_ARG;
   const int grid = A.sc.total;
 

@@ -110,11 +110,12 @@ enum { kTaskJsd = 1, kTaskRes = 2, kTaskBonus = 4 };
 // kStSkip: a row after a sure rejection that early exit did not read.
 enum { kStDecided = 1, kStAccept = 2, kStDraft = 4, kStNeq = 8, kStSkip = 16 };
 
-// Pass 2 splits each chunk into P2 in {1, 2, 4} contiguous parts, one item
-// each.  Pass-2 record of one (request, row, chunk): the JSD partial of each
+// Pass 2 splits each chunk into P2 in {1, 2, 4, 8} contiguous parts, one
+// item each.  Pass-2 record of one (request, row, chunk): the JSD partial of each
 // part (fp32, in log2 units) and the weight sums of the chunk's sub-blocks
 // (fp32, in vocabulary order), one slot each.
-constexpr int kMaxP2 = 4;
+constexpr int kMaxP2 = 8;
+static_assert(kSegPerLane % kMaxP2 == 0, "a pass-2 part must give each lane whole vectors");
 enum { P2_J = 0, P2_SEG = kMaxP2, P2_USED = P2_SEG + kSubPerChunk, kR2 = P2_USED };
 
 struct KArgs {

@@ -509,8 +509,8 @@ DEV uint32_t load_decision(const KArgs& A, int req, Smem& sm) {
 // Pass-2 sums of one thread over its nk vectors (64 apart) of a chunk part;
 // the weight sum of vector k goes to seg[k].
 // kMode 0: interior part (no masking); 1: masked, branch-free; 2: generic
-// (one vector at a time, array-end repair).  kGF vectors per group (4, or 2
-// when a lane has only 2).
+// (one vector at a time, array-end repair).  kGF vectors per group (4, or
+// fewer when a lane has fewer).
 // kNb: a and b differ somewhere in the row; otherwise b is a bitwise copy of
 // a and a's vectors stand in for it (such a row has no divergence task).
 template <int DT, int kMode, int DM, bool kNb, bool kResOnly = false, int kGF = 4>
@@ -637,9 +637,12 @@ DEV void pass2_item(const KArgs& A, int req, int sub, Smem& sm) {
       if (nk >= 4) {
         if (nbr) pass2_sums_any<DT, DM, true, 4>(A, g, rel0, nk, c0, c1, dj, dr, db, rk, jk, accj, seg);
         else pass2_sums_any<DT, DM, false, 4>(A, g, rel0, nk, c0, c1, dj, dr, db, rk, jk, accj, seg);
-      } else {
+      } else if (nk >= 2) {
         if (nbr) pass2_sums_any<DT, DM, true, 2>(A, g, rel0, nk, c0, c1, dj, dr, db, rk, jk, accj, seg);
         else pass2_sums_any<DT, DM, false, 2>(A, g, rel0, nk, c0, c1, dj, dr, db, rk, jk, accj, seg);
+      } else {
+        if (nbr) pass2_sums_any<DT, DM, true, 1>(A, g, rel0, nk, c0, c1, dj, dr, db, rk, jk, accj, seg);
+        else pass2_sums_any<DT, DM, false, 1>(A, g, rel0, nk, c0, c1, dj, dr, db, rk, jk, accj, seg);
       }
     }
     // this wave's sub-block sums: lane k < nk publishes the wave's k-th
