@@ -9,10 +9,10 @@
 //         rejection, so only the open drafts before the first sure rejection
 //         and the rows that can emit need a second look at the logits.  A
 //         greedy request with nothing open is finished here.
-// pass 2  one chunk of every row that needs it: the JSD partial of Eq. 3 and
-//         the four wave-segment sums of the residual max(0, p~ - q) (sampling
-//         drafts that can emit, and a fused bonus row) or of the bonus
-//         weights of softmax(t_K / tau).
+// pass 2  one chunk (or one of P2 parts of it) of every row that needs it:
+//         the JSD partial of Eq. 3 and the sums over each 64-vector sub-block
+//         of the residual max(0, p~ - q) (sampling drafts that can emit, and
+//         a fused bonus row) or of the bonus weights of softmax(t_K / tau).
 // pick    D for the open drafts, the final accept length, and the emitted
 //         token: the fused argmax (greedy, Eq. 2) or an inverse-CDF draw with
 //         the caller's uniform u_K; then every output of the request.
@@ -882,7 +882,7 @@ DEV void pick_item(const KArgs& A, int req, Smem& sm) {
   }
   bool ok = true;   // this thread's waits all ended in time
   const bool samp = sm.req[R_SAMP] != 0u;
-  // requested now, used after the segment sums arrive
+  // requested now, used after the sub-block sums arrive
   const float uK = samp ? A.u[(size_t)req * (K + 1) + K] : 0.0f;
   // D of each row with a JSD task, the rows dealt out over the waves (the
   // k-th such row to wave k mod 4, its chunk partials over the lanes)
