@@ -260,7 +260,7 @@ int asymspec_fuse_verify_xvocab(const void* verifier_logits,
  * allocated or freed by this call.
  *   - Shapes whose asymspec_workspace_size exceeds the array return
  *     ASYMSPEC_E_WORKSPACE with nothing enqueued (B = 512, K = 8, V = 256000
- *     bf16 needs 16.6 MiB and fits).
+ *     bf16 needs 32.4 MiB and fits).
  *   - Every call on one device uses that device's array: calls that may
  *     overlap on one device (other streams, other host threads) race and
  *     must not be issued; calls in one stream are ordered and safe.
