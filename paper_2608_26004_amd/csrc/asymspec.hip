@@ -437,6 +437,12 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   const long long p2_items = (long long)B * L.S;
   A.P2 = 1;
   while (A.P2 < kMaxP2 && p2_items * 2 * A.P2 <= in_flight) A.P2 *= 2;
+  // with the gate output and a JSD-based gate, pass 2 sums the divergence of
+  // every draft row whose views differ, not only of the open ones: at least
+  // two parts per chunk then shorten the last requests' pass 2
+  if (A.want_gate && params->gate_mode != ASYMSPEC_GATE_KL && params->gate_mode != ASYMSPEC_GATE_LAMBDA &&
+      A.P2 < 2)
+    A.P2 = 2;
   if (!sched_build(B, K, L.S, in_flight, A.sc, ee_rows, A.P2)) return ASYMSPEC_E_ARG;
   const int grid = A.sc.total;
 
