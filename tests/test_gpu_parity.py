@@ -42,13 +42,15 @@ def test_small_mixed(gpu, dtype, tau):
 def test_pass2_parts(gpu, B):
     """Pass 2 runs in 8, 4, 2 or 1 items per chunk depending on how many fit
     on the chip (B x 8 chunks of V = 120000: 4, 2 and 1 parts here, 8 in the
-    small cases), each publishing its own partials; the emission draws and
-    the divergence must not depend on the split."""
+    small cases; at least 2 when the gate output is asked for under a
+    JSD-based gate), each publishing its own partials; the emission draws
+    and the divergence must not depend on the split."""
     x = synth.generate(B=B, K=2, V=120000, dtype="bf16", rho=("uniform", 0.0, 2.0),
                        tau=("alternate", 0.0, 1.0), seed=700 + B)
     for mode in (0, 1):
-        g = run_gpu(x, gate_mode=mode)
-        _note(compare(x, g, gate_mode=mode, label=f"pass-2 parts B={B} mode={mode}"))
+        for want_gate in (True, False):
+            g = run_gpu(x, gate_mode=mode, want_gate=want_gate)
+            _note(compare(x, g, gate_mode=mode, label=f"pass-2 parts B={B} mode={mode} gate={want_gate}"))
 
 
 @pytest.mark.parametrize("V", [1, 2, 3, 5, 8, 4095, 4097, 8193, 32000])
