@@ -53,6 +53,36 @@ def test_pass2_parts(gpu, B):
             _note(compare(x, g, gate_mode=mode, label=f"pass-2 parts B={B} mode={mode} gate={want_gate}"))
 
 
+def test_argmax_ties_across_waves_and_chunks(gpu):
+    """Greedy rows whose fused maximum is attained twice, in the runs of two
+    waves of one statistics item and in two chunks: the first index wins
+    (Eq. 2), whatever the order in which the partials are combined.  a = b,
+    so f = t exactly and the tie is exact in every precision."""
+    B, K, V = 2, 1, 20000             # bf16: 2 chunks of 16384 tokens
+    x = synth.generate(B=B, K=K, V=V, dtype="bf16", rho=("uniform", 0.0, 1.0), tau=0.0, seed=77)
+    def bf(v):
+        return np.uint16(np.float32(v).view(np.uint32) >> 16)
+    x.b[:] = x.a
+    # the max of t at two tokens per request: 1500 (wave 0's run of chunk 0)
+    # and 4500 (wave 1's); 16000 (chunk 0) and 16390 (chunk 1)
+    ties = {0: (1500, 4500), 1: (16000, 16390)}
+    for r, (i1, i2) in ties.items():
+        x.t[r, :, i1] = bf(100.0)
+        x.t[r, :, i2] = bf(100.0)
+        d = int(x.draft_tokens[r, 0])
+        if d in (i1, i2):
+            d = (d + 7) % V
+            x.draft_tokens[r, 0] = d
+        # a sure rejection of draft 0: low verifier, high drafter logit
+        x.t[r, 0, d] = bf(-4.0)
+        x.a[r, 0, d] = x.b[r, 0, d] = bf(4.0)
+    g = run_gpu(x)
+    r = compare(x, g, label="argmax ties across waves and chunks")
+    assert not r["near_ties"] or all(t[2] == t[4] for t in r["near_ties"])
+    for req, (i1, _) in ties.items():
+        assert int(g[0][req]) == 0 and int(g[1][req]) == i1
+
+
 @pytest.mark.parametrize("V", [1, 2, 3, 5, 8, 4095, 4097, 8193, 32000])
 @pytest.mark.parametrize("K", [0, 1, 4])
 def test_edge_shapes(gpu, V, K):
