@@ -443,6 +443,11 @@ static int fuse_verify_impl(const void* t, const void* a, const void* b, int dty
   if (A.want_gate && params->gate_mode != ASYMSPEC_GATE_KL && params->gate_mode != ASYMSPEC_GATE_LAMBDA &&
       A.P2 < 2)
     A.P2 = 2;
+  // a launch whose statistics items fit the chip at most four times over
+  // polls every slot it waits for (measured: 0.5-0.8 us less per call
+  // there; on larger launches it saves nothing and its polling traffic
+  // costs a little)
+  A.full_poll = (long long)B * (K + 1) * L.S <= 4LL * in_flight ? 1 : 0;
   if (!sched_build(B, K, L.S, in_flight, A.sc, ee_rows, A.P2)) return ASYMSPEC_E_ARG;
   const int grid = A.sc.total;
 

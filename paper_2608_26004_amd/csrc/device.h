@@ -127,6 +127,7 @@ struct KArgs {
   unsigned long long stream_bytes;   // bytes of each logit array
   int B, K, V, S;
   int P2;             // pass-2 items per chunk
+  int full_poll;      // waits poll every slot they need, not a sentinel
   float beta, gamma; int gate_mode; int want_gate;
   int delta_mode;     // source of delta in f = t + beta * delta
   int fuse_bonus;     // the bonus row emits from f rather than t
@@ -254,12 +255,14 @@ DEV bool wait_one(const uint64_t* p, const KArgs& A) {
 // this thread's share all carry the launch epoch.  When the first attempt
 // misses, the workgroup polls only the slot `sentinel` (written about last)
 // until it is in, so that a waiting workgroup adds little traffic, and then
-// loads until every share is in (bounded).  False (in every thread) when a
-// wait timed out: the loaded values are then not this launch's.
+// loads until every share is in (bounded).  In a launch small enough that
+// the traffic does not matter (A.full_poll) every share is polled on each
+// round instead, which saves that last round trip.  False (in every thread)
+// when a wait timed out: the loaded values are then not this launch's.
 template <class F>
 DEV bool load_tagged(const KArgs& A, const uint64_t* sentinel, F&& load) {
   if (__syncthreads_and(load())) return true;
-  if (!wait_one(sentinel, A)) return false;
+  if (!A.full_poll && !wait_one(sentinel, A)) return false;
   BlockPoll bp;
   while (!bp.done(load(), A)) {
   }

@@ -222,10 +222,12 @@ DEV void decide_request(const KArgs& A, int req, Smem& sm, int nread) {
         for (int j = 0; j < R1_USED; ++j) ok = ok && tag_ok(r[j], A.epoch);
         return ok;
       }
+      // a slot that carries the epoch is final: only the others are read
+      // again
       bool ok = true;
       #pragma unroll
       for (int j = 0; j < R1_USED; ++j) {
-        r[j] = have ? ld_tag(base + j) : ((uint64_t)A.epoch << 32);
+        if (have && !tag_ok(r[j], A.epoch)) r[j] = ld_tag(base + j);
         ok = ok && tag_ok(r[j], A.epoch);
       }
       return ok;
