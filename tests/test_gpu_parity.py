@@ -668,15 +668,18 @@ def test_xvocab_drafter_vocabulary_longer(gpu, dtype):
 
 
 # ------------------------------------------------------ the error path --
-def test_timed_out_waits_mark_requests_invalid(gpu):
+@pytest.mark.parametrize("B,K,V", [(24, 3, 20000), (288, 3, 60000)])
+def test_timed_out_waits_mark_requests_invalid(gpu, B, K, V):
     """A wait bound of a few 10 ns ticks (set from the host) makes waits
     between workgroups run out under normal operation: the workspace counts
     them, and every request either carries accept_len = -1 or the oracle's
-    outputs; with the default bound restored the same call is whole."""
+    outputs; with the default bound restored the same call is whole.  The
+    small launch polls every slot it waits for, the large one (4608
+    statistics items) a sentinel slot first."""
     import paper_2608_26004_amd as asp
     import torch
     from parity_util import to_device
-    x = synth.generate(B=24, K=3, V=20000, dtype="bf16", rho=("uniform", 0.0, 2.0),
+    x = synth.generate(B=B, K=K, V=V, dtype="bf16", rho=("uniform", 0.0, 2.0),
                        tau=("alternate", 0.0, 1.0), seed=4242)
     args = [to_device(v) for v in (x.t, x.a, x.b, x.draft_tokens, x.draft_probs, x.uniforms,
                                    x.temperature)]
