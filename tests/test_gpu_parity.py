@@ -668,6 +668,20 @@ def test_xvocab_drafter_vocabulary_longer(gpu, dtype):
 
 
 # ------------------------------------------------------ the error path --
+@pytest.mark.parametrize("B", [256, 257])
+def test_polling_modes_at_the_boundary(gpu, B):
+    """A launch of at most 4096 statistics items (4 per CU slot of the
+    256-CU part) polls every slot it waits for, a larger one a sentinel slot
+    first; B = 256 and 257 requests of 4 rows x 4 chunks sit on either side
+    of that boundary, and both agree with the oracle."""
+    x = synth.generate(B=B, K=3, V=60000, dtype="bf16", rho=("uniform", 0.0, 2.0),
+                       tau=("alternate", 0.0, 1.0), seed=5150 + B)
+    g = run_gpu(x)
+    r = compare(x, g, label=f"polling boundary B={B}")
+    _note(r)
+    assert len(r["near_ties"]) <= near_tie_budget(x.B * (x.K + 1))
+
+
 @pytest.mark.parametrize("B,K,V", [(24, 3, 20000), (288, 3, 60000)])
 def test_timed_out_waits_mark_requests_invalid(gpu, B, K, V):
     """A wait bound of a few 10 ns ticks (set from the host) makes waits
